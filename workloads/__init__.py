@@ -1,0 +1,36 @@
+"""Seeded synthetic workloads shared by the GPU path and the CPU oracle.
+
+This package only describes shapes and draws random inputs.  It holds none
+of the method's arithmetic: no normalisation, projection, attention,
+scoring, selection or slot mapping lives here.
+"""
+
+from .configs import CONFIGS, ModelDims, SeqLayout, Workload, get_config
+from .gen import (
+    LayerWeightsBits,
+    bf16_bits_from_f32,
+    draw_embedding,
+    draw_hidden_rows,
+    draw_layer_weights,
+    draw_noise,
+    draw_scores,
+    draw_token_ids,
+    rng_for,
+)
+
+__all__ = [
+    "CONFIGS",
+    "ModelDims",
+    "SeqLayout",
+    "Workload",
+    "get_config",
+    "LayerWeightsBits",
+    "bf16_bits_from_f32",
+    "draw_embedding",
+    "draw_hidden_rows",
+    "draw_layer_weights",
+    "draw_noise",
+    "draw_scores",
+    "draw_token_ids",
+    "rng_for",
+]

@@ -1,0 +1,136 @@
+"""Workload shapes for the selective affix-KV recompute path.
+
+Five synthetic workloads stand in for the paper's few-shot prompts (its
+datasets and trained weights are not available): a tiny fp32 layer, one
+LLaDA-8B-shaped bf16 layer, a 32-layer LLaDA-shaped stack, a 28-layer
+Dream-7B-shaped GQA stack with an infix affix, and a serving-scale LLaDA
+stack.  Generation length 256 and block length 32 follow the paper's
+default settings (Section 5, "Default Settings"); affix lengths are chosen
+per workload because the paper does not report token counts.
+
+The anchor count is K = floor(rho * L + 1/2), clamped to [0, L].
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field, replace
+from typing import Dict, Tuple
+
+
+@dataclass(frozen=True)
+class ModelDims:
+    d_model: int
+    n_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_ff: int
+    n_layers: int
+    dtype: str  # "f32" or "bf16": storage type of weights, activations and KV
+    rms_eps: float = 1e-5
+    rope_base: float = 10000.0
+    vocab: int = 0  # 0: layer-0 inputs are given hidden rows, not token ids
+
+    @property
+    def qkv_width(self) -> int:
+        return (self.n_heads + 2 * self.n_kv_heads) * self.head_dim
+
+
+@dataclass(frozen=True)
+class SeqLayout:
+    """Logical positions of one request: a shared affix span, a masked
+    generation span, and unique (request-specific, unmasked) positions for
+    the rest.  Positions are 0-based and identical for every request."""
+
+    seq_len: int
+    affix_begin: int
+    affix_len: int
+    mask_begin: int
+    mask_len: int
+
+    @property
+    def affix_end(self) -> int:
+        return self.affix_begin + self.affix_len
+
+    @property
+    def n_nonaffix(self) -> int:
+        return self.seq_len - self.affix_len
+
+    def affix_positions(self):
+        return list(range(self.affix_begin, self.affix_end))
+
+    def masked_positions(self):
+        return list(range(self.mask_begin, self.mask_begin + self.mask_len))
+
+    def nonaffix_positions(self):
+        return [p for p in range(self.seq_len) if not (self.affix_begin <= p < self.affix_end)]
+
+
+def anchor_count(ratio: float, affix_len: int) -> int:
+    k = int(ratio * affix_len + 0.5)
+    return max(0, min(affix_len, k))
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    seed_id: int
+    dims: ModelDims
+    layout: SeqLayout
+    batch: int
+    ratio: float
+    stale: str  # "perturb": stale KV from affix inputs + N(0, 0.1^2); "donor": from a donor request
+    mask_rows: str = "random"  # "random": N(0,1) per masked row; "shared": one mask vector
+    ratios: Tuple[float, ...] = field(default=())
+
+    @property
+    def n_anchors(self) -> int:
+        return anchor_count(self.ratio, self.layout.affix_len)
+
+    @property
+    def rows_selective(self) -> int:
+        return self.n_anchors + self.layout.n_nonaffix
+
+    def with_ratio(self, ratio: float) -> "Workload":
+        return replace(self, ratio=ratio)
+
+
+LLADA = dict(d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128, d_ff=12288)
+DREAM = dict(d_model=3584, n_heads=28, n_kv_heads=4, head_dim=128, d_ff=18944)
+
+CONFIGS: Dict[str, Workload] = {
+    # one fp32 layer: 128 affix + 32 unique + 32 masked (one shared mask vector)
+    "tiny-f32": Workload(
+        name="tiny-f32", seed_id=1,
+        dims=ModelDims(d_model=256, n_heads=4, n_kv_heads=4, head_dim=64, d_ff=688,
+                       n_layers=1, dtype="f32"),
+        layout=SeqLayout(seq_len=192, affix_begin=0, affix_len=128, mask_begin=160, mask_len=32),
+        batch=1, ratio=0.2, stale="perturb", mask_rows="shared"),
+    # one LLaDA-8B-shaped bf16 layer: 1024 affix + 256 unique + 256 masked, N(0,1) rows
+    "llada-layer": Workload(
+        name="llada-layer", seed_id=2,
+        dims=ModelDims(n_layers=1, dtype="bf16", **LLADA),
+        layout=SeqLayout(seq_len=1536, affix_begin=0, affix_len=1024, mask_begin=1280, mask_len=256),
+        batch=1, ratio=0.2, stale="perturb"),
+    # 32-layer LLaDA-shaped stack, 8 requests share a 2048-token prefix affix
+    "llada-stack-b8": Workload(
+        name="llada-stack-b8", seed_id=3,
+        dims=ModelDims(n_layers=32, dtype="bf16", vocab=126464, **LLADA),
+        layout=SeqLayout(seq_len=2432, affix_begin=0, affix_len=2048, mask_begin=2176, mask_len=256),
+        batch=8, ratio=0.2, stale="donor"),
+    # 28-layer Dream-shaped GQA stack, infix affix between two unique spans
+    "dream-stack-b4": Workload(
+        name="dream-stack-b4", seed_id=4,
+        dims=ModelDims(n_layers=28, dtype="bf16", vocab=126464, **DREAM),
+        layout=SeqLayout(seq_len=5120, affix_begin=512, affix_len=4096, mask_begin=4864, mask_len=256),
+        batch=4, ratio=0.2, stale="donor", ratios=(0.1, 0.2, 0.4)),
+    # serving-scale LLaDA stack: 32 requests share an 8192-token prefix affix
+    "llada-serve-b32": Workload(
+        name="llada-serve-b32", seed_id=5,
+        dims=ModelDims(n_layers=32, dtype="bf16", vocab=126464, **LLADA),
+        layout=SeqLayout(seq_len=8704, affix_begin=0, affix_len=8192, mask_begin=8448, mask_len=256),
+        batch=32, ratio=0.2, stale="donor"),
+}
+
+
+def get_config(name: str) -> Workload:
+    return CONFIGS[name]
