@@ -1,0 +1,262 @@
+/*
+ * acache.h — C ABI of the selective affix-KV recompute path for MI355X (gfx950).
+ *
+ * The operation is ACache's ("Affix Cache for Diffusion Large Language
+ * Models"): a shared affix keeps one precomputed KV cache; each request picks
+ * Anchor Tokens once by a probe that scores affix tokens with the attention
+ * they receive from masked generation queries (Section 3.2, Eq. 4-6); at
+ * every recomputation point only the anchors and the request-specific
+ * positions are recomputed, while the other affix tokens keep the shared
+ * cache (Section 3.3).  Recomputed KV goes to request-private slots through a
+ * write-side map, and attention reads the full logical context through a
+ * read-slot map (Section 4.1, Appendix C.1).
+ *
+ * Conventions for every call:
+ *  - Pointers are DEVICE pointers unless marked [host].  Host arrays are read
+ *    during the call only.
+ *  - Ownership: the caller owns every buffer.  The library allocates and
+ *    frees no device memory, keeps no global state and never synchronises;
+ *    work is enqueued on `stream` and the call returns.  Buffers must stay
+ *    alive until the stream has passed the work.
+ *  - Errors: host-checkable faults (NULL pointers, sizes, alignment,
+ *    unsupported shapes, a workspace that is too small) return a non-zero
+ *    status and enqueue nothing.  A failed launch returns ACACHE_ERR_DEVICE.
+ *  - Device-resident indices (slots, rows, anchors) are checked on the
+ *    device against the sizes passed here: an out-of-range index is skipped
+ *    (its read yields zeros, its write is dropped), never dereferenced.
+ *  - Element types: ACACHE_BF16 is bfloat16 storage with fp32 accumulation;
+ *    ACACHE_F32 is fp32 throughout.  Weights, activations and KV pools share
+ *    the `dims->dtype` storage type; scores and log-sum-exp are fp32.
+ *  - Row-major layouts.  A KV pool is [n_slots, pool_ld] elements, one pool
+ *    per layer for K and one for V; the row of a slot holds H_kv heads of
+ *    head_dim elements (K after rotation).  Leading dimensions are in
+ *    elements unless named *_bytes.
+ *  - The fused block is the LLaDA / Dream family's: RMSNorm, Q/K/V
+ *    projections (no bias), rotary embedding on half-split pairs at the
+ *    row's position, bidirectional attention with grouped KV heads, output
+ *    projection + residual, RMSNorm, SwiGLU MLP + residual.
+ */
+#ifndef ACACHE_H
+#define ACACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ACACHE_OK = 0,
+  ACACHE_ERR_NULL = 1,        /* a required pointer is NULL */
+  ACACHE_ERR_SHAPE = 2,       /* sizes are negative, inconsistent or out of range */
+  ACACHE_ERR_ALIGN = 3,       /* a pointer or leading dimension is not 16-byte aligned */
+  ACACHE_ERR_UNSUPPORTED = 4, /* valid, but outside the shapes the kernels implement */
+  ACACHE_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than acache_workspace_size() */
+  ACACHE_ERR_DEVICE = 6       /* a HIP launch or call failed */
+} acache_status;
+
+typedef enum { ACACHE_F32 = 0, ACACHE_BF16 = 1 } acache_dtype;
+
+/* Normalisation of the Eq. 4 softmax.  AFFIX: over the affix keys only, as
+ * Eq. 4 is written.  FULL: the model's softmax over every key of the
+ * request, read through the per-row log-sum-exp the attention exports. */
+typedef enum { ACACHE_NORM_AFFIX = 0, ACACHE_NORM_FULL = 1 } acache_norm;
+
+typedef struct {
+  int32_t d_model;    /* hidden size d */
+  int32_t n_heads;    /* query heads H */
+  int32_t n_kv_heads; /* KV heads H_kv; H % H_kv == 0 (head h reads KV head h / (H / H_kv)) */
+  int32_t head_dim;   /* d_h */
+  int32_t d_ff;       /* SwiGLU width F */
+  float rms_eps;      /* RMSNorm epsilon */
+  float rope_base;    /* rotary base: theta_i = base^(-2i / d_h) */
+  acache_dtype dtype;
+} acache_dims;
+
+/* One layer's weights, [out_features, in_features] row-major, dims->dtype. */
+typedef struct {
+  const void* attn_norm; /* [d]                      RMSNorm gain before attention */
+  const void* w_qkv;     /* [(H + 2 H_kv) d_h, d]    rows: Q heads, K heads, V heads */
+  const void* w_o;       /* [d, H d_h] */
+  const void* mlp_norm;  /* [d]                      RMSNorm gain before the MLP */
+  const void* w_gate_up; /* [2 F, d]                 rows: F gate rows, then F up rows */
+  const void* w_down;    /* [d, F] */
+} acache_layer_weights;
+
+/* A ragged batch.  Request b owns rows [cu_rows[b], cu_rows[b+1]) of the
+ * row-indexed buffers and reads its logical keys through
+ * read_slots[cu_keys[b] .. cu_keys[b+1]).  batch <= 64. */
+typedef struct {
+  int32_t batch;
+  const int32_t* cu_rows; /* [host] batch + 1, nondecreasing, cu_rows[0] == 0 */
+  const int32_t* cu_keys; /* [host] batch + 1, nondecreasing, cu_keys[0] == 0 */
+} acache_ragged;
+
+/* Probe scoring inside acache_layer_recompute (Section 3.2, Eq. 4-5). */
+typedef struct {
+  const int32_t* q_rows;      /* [cu_q[batch]] rows (of this layer's rows) of the masked queries */
+  const int32_t* cu_q;        /* [host] batch + 1: request b's masked rows are q_rows[cu_q[b] ..) */
+  const int32_t* affix_slots; /* [affix_len] pool slots of the affix keys, affix-local order */
+  int32_t affix_len;          /* L */
+  acache_norm norm;
+  float* scores;              /* [batch, L] fp32, accumulated (+=) */
+} acache_score_args;
+
+/* Logical layout shared by every request of a batch, and its slot plan. */
+typedef struct {
+  int32_t seq_len;        /* S: logical positions per request, 0 .. S-1 */
+  int32_t affix_begin;    /* first position of the shared affix span */
+  int32_t affix_len;      /* L */
+  int32_t mask_begin;     /* first position of the masked generation span M_T */
+  int32_t mask_len;       /* G */
+  int32_t shared_base;    /* pool slot of affix-local index 0 (shared region) */
+  int32_t private_base;   /* first private slot */
+  int32_t private_stride; /* request b's private slots start at private_base + b * private_stride */
+} acache_layout;
+
+/* ---------------------------------------------------------------------------
+ * acache_score — Eq. 4-5 of Section 3.2 for one layer: for every request b,
+ * masked query row k (q_rows[cu_q[b] ..)), head h and affix key j,
+ *   a = softmax over the affix keys of q_k . K_j / sqrt(d_h)   (AFFIX), or
+ *   a = exp(q_k . K_j / sqrt(d_h) - row_lse[k, h])              (FULL),
+ * and scores[b, j] += sum over h and k of a.  Keys are k_pool[affix_slots[j]],
+ * KV head h / (H / H_kv).  The sum is taken in a fixed order (no float
+ * atomics): identical inputs give identical bits.
+ *   q        [rows, q_ld] post-rotation queries, head h at columns h*d_h
+ *   row_lse  [rows, H] natural-log log-sum-exp of the scaled logits over all
+ *            of the row's keys (as acache_attention exports); required for
+ *            FULL, must be NULL for AFFIX
+ *   ws       workspace of at least acache_workspace_size() bytes
+ * Requires head_dim == 128 (bf16) or head_dim <= 128 (f32); L <= 65536.
+ * L == 0 or no masked rows: no-op. */
+acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                           int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
+                           const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                           const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
+                           acache_norm norm, float* scores, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_topk — Eq. 6: per request b, the k indices j of the largest
+ * scores[b, j], written ascending to idx_out[b, 0..k).  Ties go to the lowest
+ * index; -0 equals +0; NaN ranks below every other value (-inf included).
+ * Exact: the selection compares order-preserving integer keys of the fp32
+ * bits.  0 <= k <= L <= 16384; k == 0 is a no-op. */
+acache_status acache_topk(const float* scores, int32_t batch, int32_t L, int32_t k,
+                          int32_t* idx_out, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_gather_rows — queries are formed only for recomputed positions
+ * (Section 4.3): dst row i = src row r, r = remap ? remap[idx[i]] : idx[i],
+ * for i < n.  Rows are row_bytes long (multiple of 16); src rows
+ * 0 .. src_rows-1 exist; remap has remap_len entries.  Pointers and
+ * leading dimensions 16-byte aligned.  n == 0: no-op. */
+acache_status acache_gather_rows(const void* src, int64_t src_ld_bytes, int64_t src_rows,
+                                 const int32_t* idx, const int32_t* remap, int64_t remap_len,
+                                 int32_t n, int32_t row_bytes, void* dst, int64_t dst_ld_bytes,
+                                 hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_kv_scatter — the store half of store-then-attend (Appendix C.1):
+ * k_pool[dst_slots[i]] = k_src row i and v_pool[dst_slots[i]] = v_src row i,
+ * row_elems elements each (multiple of 8), for i < n.  Sources are
+ * [n, src_ld]; pools [n_slots, pool_ld].  n == 0: no-op. */
+acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t src_ld, int32_t n,
+                                const int32_t* dst_slots, void* k_pool, void* v_pool,
+                                int64_t pool_ld, int64_t n_slots, int32_t row_elems,
+                                acache_dtype dtype, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_build_maps — the write-side recomputation map and the read-slot
+ * map of Section 4.1, built on the device from the anchor lists.  For
+ * request b the recomputed positions are every non-affix position plus
+ * affix_begin + anchors[b, i]; taken in ascending order they are rows
+ * b*R .. b*R + R-1 (R = k + S - L) and get private slots
+ * private_base + b*private_stride + (rank).  Outputs:
+ *   row_pos     [B*R]  logical position of each recomputed row
+ *   row_src     [B*R]  b*S + position (index into per-position inputs)
+ *   write_slots [B*R]  private slot of each recomputed row
+ *   read_slots  [B*S]  slot each logical position is read from: its
+ *                      private slot if recomputed, else shared_base + (p - affix_begin)
+ *   q_rows      [B*G]  (nullable) row of each masked position
+ * anchors [B, k] affix-local indices, ascending per request (NULL iff k == 0).
+ * k == 0 gives the probe / direct-reuse maps, k == L the full-recompute maps.
+ * Requires private_stride >= R. */
+acache_status acache_build_maps(const acache_layout* layout, int32_t batch,
+                                const int32_t* anchors, int32_t k, int32_t* row_pos,
+                                int32_t* row_src, int32_t* write_slots, int32_t* read_slots,
+                                int32_t* q_rows, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_attention — read-slot attention (Appendix C.1): for request b,
+ * head h and each query row r in [cu_rows[b], cu_rows[b+1]),
+ *   out[r, h] = softmax_j(q[r, h] . K_j / sqrt(d_h)) V_j
+ * over the request's logical keys j, K_j = k_pool[read_slots[cu_keys[b] + j]]
+ * (KV head h / (H / H_kv)), bidirectional, no mask.  q and out are
+ * [rows, H*d_h]; lse (nullable) [rows, H] receives the natural-log
+ * log-sum-exp of the scaled logits.  A request with rows must have keys. */
+acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg, const void* q,
+                               const int32_t* read_slots, const void* k_pool, const void* v_pool,
+                               int64_t pool_ld, int64_t n_slots, void* out, float* lse,
+                               hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_layer_recompute — one block over the recomputed rows of a ragged
+ * batch (Sections 3.3 and 4.3): with y = RMSNorm(x) the rows' Q, K, V are
+ * projected, rotated at pos[r], the fresh K/V stored at write_slots[r], and
+ * then attention reads every logical key through read_slots (store, then
+ * attend).  x is updated in place:
+ *   x += Attn(...) W_o^T;  x += (SiLU(y2 Wg^T) * (y2 Wu^T)) W_down^T,  y2 = RMSNorm(x).
+ * With `score` set (the probe of Section 3.2), this layer's Eq. 4-5
+ * contribution is added to score->scores from the masked rows' queries
+ * against the affix keys, as acache_score does.
+ *   x           [rows, d] in/out, rows = cu_rows[batch]
+ *   pos         [rows] logical position of each row (rotation angle)
+ *   write_slots [rows] pool slot receiving each row's K and V
+ *   read_slots  [cu_keys[batch]] slots of each request's logical keys
+ *   pools       [n_slots, pool_ld], pool_ld >= H_kv * d_h
+ *   ws          at least acache_workspace_size(dims, rows, batch, L) bytes
+ * bf16 requires head_dim == 128, d_model % 256 == 0, (H*d_h) % 256 == 0,
+ * (H_kv*d_h) % 128 == 0, d_ff % 128 == 0; f32 requires head_dim % 2 == 0,
+ * head_dim <= 128. */
+acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer_weights* w,
+                                     const acache_ragged* rg, void* x, const int32_t* pos,
+                                     const int32_t* write_slots, const int32_t* read_slots,
+                                     void* k_pool, void* v_pool, int64_t pool_ld, int64_t n_slots,
+                                     const acache_score_args* score, void* ws, size_t ws_bytes,
+                                     hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Building blocks of acache_layer_recompute, exported so each can be checked
+ * on its own.
+ *
+ * acache_rmsnorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g, rows x [rows, d].
+ * acache_linear:  c[m, n] = sum_k a[m, k] w[n, k] (+ c[m, n] when accumulate),
+ *                 a [M, K], w [N, K], c [M, N], dims->dtype storage, fp32
+ *                 accumulation.  bf16 requires K % 64 == 0, N % 256 == 0. */
+acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void* g, void* y,
+                             int32_t rows, hipStream_t stream);
+acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,
+                            int32_t M, int32_t N, int32_t K, int32_t accumulate,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by acache_layer_recompute, acache_score and
+ * acache_linear for up to max_rows rows, `batch` requests and affix length
+ * affix_len (0 when no scoring).  Returns 0 for invalid dims. */
+size_t acache_workspace_size(const acache_dims* dims, int32_t max_rows, int32_t batch,
+                             int32_t affix_len);
+
+/* A static English description of a status code. */
+const char* acache_status_string(acache_status status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int32_t acache_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACACHE_H */

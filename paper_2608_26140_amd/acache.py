@@ -1,0 +1,264 @@
+"""Python binding of libacache.so (ctypes).
+
+Argument marshalling only: every function here checks Python-side shapes
+and dtypes, passes raw device pointers and the current HIP stream to the C
+entry point of the same name, and raises AcacheError on a non-zero status.
+All computation runs in the library's HIP kernels.  Tensors are torch
+tensors used as device memory.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libacache.so")
+
+ACACHE_F32, ACACHE_BF16 = 0, 1
+ACACHE_NORM_AFFIX, ACACHE_NORM_FULL = 0, 1
+
+
+class AcacheError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: status {status}: {msg}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ff", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float), ("dtype", ctypes.c_int32)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
+class Ragged(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("cu_rows", ctypes.POINTER(ctypes.c_int32)),
+                ("cu_keys", ctypes.POINTER(ctypes.c_int32))]
+
+
+class ScoreArgs(ctypes.Structure):
+    _fields_ = [("q_rows", ctypes.c_void_p), ("cu_q", ctypes.POINTER(ctypes.c_int32)),
+                ("affix_slots", ctypes.c_void_p), ("affix_len", ctypes.c_int32), ("norm", ctypes.c_int32),
+                ("scores", ctypes.c_void_p)]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("seq_len", "affix_begin", "affix_len", "mask_begin", "mask_len",
+                                              "shared_base", "private_base", "private_stride")]
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2608_26140_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    PI = ctypes.POINTER(ctypes.c_int32)
+    sig = {
+        "acache_score": [ctypes.POINTER(Dims), I32, P, I64, I64, P, PI, P, I64, I64, P, I32, P, I32, P, P, SZ, P],
+        "acache_topk": [P, I32, I32, I32, P, P],
+        "acache_gather_rows": [P, I64, I64, P, P, I64, I32, I32, P, I64, P],
+        "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
+        "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
+        "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
+        "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
+                                   P, P, P, P, P, P, I64, I64, ctypes.POINTER(ScoreArgs), P, SZ, P],
+        "acache_rmsnorm": [ctypes.POINTER(Dims), P, P, P, I32, P],
+        "acache_linear": [ctypes.POINTER(Dims), P, P, P, I32, I32, I32, I32, P, SZ, P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int32
+    lib.acache_workspace_size.argtypes = [ctypes.POINTER(Dims), I32, I32, I32]
+    lib.acache_workspace_size.restype = ctypes.c_size_t
+    lib.acache_status_string.argtypes = [ctypes.c_int32]
+    lib.acache_status_string.restype = ctypes.c_char_p
+    lib.acache_version.restype = ctypes.c_int32
+    return lib
+
+
+lib = _load()
+LIB_PATH = _LIB_PATH
+
+
+def _check(name: str, st: int):
+    if st != 0:
+        raise AcacheError(name, st, lib.acache_status_string(st).decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _i32(values: Sequence[int]):
+    arr = (ctypes.c_int32 * len(values))(*[int(v) for v in values])
+    return arr
+
+
+def _dev_i32(t: torch.Tensor, name: str):
+    if t.dtype != torch.int32 or not t.is_cuda or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous int32 device tensor")
+
+
+def make_dims(d_model, n_heads, n_kv_heads, head_dim, d_ff, dtype: str, rms_eps=1e-5, rope_base=10000.0) -> Dims:
+    return Dims(d_model, n_heads, n_kv_heads, head_dim, d_ff, rms_eps, rope_base,
+                ACACHE_BF16 if dtype == "bf16" else ACACHE_F32)
+
+
+def torch_dtype(dims: Dims):
+    return torch.bfloat16 if dims.dtype == ACACHE_BF16 else torch.float32
+
+
+def acache_workspace_size(dims: Dims, max_rows: int, batch: int, affix_len: int) -> int:
+    n = lib.acache_workspace_size(ctypes.byref(dims), max_rows, batch, affix_len)
+    if n == 0:
+        raise AcacheError("acache_workspace_size", 2, "invalid dims")
+    return n
+
+
+def workspace(dims: Dims, max_rows: int, batch: int, affix_len: int, device="cuda") -> torch.Tensor:
+    return torch.empty(acache_workspace_size(dims, max_rows, batch, affix_len), dtype=torch.uint8, device=device)
+
+
+def acache_topk(scores: torch.Tensor, k: int, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    if scores.dtype != torch.float32 or scores.dim() != 2 or not scores.is_contiguous():
+        raise TypeError("scores must be a contiguous float32 [batch, L] tensor")
+    b, L = scores.shape
+    if out is None:
+        out = torch.empty((b, k), dtype=torch.int32, device=scores.device)
+    _check("acache_topk", lib.acache_topk(_ptr(scores), b, L, k, _ptr(out), _stream(stream)))
+    return out
+
+
+def acache_gather_rows(src: torch.Tensor, idx: torch.Tensor, remap: Optional[torch.Tensor] = None,
+                       out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _dev_i32(idx, "idx")
+    if remap is not None:
+        _dev_i32(remap, "remap")
+    src2 = src.reshape(src.shape[0], -1)
+    n = idx.numel()
+    if out is None:
+        out = torch.empty((n,) + tuple(src.shape[1:]), dtype=src.dtype, device=src.device)
+    row_bytes = src2.shape[1] * src2.element_size()
+    _check("acache_gather_rows", lib.acache_gather_rows(
+        _ptr(src2), src2.stride(0) * src2.element_size(), src2.shape[0], _ptr(idx), _ptr(remap),
+        0 if remap is None else remap.numel(), n, row_bytes, _ptr(out), row_bytes, _stream(stream)))
+    return out
+
+
+def acache_kv_scatter(k_src: torch.Tensor, v_src: torch.Tensor, dst_slots: torch.Tensor,
+                      k_pool: torch.Tensor, v_pool: torch.Tensor, stream=None):
+    _dev_i32(dst_slots, "dst_slots")
+    dt = ACACHE_BF16 if k_src.dtype == torch.bfloat16 else ACACHE_F32
+    n, row = k_src.shape
+    _check("acache_kv_scatter", lib.acache_kv_scatter(
+        _ptr(k_src), _ptr(v_src), k_src.stride(0), n, _ptr(dst_slots), _ptr(k_pool), _ptr(v_pool),
+        k_pool.stride(0), k_pool.shape[0], row, dt, _stream(stream)))
+
+
+def acache_build_maps(layout: Layout, batch: int, anchors: Optional[torch.Tensor], k: int, device="cuda",
+                      stream=None):
+    """Returns dict(row_pos, row_src, write_slots, read_slots, q_rows) of int32 device tensors."""
+    if anchors is not None:
+        _dev_i32(anchors, "anchors")
+    R = k + layout.seq_len - layout.affix_len
+    t = lambda n: torch.empty(n, dtype=torch.int32, device=device)
+    out = dict(row_pos=t(batch * R), row_src=t(batch * R), write_slots=t(batch * R),
+               read_slots=t(batch * layout.seq_len), q_rows=t(batch * layout.mask_len))
+    _check("acache_build_maps", lib.acache_build_maps(
+        ctypes.byref(layout), batch, _ptr(anchors) if k > 0 else None, k, _ptr(out["row_pos"]),
+        _ptr(out["row_src"]), _ptr(out["write_slots"]), _ptr(out["read_slots"]), _ptr(out["q_rows"]),
+        _stream(stream)))
+    return out
+
+
+def _ragged(cu_rows: Sequence[int], cu_keys: Sequence[int]):
+    r = _i32(cu_rows)
+    k = _i32(cu_keys)
+    return Ragged(len(cu_rows) - 1, r, k), (r, k)
+
+
+def acache_attention(dims: Dims, cu_rows, cu_keys, q: torch.Tensor, read_slots: torch.Tensor,
+                     k_pool: torch.Tensor, v_pool: torch.Tensor, out: Optional[torch.Tensor] = None,
+                     lse: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _dev_i32(read_slots, "read_slots")
+    rg, keep = _ragged(cu_rows, cu_keys)
+    if out is None:
+        out = torch.empty_like(q)
+    _check("acache_attention", lib.acache_attention(
+        ctypes.byref(dims), ctypes.byref(rg), _ptr(q), _ptr(read_slots), _ptr(k_pool), _ptr(v_pool),
+        k_pool.stride(0), k_pool.shape[0], _ptr(out), _ptr(lse), _stream(stream)))
+    return out
+
+
+def acache_score(dims: Dims, q: torch.Tensor, q_rows: torch.Tensor, cu_q, k_pool: torch.Tensor,
+                 affix_slots: torch.Tensor, scores: torch.Tensor, norm: int = ACACHE_NORM_AFFIX,
+                 row_lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    _dev_i32(q_rows, "q_rows")
+    _dev_i32(affix_slots, "affix_slots")
+    batch = len(cu_q) - 1
+    L = affix_slots.numel()
+    if ws is None:
+        ws = workspace(dims, max(1, int(cu_q[-1])), batch, L, q.device)
+    cq = _i32(cu_q)
+    _check("acache_score", lib.acache_score(
+        ctypes.byref(dims), batch, _ptr(q), q.stride(0), q.shape[0], _ptr(q_rows), cq, _ptr(k_pool),
+        k_pool.stride(0), k_pool.shape[0], _ptr(affix_slots), L, _ptr(row_lse), norm, _ptr(scores),
+        _ptr(ws), ws.numel(), _stream(stream)))
+    return scores
+
+
+def layer_weights(w: dict) -> LayerWeights:
+    return LayerWeights(*[w[n].data_ptr() for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+
+
+def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tensor, pos: torch.Tensor,
+                           write_slots: torch.Tensor, read_slots: torch.Tensor, k_pool: torch.Tensor,
+                           v_pool: torch.Tensor, ws: torch.Tensor, score: Optional[dict] = None, stream=None):
+    """One block in place on x.  weights: LayerWeights or dict of tensors.
+    score: dict(q_rows, cu_q, affix_slots, scores, norm) for the probe."""
+    for t, n in ((pos, "pos"), (write_slots, "write_slots"), (read_slots, "read_slots")):
+        _dev_i32(t, n)
+    lw = weights if isinstance(weights, LayerWeights) else layer_weights(weights)
+    rg, keep = _ragged(cu_rows, cu_keys)
+    sa = None
+    cq = None
+    if score is not None:
+        cq = _i32(score["cu_q"])
+        sa = ScoreArgs(score["q_rows"].data_ptr(), cq, score["affix_slots"].data_ptr(),
+                       score["affix_slots"].numel(), score.get("norm", ACACHE_NORM_AFFIX),
+                       score["scores"].data_ptr())
+    _check("acache_layer_recompute", lib.acache_layer_recompute(
+        ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
+        _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],
+        ctypes.byref(sa) if sa is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def acache_rmsnorm(dims: Dims, x: torch.Tensor, g: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    if out is None:
+        out = torch.empty_like(x)
+    _check("acache_rmsnorm", lib.acache_rmsnorm(ctypes.byref(dims), _ptr(x), _ptr(g), _ptr(out), x.shape[0],
+                                                _stream(stream)))
+    return out
+
+
+def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = None,
+                  accumulate: bool = False, stream=None):
+    M, K = a.shape
+    N = w.shape[0]
+    if out is None:
+        out = torch.empty((M, N), dtype=a.dtype, device=a.device)
+    _check("acache_linear", lib.acache_linear(ctypes.byref(dims), _ptr(a), _ptr(w), _ptr(out), M, N, K,
+                                              int(accumulate), None, 0, _stream(stream)))
+    return out

@@ -1,0 +1,468 @@
+// C ABI of the selective affix-KV recompute path: argument validation,
+// workspace layout and the launch sequence of each entry point.  Nothing
+// here allocates device memory or synchronises the stream.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+#include "internal.h"
+
+using namespace acache;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+inline size_t elem_size(acache_dtype dt) { return dt == ACACHE_BF16 ? 2 : 4; }
+
+#define CHECK(cond, code) \
+  do {                    \
+    if (!(cond)) return (code); \
+  } while (0)
+
+#define LAUNCH(expr)                                   \
+  do {                                                 \
+    if ((expr) != hipSuccess) return ACACHE_ERR_DEVICE; \
+  } while (0)
+
+acache_status check_dims(const acache_dims* d) {
+  CHECK(d, ACACHE_ERR_NULL);
+  CHECK(d->dtype == ACACHE_BF16 || d->dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
+  CHECK(d->d_model > 0 && d->n_heads > 0 && d->n_kv_heads > 0 && d->head_dim > 0 && d->d_ff > 0,
+        ACACHE_ERR_SHAPE);
+  CHECK(d->n_heads % d->n_kv_heads == 0, ACACHE_ERR_SHAPE);
+  CHECK(d->rms_eps >= 0.f && d->rope_base > 0.f, ACACHE_ERR_SHAPE);
+  if (d->dtype == ACACHE_BF16) {
+    CHECK(d->head_dim == 128, ACACHE_ERR_UNSUPPORTED);
+  } else {
+    CHECK(d->head_dim % 2 == 0 && d->head_dim <= 128, ACACHE_ERR_UNSUPPORTED);
+  }
+  return ACACHE_OK;
+}
+
+// Shapes the bf16 GEMM tiles and the fused epilogues need.
+acache_status check_layer_dims(const acache_dims* d) {
+  acache_status st = check_dims(d);
+  if (st != ACACHE_OK) return st;
+  if (d->dtype == ACACHE_BF16) {
+    CHECK(d->d_model % 256 == 0 && d->d_model <= 8192, ACACHE_ERR_UNSUPPORTED);
+    CHECK((d->n_heads * d->head_dim) % 256 == 0, ACACHE_ERR_UNSUPPORTED);
+    CHECK((d->n_kv_heads * d->head_dim) % 128 == 0, ACACHE_ERR_UNSUPPORTED);
+    CHECK(((d->n_heads + 2 * d->n_kv_heads) * d->head_dim) % 256 == 0, ACACHE_ERR_UNSUPPORTED);
+    CHECK(d->d_ff % 128 == 0, ACACHE_ERR_UNSUPPORTED);
+  }
+  return ACACHE_OK;
+}
+
+// Validates host cu arrays and fills the kernel-side copy.
+acache_status make_ragged(const acache_ragged* rg, Ragged& out) {
+  CHECK(rg && rg->cu_rows && rg->cu_keys, ACACHE_ERR_NULL);
+  CHECK(rg->batch >= 1 && rg->batch <= kMaxBatch, ACACHE_ERR_SHAPE);
+  CHECK(rg->cu_rows[0] == 0 && rg->cu_keys[0] == 0, ACACHE_ERR_SHAPE);
+  std::memset(&out, 0, sizeof(out));
+  out.batch = rg->batch;
+  for (int b = 0; b <= rg->batch; ++b) {
+    out.cu_rows[b] = rg->cu_rows[b];
+    out.cu_keys[b] = rg->cu_keys[b];
+    if (b > 0) {
+      const int nr = rg->cu_rows[b] - rg->cu_rows[b - 1];
+      const int nk = rg->cu_keys[b] - rg->cu_keys[b - 1];
+      CHECK(nr >= 0 && nk >= 0, ACACHE_ERR_SHAPE);
+      CHECK(nr == 0 || nk > 0, ACACHE_ERR_SHAPE);  // rows need keys
+    }
+  }
+  return ACACHE_OK;
+}
+
+acache_status check_cu(const int32_t* cu, int batch) {
+  CHECK(cu, ACACHE_ERR_NULL);
+  CHECK(cu[0] == 0, ACACHE_ERR_SHAPE);
+  for (int b = 1; b <= batch; ++b) CHECK(cu[b] >= cu[b - 1], ACACHE_ERR_SHAPE);
+  return ACACHE_OK;
+}
+
+// Workspace plan for `rows` rows (layer_recompute / score / linear).
+struct WsPlan {
+  size_t y, q, o, h, part, qkv, gu, lse, lse_aff, colsum, total;
+};
+
+WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
+  WsPlan w = {};
+  const size_t es = elem_size(d->dtype);
+  const size_t M = (size_t)rows;
+  const size_t hq = (size_t)d->n_heads * d->head_dim;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  w.y = take(M * d->d_model * es);
+  w.q = take(M * hq * es);
+  w.o = take(M * hq * es);
+  w.h = take(M * d->d_ff * es);
+  if (d->dtype == ACACHE_BF16) {
+    w.part = take(8 * M * d->d_model * sizeof(float));
+    w.qkv = w.gu = 0;
+  } else {
+    w.qkv = take(M * (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim * es);
+    w.gu = take(M * 2 * (size_t)d->d_ff * es);
+    w.part = 0;
+  }
+  w.lse = take(M * d->n_heads * sizeof(float));
+  w.lse_aff = take(M * d->n_heads * sizeof(float));
+  w.colsum = take((size_t)(batch > 0 ? batch : 1) * d->n_heads * (size_t)(L > 0 ? L : 1) * sizeof(float));
+  w.total = off;
+  return w;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Eq. 4-5 for one layer (shared by acache_score and the probe mode of
+// acache_layer_recompute).  lse_full: [q_n_rows, H] natural log, or NULL.
+acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, const void* q,
+                        int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows, const void* k_pool,
+                        int64_t pool_ld, int64_t n_slots, const int32_t* affix_slots, int L,
+                        acache_norm norm, const float* lse_full, float* scores, float* lse_aff,
+                        float* colsum, hipStream_t s) {
+  const int H = d->n_heads, Hkv = d->n_kv_heads, dh = d->head_dim;
+  const float* lse = lse_full;
+  int by_qrow = 0;
+  if (norm == ACACHE_NORM_AFFIX) {
+    if (d->dtype == ACACHE_BF16)
+      LAUNCH(launch_score_lse_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
+                                   n_slots, affix_slots, L, lse_aff, s));
+    else
+      LAUNCH(launch_score_lse_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+                                  (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse_aff, s));
+    lse = lse_aff;
+    by_qrow = 1;
+  }
+  if (d->dtype == ACACHE_BF16)
+    LAUNCH(launch_score_colsum_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
+                                    n_slots, affix_slots, L, lse, by_qrow, colsum, s));
+  else
+    LAUNCH(launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+                                   (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
+                                   colsum, s));
+  LAUNCH(launch_head_reduce(colsum, batch, H, L, scores, s));
+  return ACACHE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t acache_version(void) { return 100; }
+
+const char* acache_status_string(acache_status st) {
+  switch (st) {
+    case ACACHE_OK: return "ok";
+    case ACACHE_ERR_NULL: return "a required pointer is NULL";
+    case ACACHE_ERR_SHAPE: return "sizes are negative, inconsistent or out of range";
+    case ACACHE_ERR_ALIGN: return "a pointer or leading dimension is not 16-byte aligned";
+    case ACACHE_ERR_UNSUPPORTED: return "shape or type outside what the kernels implement";
+    case ACACHE_ERR_WORKSPACE: return "workspace missing or too small";
+    case ACACHE_ERR_DEVICE: return "a HIP launch or call failed";
+  }
+  return "unknown status";
+}
+
+size_t acache_workspace_size(const acache_dims* dims, int32_t max_rows, int32_t batch,
+                             int32_t affix_len) {
+  if (check_dims(dims) != ACACHE_OK || max_rows < 0 || batch < 0 || affix_len < 0) return 0;
+  return plan_ws(dims, max_rows, batch, affix_len).total;
+}
+
+acache_status acache_topk(const float* scores, int32_t batch, int32_t L, int32_t k,
+                          int32_t* idx_out, hipStream_t stream) {
+  CHECK(batch >= 0 && L >= 0 && k >= 0 && k <= L, ACACHE_ERR_SHAPE);
+  CHECK(L <= 16384, ACACHE_ERR_UNSUPPORTED);
+  if (batch == 0 || k == 0) return ACACHE_OK;
+  CHECK(scores && idx_out, ACACHE_ERR_NULL);
+  LAUNCH(launch_topk(scores, batch, L, k, idx_out, stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_gather_rows(const void* src, int64_t src_ld_bytes, int64_t src_rows,
+                                 const int32_t* idx, const int32_t* remap, int64_t remap_len,
+                                 int32_t n, int32_t row_bytes, void* dst, int64_t dst_ld_bytes,
+                                 hipStream_t stream) {
+  CHECK(n >= 0 && row_bytes >= 0 && src_rows >= 0, ACACHE_ERR_SHAPE);
+  if (n == 0 || row_bytes == 0) return ACACHE_OK;
+  CHECK(src && idx && dst, ACACHE_ERR_NULL);
+  CHECK(row_bytes % 16 == 0 && src_ld_bytes >= row_bytes && dst_ld_bytes >= row_bytes, ACACHE_ERR_SHAPE);
+  CHECK(!remap || remap_len >= 0, ACACHE_ERR_SHAPE);
+  CHECK(aligned16(src) && aligned16(dst) && src_ld_bytes % 16 == 0 && dst_ld_bytes % 16 == 0,
+        ACACHE_ERR_ALIGN);
+  LAUNCH(launch_gather_rows(src, src_ld_bytes, src_rows, idx, remap, remap_len, n, row_bytes, dst,
+                            dst_ld_bytes, stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t src_ld, int32_t n,
+                                const int32_t* dst_slots, void* k_pool, void* v_pool,
+                                int64_t pool_ld, int64_t n_slots, int32_t row_elems,
+                                acache_dtype dtype, hipStream_t stream) {
+  CHECK(dtype == ACACHE_BF16 || dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
+  CHECK(n >= 0 && row_elems >= 0 && n_slots >= 0, ACACHE_ERR_SHAPE);
+  if (n == 0 || row_elems == 0) return ACACHE_OK;
+  CHECK(k_src && v_src && dst_slots && k_pool && v_pool, ACACHE_ERR_NULL);
+  const int64_t es = (int64_t)elem_size(dtype);
+  CHECK(src_ld >= row_elems && pool_ld >= row_elems, ACACHE_ERR_SHAPE);
+  CHECK((row_elems * es) % 16 == 0, ACACHE_ERR_SHAPE);
+  CHECK(aligned16(k_src) && aligned16(v_src) && aligned16(k_pool) && aligned16(v_pool) &&
+            (src_ld * es) % 16 == 0 && (pool_ld * es) % 16 == 0,
+        ACACHE_ERR_ALIGN);
+  LAUNCH(launch_kv_scatter(k_src, v_src, src_ld * es, n, dst_slots, k_pool, v_pool, pool_ld * es,
+                           n_slots, (int)(row_elems * es), stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const int32_t* anchors,
+                                int32_t k, int32_t* row_pos, int32_t* row_src,
+                                int32_t* write_slots, int32_t* read_slots, int32_t* q_rows,
+                                hipStream_t stream) {
+  CHECK(lay, ACACHE_ERR_NULL);
+  const int S = lay->seq_len, ab = lay->affix_begin, L = lay->affix_len;
+  CHECK(batch >= 0 && S >= 0 && L >= 0 && ab >= 0 && ab + L <= S, ACACHE_ERR_SHAPE);
+  CHECK(k >= 0 && k <= L, ACACHE_ERR_SHAPE);
+  CHECK(lay->mask_len >= 0 && lay->mask_begin >= 0 && lay->mask_begin + lay->mask_len <= S,
+        ACACHE_ERR_SHAPE);
+  CHECK(lay->mask_len == 0 || lay->mask_begin + lay->mask_len <= ab || lay->mask_begin >= ab + L,
+        ACACHE_ERR_SHAPE);  // the masked span is not part of the affix
+  const int R = k + S - L;
+  CHECK(lay->private_stride >= R && lay->private_base >= 0 && lay->shared_base >= 0, ACACHE_ERR_SHAPE);
+  CHECK((int64_t)lay->private_base + (int64_t)batch * lay->private_stride < (int64_t)1 << 31,
+        ACACHE_ERR_SHAPE);
+  if (batch == 0 || S == 0) return ACACHE_OK;
+  CHECK(row_pos && row_src && write_slots && read_slots, ACACHE_ERR_NULL);
+  CHECK(k == 0 || anchors, ACACHE_ERR_NULL);
+  LAUNCH(launch_build_maps(*lay, batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows,
+                           stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void* g, void* y,
+                             int32_t rows, hipStream_t stream) {
+  acache_status st = check_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(rows >= 0, ACACHE_ERR_SHAPE);
+  if (rows == 0) return ACACHE_OK;
+  CHECK(x && g && y, ACACHE_ERR_NULL);
+  LAUNCH(launch_rmsnorm(dims->dtype, x, g, y, rows, dims->d_model, dims->rms_eps, stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,
+                            int32_t M, int32_t N, int32_t K, int32_t accumulate, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  (void)ws;
+  (void)ws_bytes;
+  CHECK(dims, ACACHE_ERR_NULL);
+  CHECK(dims->dtype == ACACHE_BF16 || dims->dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
+  CHECK(M >= 0 && N >= 0 && K >= 0, ACACHE_ERR_SHAPE);
+  if (M == 0 || N == 0) return ACACHE_OK;
+  CHECK(a && w && c, ACACHE_ERR_NULL);
+  if (dims->dtype == ACACHE_BF16) {
+    CHECK(K > 0 && K % 64 == 0 && N % 256 == 0, ACACHE_ERR_UNSUPPORTED);
+    CHECK(aligned16(a) && aligned16(w) && aligned16(c), ACACHE_ERR_ALIGN);
+    GemmParams p = {};
+    p.X = a;
+    p.W = w;
+    p.M = M;
+    p.N = N;
+    p.K = K;
+    p.splits = 1;
+    p.C = c;
+    p.ldc = N;
+    LAUNCH(launch_gemm_bf16(accumulate ? EPI_ACCUM : EPI_STORE, p, stream));
+  } else {
+    LAUNCH(launch_gemm_f32((const float*)a, (const float*)w, (float*)c, N, M, N, K, accumulate, stream));
+  }
+  return ACACHE_OK;
+}
+
+acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg, const void* q,
+                               const int32_t* read_slots, const void* k_pool, const void* v_pool,
+                               int64_t pool_ld, int64_t n_slots, void* out, float* lse,
+                               hipStream_t stream) {
+  acache_status st = check_dims(dims);
+  if (st != ACACHE_OK) return st;
+  Ragged r;
+  st = make_ragged(rg, r);
+  if (st != ACACHE_OK) return st;
+  const int rows = r.cu_rows[r.batch];
+  if (rows == 0) return ACACHE_OK;
+  CHECK(q && read_slots && k_pool && v_pool && out, ACACHE_ERR_NULL);
+  CHECK(pool_ld >= (int64_t)dims->n_kv_heads * dims->head_dim && n_slots >= 0, ACACHE_ERR_SHAPE);
+  const int64_t es = (int64_t)elem_size(dims->dtype);
+  CHECK(aligned16(q) && aligned16(k_pool) && aligned16(v_pool) && aligned16(out) && (pool_ld * es) % 16 == 0,
+        ACACHE_ERR_ALIGN);
+  if (dims->dtype == ACACHE_BF16)
+    LAUNCH(launch_attention_bf16(r, dims->n_heads, dims->n_kv_heads, q, read_slots, k_pool, v_pool,
+                                 pool_ld, n_slots, out, lse, stream));
+  else
+    LAUNCH(launch_attention_f32(r, dims->n_heads, dims->n_kv_heads, dims->head_dim, (const float*)q,
+                                read_slots, (const float*)k_pool, (const float*)v_pool, pool_ld, n_slots,
+                                (float*)out, lse, stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                           int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
+                           const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                           const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
+                           acache_norm norm, float* scores, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  acache_status st = check_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(batch >= 0 && batch <= kMaxBatch && affix_len >= 0 && affix_len <= 65536, ACACHE_ERR_SHAPE);
+  CHECK(norm == ACACHE_NORM_AFFIX || norm == ACACHE_NORM_FULL, ACACHE_ERR_UNSUPPORTED);
+  if (batch == 0 || affix_len == 0) return ACACHE_OK;
+  st = check_cu(cu_q, batch);
+  if (st != ACACHE_OK) return st;
+  const int n_q = cu_q[batch];
+  if (n_q == 0) return ACACHE_OK;
+  CHECK(q && q_rows && k_pool && affix_slots && scores, ACACHE_ERR_NULL);
+  CHECK(norm == ACACHE_NORM_FULL ? row_lse != nullptr : row_lse == nullptr, ACACHE_ERR_NULL);
+  CHECK(q_ld >= (int64_t)dims->n_heads * dims->head_dim && q_n_rows >= 0, ACACHE_ERR_SHAPE);
+  CHECK(pool_ld >= (int64_t)dims->n_kv_heads * dims->head_dim && n_slots >= 0, ACACHE_ERR_SHAPE);
+  const int64_t es = (int64_t)elem_size(dims->dtype);
+  CHECK(aligned16(q) && aligned16(k_pool) && (q_ld * es) % 16 == 0 && (pool_ld * es) % 16 == 0,
+        ACACHE_ERR_ALIGN);
+  // workspace: the lse and column-sum regions of a plan sized for n_q rows
+  const WsPlan w = plan_ws(dims, n_q, batch, affix_len);
+  CHECK(ws && ws_bytes >= w.total, ACACHE_ERR_WORKSPACE);
+  return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
+                   affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum),
+                   stream);
+}
+
+acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer_weights* w,
+                                     const acache_ragged* rg, void* x, const int32_t* pos,
+                                     const int32_t* write_slots, const int32_t* read_slots,
+                                     void* k_pool, void* v_pool, int64_t pool_ld, int64_t n_slots,
+                                     const acache_score_args* score, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  acache_status st = check_layer_dims(dims);
+  if (st != ACACHE_OK) return st;
+  Ragged r;
+  st = make_ragged(rg, r);
+  if (st != ACACHE_OK) return st;
+  const int M = r.cu_rows[r.batch];
+  if (M == 0) return ACACHE_OK;
+  CHECK(w && x && pos && write_slots && read_slots && k_pool && v_pool, ACACHE_ERR_NULL);
+  CHECK(w->attn_norm && w->w_qkv && w->w_o && w->mlp_norm && w->w_gate_up && w->w_down, ACACHE_ERR_NULL);
+  const int d = dims->d_model, H = dims->n_heads, Hkv = dims->n_kv_heads, dh = dims->head_dim,
+            F = dims->d_ff;
+  const int hq = H * dh, hkv = Hkv * dh, nqkv = (H + 2 * Hkv) * dh;
+  CHECK(pool_ld >= hkv && n_slots > 0, ACACHE_ERR_SHAPE);
+  const int64_t es = (int64_t)elem_size(dims->dtype);
+  CHECK(aligned16(x) && aligned16(k_pool) && aligned16(v_pool) && (pool_ld * es) % 16 == 0, ACACHE_ERR_ALIGN);
+  CHECK(aligned16(w->attn_norm) && aligned16(w->w_qkv) && aligned16(w->w_o) && aligned16(w->mlp_norm) &&
+            aligned16(w->w_gate_up) && aligned16(w->w_down),
+        ACACHE_ERR_ALIGN);
+  int L = 0;
+  if (score) {
+    L = score->affix_len;
+    CHECK(L >= 0 && L <= 65536, ACACHE_ERR_SHAPE);
+    CHECK(score->norm == ACACHE_NORM_AFFIX || score->norm == ACACHE_NORM_FULL, ACACHE_ERR_UNSUPPORTED);
+    st = check_cu(score->cu_q, r.batch);
+    if (st != ACACHE_OK) return st;
+    CHECK(score->cu_q[r.batch] <= M, ACACHE_ERR_SHAPE);
+    if (L > 0 && score->cu_q[r.batch] > 0) CHECK(score->q_rows && score->affix_slots && score->scores, ACACHE_ERR_NULL);
+  }
+  const WsPlan p = plan_ws(dims, M, r.batch, L);
+  CHECK(ws && ws_bytes >= p.total && aligned16(ws), ACACHE_ERR_WORKSPACE);
+  void* y = at<char>(ws, p.y);
+  void* q = at<char>(ws, p.q);
+  void* o = at<char>(ws, p.o);
+  void* hb = at<char>(ws, p.h);
+  const bool probe = score && L > 0 && score->cu_q[r.batch] > 0;
+  float* lse = (probe && score->norm == ACACHE_NORM_FULL) ? at<float>(ws, p.lse) : nullptr;
+
+  LAUNCH(launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
+  if (dims->dtype == ACACHE_BF16) {
+    GemmParams g = {};
+    g.X = y;
+    g.W = w->w_qkv;
+    g.M = M;
+    g.N = nqkv;
+    g.K = d;
+    g.splits = 1;
+    g.q_out = q;
+    g.k_pool = k_pool;
+    g.v_pool = v_pool;
+    g.pool_ld = pool_ld;
+    g.n_slots = n_slots;
+    g.write_slots = write_slots;
+    g.pos = pos;
+    g.hq_cols = hq;
+    g.hkv_cols = hkv;
+    g.rope_base = dims->rope_base;
+    LAUNCH(launch_gemm_bf16(EPI_QKV, g, stream));
+    LAUNCH(launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse, stream));
+  } else {
+    float* qkv = at<float>(ws, p.qkv);
+    LAUNCH(launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));
+    LAUNCH(launch_rope_scatter_f32(qkv, M, H, Hkv, dh, pos, dims->rope_base, (float*)q, write_slots,
+                                   (float*)k_pool, (float*)v_pool, pool_ld, n_slots, stream));
+    LAUNCH(launch_attention_f32(r, H, Hkv, dh, (const float*)q, read_slots, (const float*)k_pool,
+                                (const float*)v_pool, pool_ld, n_slots, (float*)o, lse, stream));
+  }
+  if (probe) {
+    st = run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots,
+                   score->affix_slots, L, score->norm, lse, score->scores, at<float>(ws, p.lse_aff),
+                   at<float>(ws, p.colsum), stream);
+    if (st != ACACHE_OK) return st;
+  }
+  if (dims->dtype == ACACHE_BF16) {
+    float* part = at<float>(ws, p.part);
+    GemmParams g = {};
+    g.X = o;
+    g.W = w->w_o;
+    g.M = M;
+    g.N = d;
+    g.K = hq;
+    g.splits = gemm_bf16_splits(M, d, hq);
+    g.P = part;
+    LAUNCH(launch_gemm_bf16(EPI_PARTIAL, g, stream));
+    LAUNCH(launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
+    GemmParams u = {};
+    u.X = y;
+    u.W = w->w_gate_up;
+    u.M = M;
+    u.N = 2 * F;
+    u.K = d;
+    u.splits = 1;
+    u.C = hb;
+    u.ldc = F;
+    LAUNCH(launch_gemm_bf16(EPI_SWIGLU, u, stream));
+    GemmParams dn = {};
+    dn.X = hb;
+    dn.W = w->w_down;
+    dn.M = M;
+    dn.N = d;
+    dn.K = F;
+    dn.splits = gemm_bf16_splits(M, d, F);
+    dn.P = part;
+    LAUNCH(launch_gemm_bf16(EPI_PARTIAL, dn, stream));
+    LAUNCH(launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+  } else {
+    float* gu = at<float>(ws, p.gu);
+    LAUNCH(launch_gemm_f32((const float*)o, (const float*)w->w_o, (float*)x, d, M, d, hq, 1, stream));
+    LAUNCH(launch_rmsnorm(ACACHE_F32, x, w->mlp_norm, y, M, d, dims->rms_eps, stream));
+    LAUNCH(launch_gemm_f32((const float*)y, (const float*)w->w_gate_up, gu, 2 * F, M, 2 * F, d, 0, stream));
+    LAUNCH(launch_swiglu_f32(gu, M, F, (float*)hb, stream));
+    LAUNCH(launch_gemm_f32((const float*)hb, (const float*)w->w_down, (float*)x, d, M, d, F, 1, stream));
+  }
+  return ACACHE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Internal launch interface between the C ABI (api.cpp) and the gfx950
+// kernels.  Every launcher enqueues on `stream` and returns the launch
+// status; none allocates or synchronises.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/acache.h"
+
+namespace acache {
+
+constexpr int kMaxBatch = 64;
+
+// Per-request row/key offsets and query-tile starts, passed by value.
+struct Ragged {
+  int batch;
+  int cu_rows[kMaxBatch + 1];
+  int cu_keys[kMaxBatch + 1];
+  int tile_start[kMaxBatch + 1];  // cumulative query tiles of `tile_rows` rows
+};
+
+// ---- rows, maps, selection (k_rows.hip, k_topk.hip)
+hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
+                              const int32_t* remap, int64_t remap_len, int n, int row_bytes,
+                              void* dst, int64_t dst_ld, hipStream_t s);
+hipError_t launch_kv_scatter(const void* k_src, const void* v_src, int64_t src_ld_bytes, int n,
+                             const int32_t* slots, void* k_pool, void* v_pool,
+                             int64_t pool_ld_bytes, int64_t n_slots, int row_bytes, hipStream_t s);
+hipError_t launch_build_maps(const acache_layout& lay, int batch, const int32_t* anchors, int k,
+                             int32_t* row_pos, int32_t* row_src, int32_t* write_slots,
+                             int32_t* read_slots, int32_t* q_rows, hipStream_t s);
+hipError_t launch_topk(const float* scores, int batch, int L, int k, int32_t* out, hipStream_t s);
+hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y, int rows, int d,
+                          float eps, hipStream_t s);
+// x[m] += sum_s part[s][m] (bf16 x, fp32 partials [splits][M][d]); if y,
+// y[m] = RMSNorm(x[m]) * g.
+hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M, int d,
+                                  const void* g, void* y, float eps, hipStream_t s);
+// scores[b][j] += sum_h part[b][h][j]
+hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
+                              hipStream_t s);
+
+// ---- bf16 MFMA GEMM (k_gemm.hip).  C = X W^T, X [M, K], W [N, K].
+enum GemmEpi { EPI_STORE = 0, EPI_ACCUM = 1, EPI_PARTIAL = 2, EPI_QKV = 3, EPI_SWIGLU = 4 };
+struct GemmParams {
+  const void* X;
+  const void* W;
+  int M, N, K;      // N: weight rows (for SWIGLU: 2F)
+  int splits;       // k splits (EPI_PARTIAL only)
+  void* C;          // STORE / ACCUM / SWIGLU output, [M, ldc]
+  int64_t ldc;
+  float* P;         // PARTIAL output [splits][M][N]
+  // QKV epilogue
+  void* q_out;      // [M, hq_cols]
+  void* k_pool;
+  void* v_pool;
+  int64_t pool_ld;
+  int64_t n_slots;
+  const int32_t* write_slots;
+  const int32_t* pos;
+  int hq_cols, hkv_cols;
+  float rope_base;
+};
+hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s);
+int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL
+
+// ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
+hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
+                                 const int32_t* read_slots, const void* k_pool, const void* v_pool,
+                                 int64_t pool_ld, int64_t n_slots, void* out, float* lse,
+                                 hipStream_t s);
+int attention_tile_rows();
+// Per masked row and head, natural-log LSE over the affix keys.
+hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
+                                 int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
+                                 const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                                 const int32_t* affix_slots, int L, float* lse_out,
+                                 hipStream_t s);
+// part[b][h][j] = sum over request b's masked rows of exp(logit - lse);
+// lse indexed by q_rows position (lse_by_qrow) or by row (row_lse, [rows, H]).
+hipError_t launch_score_colsum_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
+                                    int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
+                                    const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                                    const int32_t* affix_slots, int L, const float* lse,
+                                    int lse_by_qrow, float* part, hipStream_t s);
+
+// ---- fp32 VALU path (k_f32.hip)
+hipError_t launch_gemm_f32(const float* X, const float* W, float* C, int64_t ldc, int M, int N,
+                           int K, int accumulate, hipStream_t s);
+hipError_t launch_rope_scatter_f32(const float* qkv, int M, int H, int Hkv, int dh,
+                                   const int32_t* pos, float rope_base, float* q_out,
+                                   const int32_t* write_slots, float* k_pool, float* v_pool,
+                                   int64_t pool_ld, int64_t n_slots, hipStream_t s);
+hipError_t launch_swiglu_f32(const float* gu, int M, int F, float* h, hipStream_t s);
+hipError_t launch_attention_f32(const Ragged& rg, int H, int Hkv, int dh, const float* q,
+                                const int32_t* read_slots, const float* k_pool,
+                                const float* v_pool, int64_t pool_ld, int64_t n_slots, float* out,
+                                float* lse, hipStream_t s);
+hipError_t launch_score_lse_f32(int batch, const int* cu_q, int H, int Hkv, int dh, const float* q,
+                                int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
+                                const float* k_pool, int64_t pool_ld, int64_t n_slots,
+                                const int32_t* affix_slots, int L, float* lse_out, hipStream_t s);
+hipError_t launch_score_colsum_f32(int batch, const int* cu_q, int H, int Hkv, int dh,
+                                   const float* q, int64_t q_ld, int64_t q_n_rows,
+                                   const int32_t* q_rows, const float* k_pool, int64_t pool_ld,
+                                   int64_t n_slots, const int32_t* affix_slots, int L,
+                                   const float* lse, int lse_by_qrow, float* part, hipStream_t s);
+
+}  // namespace acache

@@ -1,0 +1,344 @@
+// Read-slot flash attention for gfx950 (Appendix C.1): bidirectional, no
+// mask, grouped KV heads, keys and values gathered through a slot map.
+//
+// Each wavefront owns 32 queries of one head; a workgroup of 2 wavefronts
+// shares the K/V tiles (64 keys) in LDS, double buffered, with the loads of
+// tile t+1 in flight while tile t computes.  Per tile:
+//
+//   S^T = K Q^T       MFMA 32x32x16, K tile as the A operand, the wave's Q
+//                     fragments (registers) as B.  Lane l then holds query
+//                     l%32 and 16 keys per 32-key block, so the softmax row
+//                     statistics are an in-register reduction plus one
+//                     exchange with lane l^32.
+//   O^T += V^T P^T    the lane's own exp'd logits, packed to bf16, are the B
+//                     operand directly.  For that the rows of S^T are a fixed
+//                     permutation of the keys inside each 16-key group,
+//                     chosen so that B element j of lane half h is key 8h+j;
+//                     the A operand then reads 8 consecutive keys of the
+//                     transposed V tile (one ds_read_b128).
+//
+// The V tile is transposed on its way into LDS: each thread loads 4 keys x 8
+// dims (four 16-byte loads) and writes 8 packed 4-key runs.  Softmax runs in
+// base 2 on log2(e)/sqrt(d_h)-prescaled logits (hardware exp2).  The same
+// kernel without the V half computes only the row log-sum-exp; it serves the
+// affix-only normalisation of the probe scores (Eq. 4).
+#include "device.h"
+#include "internal.h"
+
+namespace acache {
+
+namespace {
+
+constexpr int kDh = 128;
+constexpr int kWaves = 2;
+constexpr int kTileQ = 32 * kWaves;  // queries per workgroup
+constexpr int kTileK = 64;           // keys per LDS stage
+constexpr int kLdK = kDh + 8;        // K tile row (elements)
+constexpr int kLdV = kTileK + 8;     // transposed V tile row (elements)
+constexpr int kThreads = 64 * kWaves;
+
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
+struct AttnArgs {
+  const bf16* q;
+  int64_t q_ld;
+  int64_t q_n_rows;
+  const int32_t* q_idx;  // nullable: query i of a request is row q_idx[row_start + i]
+  const int32_t* slots;  // key j of request b is pool row slots[key_start[b] + j]
+  const bf16* k_pool;
+  const bf16* v_pool;
+  int64_t pool_ld;
+  int64_t n_slots;
+  bf16* out;             // [rows, H * 128] (PV only)
+  float* lse;            // [.., H] natural log; nullable for PV
+  int H, Hkv;
+  int batch;
+  int row_start[kMaxBatch + 1];
+  int key_start[kMaxBatch + 1];
+  int key_len[kMaxBatch + 1];
+  int tile_start[kMaxBatch + 1];
+};
+
+// Physical key (within a 32-key block) read by S^T row i.
+__device__ __forceinline__ int key_perm(int i) {
+  const int r = i & 15;
+  return (i & 16) | (8 * ((r >> 2) & 1) + (r & 3) + 4 * (r >> 3));
+}
+
+template <bool PV>
+__global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16 sK[2][kTileK * kLdK];
+  __shared__ __attribute__((aligned(16))) bf16 sV[PV ? 2 : 1][PV ? kDh * kLdV : 8];
+
+  // request of this workgroup
+  const int tile = blockIdx.x;
+  int b = 0;
+  {
+    int lo = 0, hi = a.batch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+  }
+  const int h = blockIdx.y;
+  const int g = h / (a.H / a.Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
+  const int n_rows = a.row_start[b + 1] - a.row_start[b];
+  const int qi = (tile - a.tile_start[b]) * kTileQ + wave * 32 + (lane & 31);
+  const bool q_ok = qi < n_rows;
+  const int S = a.key_len[b];
+  const int32_t* slots = a.slots + a.key_start[b];
+
+  // query fragments: Q[q][16 s + 8 hl .. +7], s = 0..7
+  int64_t qrow = -1;
+  if (q_ok) {
+    qrow = a.row_start[b] + qi;
+    if (a.q_idx) qrow = a.q_idx[qrow];
+    if (qrow < 0 || qrow >= a.q_n_rows) qrow = -1;
+  }
+  bf16x8 qf[8];
+  {
+    const bf16* qp = a.q + (qrow < 0 ? 0 : qrow) * a.q_ld + h * kDh + hl * 8;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (qrow >= 0) v = *reinterpret_cast<const u32x4*>(qp + s * 16);
+      qf[s] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  // staging: K 8 chunks, V 2 items of 4 keys x 8 dims per thread
+  u32x4 kreg[8];
+  u32x4 vreg[PV ? 8 : 1];
+  const int64_t head_off = (int64_t)g * kDh;
+  auto slot_of = [&](int key) -> int64_t {
+    if (key >= S) return -1;
+    const int64_t s = slots[key];
+    return (s >= 0 && s < a.n_slots) ? s : -1;
+  };
+  auto load_tile = [&](int t) {
+    const int k0 = t * kTileK;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * kThreads;
+      const int key = c >> 4, ch = c & 15;
+      const int64_t sl = slot_of(k0 + key);
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (sl >= 0) v = *reinterpret_cast<const u32x4*>(a.k_pool + sl * a.pool_ld + head_off + ch * 8);
+      kreg[i] = v;
+    }
+    if constexpr (PV) {
+#pragma unroll
+      for (int it = 0; it < 2; ++it) {
+        const int item = tid + it * kThreads;
+        const int kg = item & 15, dc = item >> 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t sl = slot_of(k0 + kg * 4 + r);
+          u32x4 v = {0u, 0u, 0u, 0u};
+          if (sl >= 0) v = *reinterpret_cast<const u32x4*>(a.v_pool + sl * a.pool_ld + head_off + dc * 8);
+          vreg[it * 4 + r] = v;
+        }
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = tid + i * kThreads;
+      const int key = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sK[buf][key * kLdK + ch * 8]) = kreg[i];
+    }
+    if constexpr (PV) {
+#pragma unroll
+      for (int it = 0; it < 2; ++it) {
+        const int item = tid + it * kThreads;
+        const int kg = item & 15, dc = item >> 4;
+        const bf16x8 v0 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 0]);
+        const bf16x8 v1 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 1]);
+        const bf16x8 v2 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 2]);
+        const bf16x8 v3 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 3]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          bf16x4 w;
+          w[0] = v0[e]; w[1] = v1[e]; w[2] = v2[e]; w[3] = v3[e];
+          *reinterpret_cast<bf16x4*>(&sV[buf][(dc * 8 + e) * kLdV + kg * 4]) = w;
+        }
+      }
+    }
+  };
+
+  f32x16 o_acc[PV ? 4 : 1];
+  if constexpr (PV) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o_acc[d][r] = 0.f;
+  }
+  float m_run = -INFINITY, l_part = 0.f;
+  const float scale = kLog2e * rsqrtf((float)kDh);
+  const int n_tiles = (S + kTileK - 1) / kTileK;
+  const int krow = key_perm(lane & 31);
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int t = 0; t < n_tiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < n_tiles) load_tile(t + 1);
+    const bf16* ks = sK[buf];
+    f32x16 st[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[kb][r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const bf16x8 af = *reinterpret_cast<const bf16x8*>(ks + (kb * 32 + krow) * kLdK + s * 16 + hl * 8);
+        st[kb] = mfma32x32x16(af, qf[s], st[kb]);
+      }
+    }
+    // register r of block kb holds key kb*32 + 16(r/8) + 8 hl + r%8
+    const int kt0 = t * kTileK;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
+        const float u = key < S ? st[kb][r] * scale : -INFINITY;
+        st[kb][r] = u;
+        mx = fmaxf(mx, u);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = exp2f(st[kb][r] - m_new);
+        st[kb][r] = e;
+        psum += e;
+      }
+    l_part = l_part * alpha + psum;
+    m_run = m_new;
+    if constexpr (PV) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
+      const bf16* vs = sV[buf];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int g2 = 0; g2 < 2; ++g2) {
+          bf16x8 pb;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) pb[j] = (bf16)st[kb][8 * g2 + j];
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+                vs + (d * 32 + (lane & 31)) * kLdV + kb * 32 + 16 * g2 + 8 * hl);
+            o_acc[d] = mfma32x32x16(vf, pb, o_acc[d]);
+          }
+        }
+    }
+    if (t + 1 < n_tiles) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_part + __shfl_xor(l_part, 32);
+  if (!q_ok) return;
+  const int64_t row = a.row_start[b] + qi;
+  if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run + __log2f(l_tot)) * kLn2;
+  if constexpr (PV) {
+    const float inv = 1.f / l_tot;
+    bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = (bf16)(o_acc[d][4 * gq + j] * inv);
+        *reinterpret_cast<bf16x4*>(op + d * 32 + 8 * gq + 4 * hl) = w;
+      }
+  }
+}
+
+template <bool PV>
+hipError_t launch(AttnArgs& a, hipStream_t s) {
+  int tiles = 0;
+  for (int b = 0; b < a.batch; ++b) {
+    a.tile_start[b] = tiles;
+    tiles += (a.row_start[b + 1] - a.row_start[b] + kTileQ - 1) / kTileQ;
+  }
+  a.tile_start[a.batch] = tiles;
+  if (tiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(attention_kernel<PV>, dim3(tiles, a.H), dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int attention_tile_rows() { return kTileQ; }
+
+hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
+                                 const int32_t* read_slots, const void* k_pool, const void* v_pool,
+                                 int64_t pool_ld, int64_t n_slots, void* out, float* lse,
+                                 hipStream_t s) {
+  AttnArgs a = {};
+  a.q = (const bf16*)q;
+  a.q_ld = (int64_t)H * kDh;
+  a.q_n_rows = rg.cu_rows[rg.batch];
+  a.q_idx = nullptr;
+  a.slots = read_slots;
+  a.k_pool = (const bf16*)k_pool;
+  a.v_pool = (const bf16*)v_pool;
+  a.pool_ld = pool_ld;
+  a.n_slots = n_slots;
+  a.out = (bf16*)out;
+  a.lse = lse;
+  a.H = H;
+  a.Hkv = Hkv;
+  a.batch = rg.batch;
+  for (int b = 0; b <= rg.batch; ++b) {
+    a.row_start[b] = rg.cu_rows[b];
+    a.key_start[b] = rg.cu_keys[b];
+  }
+  for (int b = 0; b < rg.batch; ++b) a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
+  return launch<true>(a, s);
+}
+
+hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
+                                 int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
+                                 const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                                 const int32_t* affix_slots, int L, float* lse_out,
+                                 hipStream_t s) {
+  AttnArgs a = {};
+  a.q = (const bf16*)q;
+  a.q_ld = q_ld;
+  a.q_n_rows = q_n_rows;
+  a.q_idx = q_rows;
+  a.slots = affix_slots;
+  a.k_pool = (const bf16*)k_pool;
+  a.v_pool = nullptr;
+  a.pool_ld = pool_ld;
+  a.n_slots = n_slots;
+  a.out = nullptr;
+  a.lse = lse_out;
+  a.H = H;
+  a.Hkv = Hkv;
+  a.batch = batch;
+  for (int b = 0; b <= batch; ++b) a.row_start[b] = cu_q[b];
+  for (int b = 0; b < batch; ++b) {
+    a.key_start[b] = 0;
+    a.key_len[b] = L;
+  }
+  return launch<false>(a, s);
+}
+
+}  // namespace acache

@@ -1,0 +1,286 @@
+// bf16 MFMA GEMM for the recompute rows: C[m, n] = sum_k X[m, k] W[n, k].
+//
+// Both operands are K-contiguous (activations [M, K], weights [N, K]), so
+// each lane loads 16-byte runs along K straight into the MFMA operand
+// layout.  The weight tile feeds the MFMA A operand and the activation tile
+// the B operand: the accumulator then holds, per lane, one activation row
+// and runs of 4 consecutive output columns, which gives 8-byte output stores
+// and puts both halves of every rotary pair (columns d and d + 64 of one
+// head) in the same lane.
+//
+// Workgroup tile: 256 weight rows x 128 activation rows x 64 K, 4 waves
+// (2 x 2), each wave 128 x 64 = 4 x 2 MFMA 32x32x16 tiles.  LDS is double
+// buffered with one barrier per K step; global loads for step k+1 are in
+// flight while step k computes.  Rows are padded to 144 bytes so the
+// 16-lane groups of a ds_read_b128 hit distinct banks.  Workgroups are
+// renumbered so that each XCD (8 per chip, own L2) receives a contiguous run
+// of tiles with the M index fastest: the tiles sharing one weight tile run on
+// the same L2.
+//
+// Epilogues: plain store, accumulate, fp32 split-K partials, Q/K/V with
+// rotary embedding and the K/V store to pool slots, and SwiGLU.
+#include "device.h"
+#include "internal.h"
+
+namespace acache {
+
+namespace {
+
+constexpr int BN = 256;       // weight rows per workgroup
+constexpr int BM = 128;       // activation rows per workgroup
+constexpr int BK = 64;        // K per LDS stage
+constexpr int LDK = BK + 8;   // padded LDS row (elements)
+constexpr int kThreads = 256;
+
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
+struct TileMap {
+  int n_tiles, m_tiles, splits, k_per_split;
+};
+
+// Workgroup -> (n tile, m tile, split): XCD-contiguous, M fastest.
+__device__ __forceinline__ void tile_of(const TileMap& tm, int& nt, int& mt, int& sp) {
+  const int nb = gridDim.x;
+  const int i = blockIdx.x;
+  const int q = nb >> 3, r = nb & 7;
+  const int x = i & 7, slot = i >> 3;
+  const int t = x * q + min(x, r) + slot;
+  mt = t % tm.m_tiles;
+  const int rest = t / tm.m_tiles;
+  nt = rest % tm.n_tiles;
+  sp = rest / tm.n_tiles;
+}
+
+template <int EPI>
+__device__ __forceinline__ int weight_row(int nt, int r, int F) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    // per wave half: 64 gate rows, then the matching 64 up rows
+    const int half = r >> 7, w = r & 127;
+    const int col = nt * 128 + half * 64 + (w & 63);
+    return w < 64 ? col : F + col;
+  } else {
+    return nt * BN + r;
+  }
+}
+
+__device__ __forceinline__ void store4(bf16* p, const float v[4]) {
+  bf16x4 o;
+  o[0] = (bf16)v[0]; o[1] = (bf16)v[1]; o[2] = (bf16)v[2]; o[3] = (bf16)v[3];
+  *reinterpret_cast<bf16x4*>(p) = o;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
+  __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 sX[2][BM * LDK];
+  __shared__ double inv_freq[64];
+
+  int nt, mt, sp;
+  tile_of(tm, nt, mt, sp);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int F = p.N >> 1;
+  const bf16* __restrict__ X = (const bf16*)p.X;
+  const bf16* __restrict__ W = (const bf16*)p.W;
+  const int K = p.K;
+  const int k0 = sp * tm.k_per_split;
+  const int nk = tm.k_per_split / BK;
+
+  if constexpr (EPI == EPI_QKV) {
+    if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
+  }
+
+  // global -> register staging: 8 W chunks and 4 X chunks of 16 B per thread
+  const bf16* wsrc[8];
+  const bf16* xsrc[4];
+  int wdst[8], xdst[4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int q = tid + i * kThreads;
+    const int r = q >> 3, ch = q & 7;
+    wsrc[i] = W + (int64_t)weight_row<EPI>(nt, r, F) * K + k0 + ch * 8;
+    wdst[i] = r * LDK + ch * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int q = tid + i * kThreads;
+    const int r = q >> 3, ch = q & 7;
+    const int m = min(mt * BM + r, p.M - 1);
+    xsrc[i] = X + (int64_t)m * K + k0 + ch * 8;
+    xdst[i] = r * LDK + ch * 8;
+  }
+  u32x4 wreg[8], xreg[4];
+  auto load_global = [&](int kt) {
+    const int ko = kt * BK;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) wreg[i] = *reinterpret_cast<const u32x4*>(wsrc[i] + ko);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xreg[i] = *reinterpret_cast<const u32x4*>(xsrc[i] + ko);
+  };
+  auto store_lds = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = wreg[i];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = xreg[i];
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int arow = wn * 128 + (lane & 31);
+  const int brow = wm * 64 + (lane & 31);
+  const int kofs = (lane >> 5) * 8;
+
+  load_global(0);
+  store_lds(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_global(kt + 1);
+    const bf16* w_s = sW[buf];
+    const bf16* x_s = sX[buf];
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      bf16x8 af[4], bfr[2];
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        af[a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+        bfr[b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) acc[a][b] = mfma32x32x16(af[a], bfr[b], acc[a][b]);
+    }
+    if (kt + 1 < nk) store_lds(buf ^ 1);
+    __syncthreads();
+  }
+
+  // ------------------------------------------------------------ epilogue
+  // acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
+  const int hl = lane >> 5;
+  const int mbase = mt * BM + wm * 64 + (lane & 31);
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int m = mbase + b * 32;
+    if (m >= p.M) continue;
+    if constexpr (EPI == EPI_STORE || EPI == EPI_ACCUM || EPI == EPI_PARTIAL) {
+      const int nbase = nt * BN + wn * 128;
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int n = nbase + a * 32 + g * 8 + hl * 4;
+          float v[4] = {acc[a][b][4 * g], acc[a][b][4 * g + 1], acc[a][b][4 * g + 2], acc[a][b][4 * g + 3]};
+          if constexpr (EPI == EPI_PARTIAL) {
+            float* dst = p.P + ((int64_t)sp * p.M + m) * p.N + n;
+            f32x4 o = {v[0], v[1], v[2], v[3]};
+            *reinterpret_cast<f32x4*>(dst) = o;
+          } else {
+            bf16* dst = (bf16*)p.C + (int64_t)m * p.ldc + n;
+            if constexpr (EPI == EPI_ACCUM) {
+              const bf16x4 old = *reinterpret_cast<const bf16x4*>(dst);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) v[j] += (float)old[j];
+            }
+            store4(dst, v);
+          }
+        }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      const int cbase = nt * 128 + wn * 64;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float gt = acc[a][b][4 * g + j], up = acc[a + 2][b][4 * g + j];
+            v[j] = gt / (1.f + __expf(-gt)) * up;
+          }
+          store4((bf16*)p.C + (int64_t)m * p.ldc + cbase + a * 32 + g * 8 + hl * 4, v);
+        }
+    } else if constexpr (EPI == EPI_QKV) {
+      const int col0 = nt * BN + wn * 128;  // first weight row of this wave = one head
+      const bool is_v = col0 >= p.hq_cols + p.hkv_cols;
+      float out[4][16];
+      if (!is_v) {
+        const double ang_pos = (double)p.pos[m];
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int d = a * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
+            double ang = ang_pos * inv_freq[d];
+            ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
+            float sn, cs;
+            sincosf((float)ang, &sn, &cs);
+            const float x1 = acc[a][b][r], x2 = acc[a + 2][b][r];
+            out[a][r] = x1 * cs - x2 * sn;
+            out[a + 2][r] = x2 * cs + x1 * sn;
+          }
+      } else {
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) out[a][r] = acc[a][b][r];
+      }
+      bf16* dst;
+      if (col0 < p.hq_cols) {
+        dst = (bf16*)p.q_out + (int64_t)m * p.hq_cols + col0;
+      } else {
+        const int64_t slot = p.write_slots[m];
+        if (slot < 0 || slot >= p.n_slots) continue;
+        const int c = is_v ? col0 - p.hq_cols - p.hkv_cols : col0 - p.hq_cols;
+        dst = (bf16*)(is_v ? p.v_pool : p.k_pool) + slot * p.pool_ld + c;
+      }
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const float v[4] = {out[a][4 * g], out[a][4 * g + 1], out[a][4 * g + 2], out[a][4 * g + 3]};
+          store4(dst + a * 32 + g * 8 + hl * 4, v);
+        }
+    }
+  }
+}
+
+}  // namespace
+
+int gemm_bf16_splits(int M, int N, int K) {
+  const int tiles = ((M + BM - 1) / BM) * (N / BN);
+  const int ksteps = K / BK;
+  int best = 1;
+  // enough workgroups to cover 256 CUs about twice, K per split >= 8 steps
+  for (int s = 1; s <= 8; ++s) {
+    if (ksteps % s || ksteps / s < 8) continue;
+    best = s;
+    if (tiles * s >= 448) break;
+  }
+  return best;
+}
+
+hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {
+  TileMap tm;
+  tm.m_tiles = (p.M + BM - 1) / BM;
+  tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / 128 : p.N / BN;
+  tm.splits = epi == EPI_PARTIAL ? p.splits : 1;
+  tm.k_per_split = p.K / tm.splits;
+  const dim3 grid(tm.m_tiles * tm.n_tiles * tm.splits);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, grid, dim3(kThreads), 0, s, p, tm); break;
+    case EPI_ACCUM: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_ACCUM>, grid, dim3(kThreads), 0, s, p, tm); break;
+    case EPI_PARTIAL: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_PARTIAL>, grid, dim3(kThreads), 0, s, p, tm); break;
+    case EPI_QKV: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, grid, dim3(kThreads), 0, s, p, tm); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, dim3(kThreads), 0, s, p, tm); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace acache

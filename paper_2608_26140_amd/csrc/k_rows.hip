@@ -1,0 +1,259 @@
+// Row-level kernels: gather of recomputed rows, K/V scatter to pool slots,
+// the write/read slot maps, RMSNorm, split-K reduction with residual add and
+// RMSNorm, and the per-head reduction of probe scores.  All are HBM-bound
+// row copies or row reductions: 16-byte vector accesses, one row per
+// workgroup or grid-stride over 16-byte chunks.
+#include "device.h"
+#include "internal.h"
+
+namespace acache {
+
+namespace {
+
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
+// ---------------------------------------------------------------- gather (Section 4.3)
+__global__ __launch_bounds__(256) void gather_rows_kernel(const char* __restrict__ src, int64_t src_ld,
+                                                          int64_t src_rows, const int32_t* __restrict__ idx,
+                                                          const int32_t* __restrict__ remap, int64_t remap_len,
+                                                          int n, int chunks, char* __restrict__ dst,
+                                                          int64_t dst_ld) {
+  const int64_t total = (int64_t)n * chunks;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(c / chunks);
+    const int ch = (int)(c - (int64_t)i * chunks);
+    int64_t r = idx[i];
+    bool ok = true;
+    if (remap) {
+      ok = r >= 0 && r < remap_len;
+      r = ok ? remap[r] : 0;
+    }
+    ok = ok && r >= 0 && r < src_rows;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (ok) v = *reinterpret_cast<const u32x4*>(src + r * src_ld + (int64_t)ch * 16);
+    *reinterpret_cast<u32x4*>(dst + (int64_t)i * dst_ld + (int64_t)ch * 16) = v;
+  }
+}
+
+// ---------------------------------------------------------------- scatter (Appendix C.1 store)
+__global__ __launch_bounds__(256) void kv_scatter_kernel(const char* __restrict__ ks, const char* __restrict__ vs,
+                                                         int64_t src_ld, int n, const int32_t* __restrict__ slots,
+                                                         char* __restrict__ kp, char* __restrict__ vp,
+                                                         int64_t pool_ld, int64_t n_slots, int chunks) {
+  const int64_t total = (int64_t)n * chunks;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < total;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(c / chunks);
+    const int ch = (int)(c - (int64_t)i * chunks);
+    const int64_t slot = slots[i];
+    if (slot < 0 || slot >= n_slots) continue;
+    const int64_t so = (int64_t)i * src_ld + (int64_t)ch * 16;
+    const int64_t po = slot * pool_ld + (int64_t)ch * 16;
+    *reinterpret_cast<u32x4*>(kp + po) = *reinterpret_cast<const u32x4*>(ks + so);
+    *reinterpret_cast<u32x4*>(vp + po) = *reinterpret_cast<const u32x4*>(vs + so);
+  }
+}
+
+// ---------------------------------------------------------------- maps (Section 4.1)
+__global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, int batch,
+                                                         const int32_t* __restrict__ anchors, int k,
+                                                         int32_t* __restrict__ row_pos,
+                                                         int32_t* __restrict__ row_src,
+                                                         int32_t* __restrict__ wslots,
+                                                         int32_t* __restrict__ rslots,
+                                                         int32_t* __restrict__ q_rows) {
+  const int S = lay.seq_len, ab = lay.affix_begin, L = lay.affix_len;
+  const int ae = ab + L;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)batch * S) return;
+  const int b = (int)(t / S);
+  const int p = (int)(t - (int64_t)b * S);
+  const int R = k + S - L;
+  bool rec = true;
+  int rank;
+  if (p < ab) {
+    rank = p;
+  } else if (p >= ae) {
+    rank = ab + k + (p - ae);
+  } else {
+    // lower bound of the affix-local index among the request's anchors
+    const int a = p - ab;
+    const int32_t* an = anchors + (int64_t)b * k;
+    int lo = 0, hi = k;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (an[mid] < a) lo = mid + 1; else hi = mid;
+    }
+    rec = lo < k && an[lo] == a;
+    rank = ab + lo;
+  }
+  int32_t slot;
+  if (rec) {
+    slot = lay.private_base + b * lay.private_stride + rank;
+    const int64_t row = (int64_t)b * R + rank;
+    row_pos[row] = p;
+    row_src[row] = b * S + p;
+    wslots[row] = slot;
+    if (q_rows && p >= lay.mask_begin && p < lay.mask_begin + lay.mask_len)
+      q_rows[(int64_t)b * lay.mask_len + (p - lay.mask_begin)] = (int32_t)row;
+  } else {
+    slot = lay.shared_base + (p - ab);
+  }
+  rslots[t] = slot;
+}
+
+// ---------------------------------------------------------------- RMSNorm
+template <typename T>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, const T* __restrict__ g,
+                                                      T* __restrict__ y, int d, float eps) {
+  const int64_t row = blockIdx.x;
+  const T* xr = x + row * d;
+  T* yr = y + row * d;
+  __shared__ float red[4];
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = to_f32(xr[i]);
+    ss += v * v;
+  }
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = rsqrtf(tot / (float)d + eps);
+  for (int i = threadIdx.x; i < d; i += 256) yr[i] = from_f32<T>(to_f32(xr[i]) * inv * to_f32(g[i]));
+}
+
+// ---------------------------------------------------------------- split-K reduce + residual (+ RMSNorm)
+// One workgroup per row; each thread keeps up to 4 chunks of 8 columns in
+// registers between the residual sum and the normalisation (d <= 8192).
+__global__ __launch_bounds__(256) void reduce_residual_kernel(bf16* __restrict__ x, const float* __restrict__ part,
+                                                              int splits, int M, int d,
+                                                              const bf16* __restrict__ g,
+                                                              bf16* __restrict__ y, float eps) {
+  const int64_t row = blockIdx.x;
+  const int nch = d >> 3;
+  float v[4][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch < nch) {
+      const int64_t off = row * d + (int64_t)ch * 8;
+      const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + off);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[c][j] = (float)xv[j];
+      for (int sp = 0; sp < splits; ++sp) {
+        const float* pp = part + (int64_t)sp * M * d + off;
+        const f32x4 a = *reinterpret_cast<const f32x4*>(pp);
+        const f32x4 b = *reinterpret_cast<const f32x4*>(pp + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) { v[c][j] += a[j]; v[c][4 + j] += b[j]; }
+      }
+      bf16x8 o;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        o[j] = (bf16)v[c][j];
+        v[c][j] = (float)o[j];
+        ss += v[c][j] * v[c][j];
+      }
+      *reinterpret_cast<bf16x8*>(x + off) = o;
+    }
+  }
+  if (!y) return;
+  __shared__ float red[4];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float inv = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch < nch) {
+      const int64_t off = row * d + (int64_t)ch * 8;
+      const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + (int64_t)ch * 8);
+      bf16x8 o;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (bf16)(v[c][j] * inv * (float)gv[j]);
+      *reinterpret_cast<bf16x8*>(y + off) = o;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- probe-score head reduction (Eq. 5)
+__global__ __launch_bounds__(256) void head_reduce_kernel(const float* __restrict__ part, int batch, int H,
+                                                          int L, float* __restrict__ scores) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)batch * L) return;
+  const int b = (int)(t / L);
+  const int j = (int)(t - (int64_t)b * L);
+  const float* p = part + (int64_t)b * H * L + j;
+  float s = 0.f;
+  for (int h = 0; h < H; ++h) s += p[(int64_t)h * L];  // fixed order over heads
+  scores[t] += s;
+}
+
+inline int grid_for(int64_t work, int per_block = 256, int cap = 65535) {
+  int64_t g = (work + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  return (int)(g > cap ? cap : g);
+}
+
+}  // namespace
+
+hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
+                              const int32_t* remap, int64_t remap_len, int n, int row_bytes,
+                              void* dst, int64_t dst_ld, hipStream_t s) {
+  const int chunks = row_bytes / 16;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(grid_for((int64_t)n * chunks)), dim3(256), 0, s,
+                     (const char*)src, src_ld, src_rows, idx, remap, remap_len, n, chunks,
+                     (char*)dst, dst_ld);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_scatter(const void* k_src, const void* v_src, int64_t src_ld_bytes, int n,
+                             const int32_t* slots, void* k_pool, void* v_pool,
+                             int64_t pool_ld_bytes, int64_t n_slots, int row_bytes, hipStream_t s) {
+  const int chunks = row_bytes / 16;
+  hipLaunchKernelGGL(kv_scatter_kernel, dim3(grid_for((int64_t)n * chunks)), dim3(256), 0, s,
+                     (const char*)k_src, (const char*)v_src, src_ld_bytes, n, slots, (char*)k_pool,
+                     (char*)v_pool, pool_ld_bytes, n_slots, chunks);
+  return hipGetLastError();
+}
+
+hipError_t launch_build_maps(const acache_layout& lay, int batch, const int32_t* anchors, int k,
+                             int32_t* row_pos, int32_t* row_src, int32_t* write_slots,
+                             int32_t* read_slots, int32_t* q_rows, hipStream_t s) {
+  const int64_t work = (int64_t)batch * lay.seq_len;
+  hipLaunchKernelGGL(build_maps_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, lay,
+                     batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y, int rows, int d,
+                          float eps, hipStream_t s) {
+  if (dt == ACACHE_BF16)
+    hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x,
+                       (const bf16*)g, (bf16*)y, d, eps);
+  else
+    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x,
+                       (const float*)g, (float*)y, d, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M, int d,
+                                  const void* g, void* y, float eps, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_residual_kernel, dim3(M), dim3(256), 0, s, (bf16*)x, part, splits, M, d,
+                     (const bf16*)g, (bf16*)y, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
+                              hipStream_t s) {
+  const int64_t work = (int64_t)batch * L;
+  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, part,
+                     batch, H, L, scores);
+  return hipGetLastError();
+}
+
+}  // namespace acache

@@ -1,0 +1,111 @@
+"""The C ABI library loads and exports every entry point include/acache.h
+declares; host-side validation returns the documented status codes without
+touching a GPU.  CPU only."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "acache.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(acache_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def A():
+    from paper_2608_26140_amd import acache
+    return acache
+
+
+def test_every_declared_symbol_is_exported(A):
+    names = declared_symbols()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(A.lib, n), f"{n} declared in acache.h but not exported"
+
+
+def test_five_paper_calls_present():
+    names = declared_symbols()
+    for n in ("acache_score", "acache_topk", "acache_gather_rows", "acache_layer_recompute", "acache_kv_scatter"):
+        assert n in names
+
+
+def test_status_strings(A):
+    for st in range(7):
+        assert A.lib.acache_status_string(st)
+
+
+def test_workspace_size_validation(A):
+    good = A.make_dims(4096, 32, 32, 128, 12288, "bf16")
+    assert A.acache_workspace_size(good, 717, 1, 1024) > 717 * 4096 * 2
+    bad = A.make_dims(4096, 32, 32, 64, 12288, "bf16")  # bf16 needs head_dim 128
+    assert A.lib.acache_workspace_size(ctypes.byref(bad), 10, 1, 0) == 0
+    gqa_bad = A.make_dims(4096, 30, 4, 128, 12288, "bf16")  # 30 % 4 != 0
+    assert A.lib.acache_workspace_size(ctypes.byref(gqa_bad), 10, 1, 0) == 0
+
+
+def test_host_validation_enqueues_nothing(A):
+    """Invalid arguments return their status before any device work (these
+    calls pass NULL or bogus pointers that a launch would fault on)."""
+    lib = A.lib
+    # k > L
+    assert lib.acache_topk(None, 1, 10, 11, None, None) == 2
+    # k == 0 and batch == 0 are no-ops even with NULL pointers
+    assert lib.acache_topk(None, 1, 10, 0, None, None) == 0
+    assert lib.acache_topk(None, 0, 10, 3, None, None) == 0
+    # NULL scores with work to do
+    assert lib.acache_topk(None, 1, 10, 3, None, None) == 1
+    # L beyond the LDS capacity of one workgroup
+    assert lib.acache_topk(ctypes.c_void_p(16), 1, 20000, 3, ctypes.c_void_p(16), None) == 4
+    # gather: row bytes not a multiple of 16
+    assert lib.acache_gather_rows(ctypes.c_void_p(16), 24, 5, ctypes.c_void_p(16), None, 0, 3, 24,
+                                  ctypes.c_void_p(16), 24, None) == 2
+    # gather: misaligned destination
+    assert lib.acache_gather_rows(ctypes.c_void_p(16), 32, 5, ctypes.c_void_p(16), None, 0, 3, 32,
+                                  ctypes.c_void_p(20), 32, None) == 3
+    # scatter: unsupported dtype code
+    assert lib.acache_kv_scatter(None, None, 8, 1, None, None, None, 8, 1, 8, 7, None) == 4
+    # maps: anchors missing when k > 0; private stride too small
+    lay = A.Layout(100, 0, 60, 80, 20, 0, 60, 100)
+    assert lib.acache_build_maps(ctypes.byref(lay), 1, None, 5, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                                 ctypes.c_void_p(16), ctypes.c_void_p(16), None, None) == 1
+    lay_small = A.Layout(100, 0, 60, 80, 20, 0, 60, 30)
+    assert lib.acache_build_maps(ctypes.byref(lay_small), 1, ctypes.c_void_p(16), 5, ctypes.c_void_p(16),
+                                 ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.c_void_p(16), None, None) == 2
+    # maps: masked span overlapping the affix
+    lay_ovl = A.Layout(100, 0, 60, 50, 20, 0, 60, 100)
+    assert lib.acache_build_maps(ctypes.byref(lay_ovl), 1, None, 0, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                                 ctypes.c_void_p(16), ctypes.c_void_p(16), None, None) == 2
+
+
+def test_layer_recompute_validation(A):
+    lib = A.lib
+    dims = A.make_dims(4096, 32, 32, 128, 12288, "bf16")
+    cu_rows = (ctypes.c_int32 * 2)(0, 10)
+    cu_keys = (ctypes.c_int32 * 2)(0, 0)  # rows without keys
+    rg = A.Ragged(1, cu_rows, cu_keys)
+    w = A.LayerWeights(16, 16, 16, 16, 16, 16)
+    p = ctypes.c_void_p(16)
+    assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(rg), p, p, p, p, p, p,
+                                      4096, 100, None, p, 1 << 30, None) == 2
+    cu_keys2 = (ctypes.c_int32 * 2)(0, 20)
+    rg2 = A.Ragged(1, cu_rows, cu_keys2)
+    # workspace too small
+    assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(rg2), p, p, p, p, p, p,
+                                      4096, 100, None, p, 100, None) == 5
+    # bf16 d_ff not a multiple of 128
+    dims_bad = A.make_dims(4096, 32, 32, 128, 12200, "bf16")
+    assert lib.acache_layer_recompute(ctypes.byref(dims_bad), ctypes.byref(w), ctypes.byref(rg2), p, p, p, p, p,
+                                      p, 4096, 100, None, p, 1 << 30, None) == 4
+    # batch above 64
+    big = A.Ragged(65, cu_rows, cu_keys2)
+    assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(big), p, p, p, p, p, p,
+                                      4096, 100, None, p, 1 << 30, None) == 2

@@ -1,0 +1,227 @@
+"""GPU parity of each kernel against the fp64 oracle, through the C ABI.
+
+Sizes span several tiles with ragged tails; every case is seeded."""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import acache_oracle as O
+from tests.gpu_util import TOL, assert_close, down, down_bits, up, up_i32
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def A():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2608_26140_amd import acache
+    return acache
+
+
+def _torch():
+    import torch
+    return torch
+
+
+# ----------------------------------------------------------------------------- top-K (Eq. 6)
+
+@pytest.mark.parametrize("kind", ["normal", "ties", "signed_zero", "special", "equal"])
+@pytest.mark.parametrize("B,L,k", [(1, 128, 26), (3, 1024, 205), (2, 8192, 1638), (1, 1, 1), (2, 300, 300),
+                                   (1, 16384, 1), (4, 2048, 2047)])
+def test_topk_bit_exact(A, kind, B, L, k):
+    s = W.draw_scores(B, L, seed=L + k, kind=kind)
+    out = A.acache_topk(up(s, "f32"), k)
+    got = out.cpu().numpy()
+    for b in range(B):
+        ref = O.topk_anchors(s[b].astype(np.float64), k)
+        np.testing.assert_array_equal(got[b], ref, err_msg=f"request {b}")
+
+
+def test_topk_k_zero_is_noop(A):
+    torch = _torch()
+    s = up(W.draw_scores(1, 64, 0), "f32")
+    out = torch.full((1, 0), 7, dtype=torch.int32, device="cuda")
+    A.acache_topk(s, 0, out)
+
+
+# ----------------------------------------------------------------------------- gather / scatter
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gather_rows_with_remap(A, dtype):
+    src = W.draw_tensor((500, 384), dtype, seed=1)
+    idx = W.draw_ints(777, 0, 300, seed=2)
+    remap = W.draw_ints(300, 0, 500, seed=3)
+    g = A.acache_gather_rows(up(src, dtype), up_i32(idx))
+    np.testing.assert_array_equal(down_bits(g), src[idx])
+    g2 = A.acache_gather_rows(up(src, dtype), up_i32(idx), up_i32(remap))
+    np.testing.assert_array_equal(down_bits(g2), src[remap[idx]])
+
+
+def test_gather_out_of_range_reads_zero(A):
+    src = W.draw_tensor((10, 64), "f32", seed=4)
+    idx = np.array([0, 9, 10, -1, 3], dtype=np.int32)
+    g = down_bits(A.acache_gather_rows(up(src, "f32"), up_i32(idx)))
+    np.testing.assert_array_equal(g[[0, 1, 4]], src[[0, 9, 3]])
+    assert np.all(g[[2, 3]] == 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_kv_scatter(A, dtype):
+    torch = _torch()
+    n_slots, row = 900, 4 * 128
+    kp0 = W.draw_tensor((n_slots, row), dtype, seed=5)
+    vp0 = W.draw_tensor((n_slots, row), dtype, seed=6)
+    ks = W.draw_tensor((300, row), dtype, seed=7)
+    vs = W.draw_tensor((300, row), dtype, seed=8)
+    slots = W.draw_permutation(n_slots, seed=9)[:300]
+    slots[5] = n_slots + 3  # out of range: dropped
+    kp, vp = up(kp0, dtype), up(vp0, dtype)
+    A.acache_kv_scatter(up(ks, dtype), up(vs, dtype), up_i32(slots), kp, vp)
+    ek, ev = kp0.copy(), vp0.copy()
+    ok = slots < n_slots
+    ek[slots[ok]] = ks[ok]
+    ev[slots[ok]] = vs[ok]
+    np.testing.assert_array_equal(down_bits(kp), ek)
+    np.testing.assert_array_equal(down_bits(vp), ev)
+
+
+# ----------------------------------------------------------------------------- maps (Section 4.1)
+
+@pytest.mark.parametrize("layout,B,k", [((1536, 0, 1024, 1280, 256), 1, 205), ((192, 0, 128, 160, 32), 1, 26),
+                                        ((5120, 512, 4096, 4864, 256), 4, 819), ((2432, 0, 2048, 2176, 256), 8, 0),
+                                        ((2432, 0, 2048, 2176, 256), 3, 2048)])
+def test_build_maps(A, layout, B, k):
+    S, ab, L, mb, G = layout
+    anchors = np.stack([np.sort(W.draw_permutation(L, seed=b)[:k]) for b in range(B)]).astype(np.int32)
+    R = k + S - L
+    lay = A.Layout(S, ab, L, mb, G, 0, L, S)
+    got = A.acache_build_maps(lay, B, up_i32(anchors) if k else None, k)
+    ref = O.build_maps(S, ab, L, mb, G, anchors, 0, L, S)
+    for name, r in zip(["row_pos", "row_src", "write_slots", "read_slots", "q_rows"], ref):
+        np.testing.assert_array_equal(got[name].cpu().numpy(), r, err_msg=name)
+    assert got["row_pos"].numel() == B * R
+
+
+# ----------------------------------------------------------------------------- RMSNorm, linear
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 4096), ("f32", 256), ("bf16", 3584)])
+def test_rmsnorm(A, dtype, d):
+    x = W.draw_tensor((77, d), dtype, seed=10)
+    g = W.draw_tensor((d,), dtype, std=0.5, seed=11)
+    dims = A.make_dims(d, 32, 32, 128, 128, dtype)
+    y = A.acache_rmsnorm(dims, up(x, dtype), up(g, dtype))
+    ref = O.rms_norm(O.from_bits(x, dtype), O.from_bits(g, dtype), 1e-5)
+    assert_close(down(y), ref, dtype, "rmsnorm")
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 256, 64), (77, 512, 256), (128, 256, 4096), (717, 768, 1024), (300, 4096, 128)])
+def test_linear_bf16(A, M, N, K):
+    a = W.draw_tensor((M, K), "bf16", seed=M)
+    w = W.draw_tensor((N, K), "bf16", std=0.05, seed=N + K)
+    dims = A.make_dims(256, 2, 2, 128, 128, "bf16")
+    c = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"))
+    ref = O.from_bits(a, "bf16") @ O.from_bits(w, "bf16").T
+    assert_close(down(c), ref, "bf16", "linear")
+    c2 = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"), out=c, accumulate=True)
+    assert_close(down(c2), 2 * ref, "bf16", "linear accumulate")
+
+
+@pytest.mark.parametrize("M,N,K", [(90, 688, 256), (1, 5, 3), (65, 130, 77)])
+def test_linear_f32(A, M, N, K):
+    a = W.draw_tensor((M, K), "f32", seed=M)
+    w = W.draw_tensor((N, K), "f32", std=0.05, seed=N + K)
+    dims = A.make_dims(256, 4, 4, 64, 688, "f32")
+    c = A.acache_linear(dims, up(a, "f32"), up(w, "f32"))
+    ref = O.from_bits(a, "f32") @ O.from_bits(w, "f32").T
+    assert_close(down(c), ref, "f32", "linear")
+
+
+# ----------------------------------------------------------------------------- attention (Appendix C.1)
+
+def _attn_case(dtype, H, Hkv, dh, rows, keys, seed):
+    n_slots = sum(keys) + 37
+    q = W.draw_tensor((sum(rows), H * dh), dtype, std=1.0, seed=seed)
+    kp = W.draw_tensor((n_slots, Hkv * dh), dtype, std=1.0, seed=seed + 1)
+    vp = W.draw_tensor((n_slots, Hkv * dh), dtype, std=1.0, seed=seed + 2)
+    slots = W.draw_permutation(n_slots, seed=seed + 3)[:sum(keys)]
+    cu_rows = np.concatenate([[0], np.cumsum(rows)]).astype(int).tolist()
+    cu_keys = np.concatenate([[0], np.cumsum(keys)]).astype(int).tolist()
+    return q, kp, vp, slots, cu_rows, cu_keys, n_slots
+
+
+@pytest.mark.parametrize("dtype,H,Hkv,dh,rows,keys", [
+    ("bf16", 4, 4, 128, [717], [1536]),
+    ("bf16", 8, 2, 128, [65, 1, 130], [200, 64, 1]),
+    ("bf16", 7, 1, 128, [33, 100], [5000, 333]),
+    ("f32", 4, 4, 64, [90], [192]),
+    ("f32", 4, 2, 64, [3, 70], [1, 100]),
+])
+def test_attention(A, dtype, H, Hkv, dh, rows, keys):
+    torch = _torch()
+    q, kp, vp, slots, cu_rows, cu_keys, n_slots = _attn_case(dtype, H, Hkv, dh, rows, keys, seed=sum(rows))
+    dims = A.make_dims(256, H, Hkv, dh, 128, dtype)
+    lse = torch.empty((sum(rows), H), dtype=torch.float32, device="cuda")
+    out = A.acache_attention(dims, cu_rows, cu_keys, up(q, dtype), up_i32(slots), up(kp, dtype), up(vp, dtype),
+                             lse=lse)
+    f = lambda a: O.from_bits(a, dtype)
+    o_ref, lse_ref = O.attention_via_slots(f(q).reshape(-1, H, dh), f(kp).reshape(-1, Hkv, dh),
+                                           f(vp).reshape(-1, Hkv, dh), slots, cu_rows, cu_keys)
+    assert_close(down(out), o_ref.reshape(sum(rows), H * dh), dtype, "attention out")
+    assert_close(down(lse), lse_ref, dtype, "attention lse")
+
+
+def test_attention_rows_sum_to_one(A):
+    """V = 1 gives O = 1 exactly up to rounding: attention rows sum to one."""
+    torch = _torch()
+    dtype, H, Hkv, dh = "bf16", 4, 2, 128
+    q, kp, vp, slots, cu_rows, cu_keys, n_slots = _attn_case(dtype, H, Hkv, dh, [100, 64], [777, 65], seed=5)
+    ones = torch.ones((n_slots, Hkv * dh), dtype=torch.bfloat16, device="cuda")
+    dims = A.make_dims(256, H, Hkv, dh, 128, dtype)
+    out = A.acache_attention(dims, cu_rows, cu_keys, up(q, dtype), up_i32(slots), up(kp, dtype), ones)
+    np.testing.assert_allclose(down(out), 1.0, rtol=0, atol=2 ** -7)
+
+
+# ----------------------------------------------------------------------------- scores (Eq. 4-5)
+
+@pytest.mark.parametrize("dtype,H,Hkv,dh", [("bf16", 4, 4, 128), ("bf16", 8, 2, 128), ("f32", 4, 4, 64)])
+@pytest.mark.parametrize("norm", ["affix", "full"])
+def test_score(A, dtype, H, Hkv, dh, norm):
+    torch = _torch()
+    rows, nq, L = 300, [70, 33], 1000
+    q = W.draw_tensor((rows, H * dh), dtype, seed=20)
+    n_slots = L + 500
+    kp = W.draw_tensor((n_slots, Hkv * dh), dtype, seed=21)
+    q_rows = W.draw_permutation(rows, seed=22)[:sum(nq)]
+    cu_q = [0, nq[0], nq[0] + nq[1]]
+    affix_slots = W.draw_permutation(n_slots, seed=23)[:L]
+    f = lambda a: O.from_bits(a, dtype)
+    qf = f(q).reshape(rows, H, dh)
+    kf = f(kp).reshape(n_slots, Hkv, dh)
+    dims = A.make_dims(256, H, Hkv, dh, 128, dtype)
+    scores = torch.zeros((2, L), dtype=torch.float32, device="cuda")
+    row_lse = None
+    lse_np = None
+    if norm == "full":
+        # any per-row log-normaliser works; use the affix LSE plus a positive offset
+        lse_np = np.empty((rows, H))
+        for h in range(H):
+            lg = qf[:, h] @ kf[affix_slots, h // (H // Hkv)].T / np.sqrt(dh)
+            lse_np[:, h] = np.log(np.exp(lg - lg.max(1, keepdims=True)).sum(1)) + lg.max(1) + 0.3
+        row_lse = torch.from_numpy(lse_np.astype(np.float32)).cuda()
+        lse_np = lse_np.astype(np.float32).astype(np.float64)
+    A.acache_score(dims, up(q, dtype), up_i32(q_rows), cu_q, up(kp, dtype), up_i32(affix_slots), scores,
+                   norm=A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL, row_lse=row_lse)
+    ref = O.scores_via_slots(qf, q_rows, cu_q, kf, affix_slots, norm, lse_np)
+    assert_close(down(scores), ref, dtype, "scores")
+    if norm == "affix":
+        np.testing.assert_allclose(down(scores).sum(1), H * np.array(nq), rtol=2e-3)
+    # bit-reproducible: a second accumulation adds exactly the same values
+    s1 = scores.clone()
+    A.acache_score(dims, up(q, dtype), up_i32(q_rows), cu_q, up(kp, dtype), up_i32(affix_slots), scores,
+                   norm=A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL, row_lse=row_lse)
+    s2 = torch.zeros_like(scores)
+    A.acache_score(dims, up(q, dtype), up_i32(q_rows), cu_q, up(kp, dtype), up_i32(affix_slots), s2,
+                   norm=A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL, row_lse=row_lse)
+    assert torch.equal(s2, s1)

@@ -14,6 +14,9 @@ from .gen import (
     draw_layer_weights,
     draw_noise,
     draw_scores,
+    draw_ints,
+    draw_permutation,
+    draw_tensor,
     draw_token_ids,
     rng_for,
 )
@@ -31,6 +34,9 @@ __all__ = [
     "draw_layer_weights",
     "draw_noise",
     "draw_scores",
+    "draw_ints",
+    "draw_permutation",
+    "draw_tensor",
     "draw_token_ids",
     "rng_for",
 ]

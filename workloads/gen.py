@@ -177,3 +177,17 @@ def draw_scores(n_req: int, L: int, seed: int, kind: str = "normal") -> np.ndarr
     if kind == "equal":
         return np.full((n_req, L), 0.5, dtype=np.float32)
     raise ValueError(kind)
+
+
+def draw_tensor(shape, dtype: str, std: float = 1.0, seed: int = 0, tag: int = 0) -> np.ndarray:
+    """A test tensor N(0, std^2) in storage bits (stream 4)."""
+    return _store(_normal_f32(tuple(shape), std, 98, 4, seed, tag), dtype)
+
+
+def draw_ints(shape, low: int, high: int, seed: int = 0, tag: int = 0) -> np.ndarray:
+    """Uniform int32 in [low, high) (stream 4)."""
+    return rng_for(97, 4, seed, tag).integers(low, high, size=shape).astype(np.int32)
+
+
+def draw_permutation(n: int, seed: int = 0, tag: int = 0) -> np.ndarray:
+    return rng_for(96, 4, seed, tag).permutation(n).astype(np.int32)
