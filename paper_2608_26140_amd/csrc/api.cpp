@@ -3,6 +3,7 @@
 // here allocates device memory or synchronises the stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 
 #include "internal.h"
@@ -104,7 +105,15 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
   w.o = take(M * hq * es);
   w.h = take(M * d->d_ff * es);
   if (d->dtype == ACACHE_BF16) {
-    w.part = take(8 * M * d->d_model * sizeof(float));
+    // largest splits x rows over every row count up to `rows`, so one
+    // workspace serves any smaller call (splits change only per 128 rows)
+    size_t part_rows = 0;
+    for (int t = 1; (t - 1) * 128 < rows; ++t) {
+      const int m = std::min(rows, t * 128);
+      const int sp = std::max(gemm_bf16_splits(m, d->d_model, (int)hq), gemm_bf16_splits(m, d->d_model, d->d_ff));
+      part_rows = std::max(part_rows, (size_t)sp * (size_t)m);
+    }
+    w.part = take(part_rows * d->d_model * sizeof(float));
     w.qkv = w.gu = 0;
   } else {
     w.qkv = take(M * (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim * es);

@@ -1,0 +1,142 @@
+"""Stack driver: sequences the C-ABI calls for a batch of requests that share
+one affix (Sections 3.2, 3.3 and 4.1-4.3).
+
+    probe      build_maps(k=0) -> gather_rows -> layer_recompute with scoring
+               (every layer) -> topk                                 [Eq. 4-6]
+    refresh    build_maps(anchors) -> gather_rows -> layer_recompute x N
+    baselines  full refresh = the same calls with every affix token as an
+               anchor; direct reuse = the same calls with none
+
+Every step runs in the library's kernels; this module only allocates device
+memory (torch), fills the small host-side offset arrays and issues the calls
+on one stream, without synchronising.
+"""
+
+from __future__ import annotations
+
+from typing import List, Optional
+
+import torch
+
+from . import acache as A
+
+
+class Model:
+    """Device weights of a stack, one dict of tensors per layer
+    (attn_norm, w_qkv, w_o, mlp_norm, w_gate_up, w_down)."""
+
+    def __init__(self, dims: A.Dims, layers: List[dict]):
+        self.dims = dims
+        self.layers = layers
+        self.lw = [A.layer_weights(w) for w in layers]
+
+    @property
+    def n_layers(self) -> int:
+        return len(self.layers)
+
+    @property
+    def kv_width(self) -> int:
+        return self.dims.n_kv_heads * self.dims.head_dim
+
+    @property
+    def dtype(self):
+        return A.torch_dtype(self.dims)
+
+
+class AffixBatch:
+    """A batch of requests with one logical layout: S positions, the shared
+    affix at [affix_begin, affix_begin + L), the masked span at
+    [mask_begin, mask_begin + G).  Layer-0 inputs come from ``x_src`` rows,
+    either indexed by b * S + position (hidden rows) or through ``remap``
+    (token ids, x_src = embedding table).
+
+    KV pools: one K and one V pool per layer, [L + B * private_stride,
+    H_kv * d_h].  Slots [0, L) are the shared affix region; request b's
+    recomputed rows use [L + b * private_stride, ...) (Section 4.1)."""
+
+    def __init__(self, model: Model, seq_len: int, affix_begin: int, affix_len: int, mask_begin: int,
+                 mask_len: int, batch: int, x_src: torch.Tensor, remap: Optional[torch.Tensor] = None,
+                 private_stride: Optional[int] = None, max_rows: Optional[int] = None, device="cuda"):
+        self.model = model
+        self.S, self.ab, self.L = seq_len, affix_begin, affix_len
+        self.mb, self.G, self.B = mask_begin, mask_len, batch
+        self.stride = seq_len if private_stride is None else private_stride
+        self.x_src = x_src
+        self.remap = remap
+        self.device = device
+        self.n_slots = affix_len + batch * self.stride
+        shape = (self.n_slots, model.kv_width)
+        self.k_pools = [torch.zeros(shape, dtype=model.dtype, device=device) for _ in range(model.n_layers)]
+        self.v_pools = [torch.zeros(shape, dtype=model.dtype, device=device) for _ in range(model.n_layers)]
+        self.affix_slots = torch.arange(affix_len, dtype=torch.int32, device=device)
+        rows = batch * (seq_len if max_rows is None else max_rows)
+        self.ws = A.workspace(model.dims, rows, batch, affix_len, device)
+        self.layout = A.Layout(seq_len, affix_begin, affix_len, mask_begin, mask_len, 0, affix_len, self.stride)
+
+    # ------------------------------------------------------------------ pieces
+    def rows_per_request(self, k: int) -> int:
+        return k + self.S - self.L
+
+    def maps(self, anchors: Optional[torch.Tensor], k: int, stream=None) -> dict:
+        return A.acache_build_maps(self.layout, self.B, anchors, k, self.device, stream)
+
+    def gather_inputs(self, m: dict, stream=None) -> torch.Tensor:
+        return A.acache_gather_rows(self.x_src, m["row_src"], self.remap, stream=stream)
+
+    def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None, stream=None):
+        R = self.rows_per_request(k)
+        cu_rows = [b * R for b in range(self.B + 1)]
+        cu_keys = [b * self.S for b in range(self.B + 1)]
+        for n in range(self.model.n_layers):
+            A.acache_layer_recompute(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x, m["row_pos"],
+                                     m["write_slots"], m["read_slots"], self.k_pools[n], self.v_pools[n],
+                                     self.ws, score=score, stream=stream)
+        return x
+
+    # ------------------------------------------------------------------ the method
+    def materialize_affix(self, donor_x: torch.Tensor, donor_pos: torch.Tensor, write_slots: torch.Tensor,
+                          read_slots: torch.Tensor, stream=None) -> torch.Tensor:
+        """Materialise the shared affix cache once (Sections 3.3, 4.2): a full
+        forward of a donor sequence whose affix rows write to the shared slots.
+        donor_x [n, d] layer-0 inputs (consumed), donor_pos / write_slots [n],
+        read_slots [n_keys] (the donor's logical view)."""
+        n = donor_x.shape[0]
+        for i in range(self.model.n_layers):
+            A.acache_layer_recompute(self.model.dims, self.model.lw[i], [0, n], [0, read_slots.numel()], donor_x,
+                                     donor_pos, write_slots, read_slots, self.k_pools[i], self.v_pools[i], self.ws,
+                                     stream=stream)
+        return donor_x
+
+    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None):
+        """One-shot probe (Section 3.2): forward the non-affix rows against the
+        fixed shared affix cache and accumulate Eq. 5 over layers.  Returns
+        (scores [B, L] fp32, x rows, maps)."""
+        m = self.maps(None, 0, stream)
+        x = self.gather_inputs(m, stream)
+        scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
+        score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
+                     affix_slots=self.affix_slots, scores=scores, norm=norm)
+        self.run_layers(x, m, 0, score=score, stream=stream)
+        return scores, x, m
+
+    def select_anchors(self, k: int, norm: int = A.ACACHE_NORM_AFFIX, stream=None):
+        """Probe then Eq. 6.  Returns (anchors [B, k] int32 ascending, scores)."""
+        scores, _, _ = self.probe(norm, stream)
+        if k == 0:
+            return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
+        return A.acache_topk(scores, k, stream=stream), scores
+
+    def refresh(self, anchors: Optional[torch.Tensor], k: int, stream=None):
+        """Selective recomputation (Section 3.3): anchors plus every
+        request-specific row through all layers.  Returns (x rows [B*R, d], maps)."""
+        m = self.maps(anchors, k, stream)
+        x = self.gather_inputs(m, stream)
+        self.run_layers(x, m, k, stream=stream)
+        return x, m
+
+    def full_refresh(self, stream=None):
+        every = torch.arange(self.L, dtype=torch.int32, device=self.device).repeat(self.B, 1).contiguous()
+        return self.refresh(every, self.L, stream)
+
+    def direct_reuse(self, stream=None):
+        return self.refresh(None, 0, stream)

@@ -1,0 +1,273 @@
+"""End-to-end GPU parity of the hot path on seeded workloads, through the
+C ABI: stale affix cache, probe scores (Eq. 4-5), anchors (Eq. 6) and the
+selective refresh (Section 3.3), each against the fp64 oracle computed
+from the same input bits; plus the paper's invariants on the GPU path.
+
+Workloads: the tiny fp32 layer and the LLaDA-shaped bf16 layer at their
+full sizes, and small bf16 / fp32 stacks (prefix MHA, infix GQA)."""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import acache_oracle as O
+from tests.gpu_util import TOL, assert_close, down, down_bits, up, up_i32
+from tests.oracle_side import anchors_agree, oracle_dims, oracle_layers, oracle_request, oracle_stale
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ["tiny-f32", "llada-layer", "mini-stack", "mini-gqa-infix", "mini-f32-stack"]
+
+
+def storage_round(a: np.ndarray, dtype: str) -> np.ndarray:
+    """float64 -> storage bits of the KV cache type."""
+    return W.bf16_bits_from_f32(a.astype(np.float32)) if dtype == "bf16" else a.astype(np.float32)
+
+
+@pytest.fixture(scope="module", params=NAMES)
+def case(request):
+    """GPU setup plus the oracle.  The GPU first materialises its own stale
+    affix cache (kept in ``materialized``); then both sides switch to one
+    common stale cache, the oracle's rounded to the storage type, so the
+    probe, selection and refresh are compared on identical inputs."""
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2608_26140_amd import workload as WL
+    w = W.get_config(request.param)
+    s = WL.build(w)
+    torch.cuda.synchronize()
+    dt = w.dims.dtype
+    L = w.layout.affix_len
+    layers = oracle_layers(w, s.host)
+    sk64, sv64 = oracle_stale(w, s.host, layers)
+    materialized = [(k[:L].clone(), v[:L].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
+    sk, sv = [], []
+    for n in range(len(layers)):
+        kb, vb = storage_round(sk64[n], dt), storage_round(sv64[n], dt)
+        s.batch.k_pools[n][:L] = up(kb.reshape(L, -1), dt)
+        s.batch.v_pools[n][:L] = up(vb.reshape(L, -1), dt)
+        sk.append(O.from_bits(kb, dt))
+        sv.append(O.from_bits(vb, dt))
+    torch.cuda.synchronize()
+    s.host["materialized"] = materialized
+    s.host["stale64"] = (sk64, sv64)
+    return w, s, layers, sk, sv, OracleCache(w, s.host, layers, sk, sv)
+
+
+class OracleCache:
+    """Each oracle quantity is computed once per workload."""
+
+    def __init__(self, w, host, layers, sk, sv):
+        self.w, self.host, self.layers, self.sk, self.sv = w, host, layers, sk, sv
+        self.dims = oracle_dims(w)
+        self.memo = {}
+
+    def _get(self, key, fn):
+        if key not in self.memo:
+            self.memo[key] = fn()
+        return self.memo[key]
+
+    def req(self, b):
+        return self._get(("req", b), lambda: oracle_request(self.w, self.host, b))
+
+    def probe(self, b, norm="affix"):
+        return self._get(("probe", b, norm), lambda: O.probe(self.layers, self.dims, self.req(b), self.sk, self.sv, norm))
+
+    def anchors(self, b):
+        return self._get(("anchors", b), lambda: O.topk_anchors(self.probe(b).scores, self.w.n_anchors))
+
+    def selective(self, b):
+        return self._get(("sel", b), lambda: O.selective_refresh(self.layers, self.dims, self.req(b), self.anchors(b),
+                                                                   self.sk, self.sv))
+
+    def full(self, b):
+        return self._get(("full", b), lambda: O.full_refresh(self.layers, self.dims, self.req(b)))
+
+
+def _pool_rows(pool, slots, w):
+    d = w.dims
+    return down(pool)[np.asarray(slots)].reshape(len(slots), d.n_kv_heads, d.head_dim)
+
+
+def test_stale_cache(case):
+    """The GPU's own materialisation of the shared affix cache (a full
+    forward of the donor context) against the oracle's."""
+    w, s, layers, sk, sv, oc = case
+    sk64, sv64 = s.host["stale64"]
+    for n, (k, v) in enumerate(s.host["materialized"]):
+        assert_close(_pool_rows(k, np.arange(k.shape[0]), w), sk64[n], w.dims.dtype, f"stale K layer {n}")
+        assert_close(_pool_rows(v, np.arange(v.shape[0]), w), sv64[n], w.dims.dtype, f"stale V layer {n}")
+
+
+@pytest.mark.parametrize("norm", ["affix", "full"])
+def test_probe_scores_and_anchors(case, norm):
+    from paper_2608_26140_amd import acache as A
+    w, s, layers, sk, sv, oc = case
+    dims = oracle_dims(w)
+    dt = w.dims.dtype
+    code = A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL
+    scores, x_probe, m = s.batch.probe(code)
+    anchors = A.acache_topk(scores, w.n_anchors)
+    g_scores = down(scores)
+    g_anchors = anchors.cpu().numpy()
+    P = w.layout.n_nonaffix
+    overlaps = []
+    for b in range(w.batch):
+        res = oc.probe(b, norm)
+        assert_close(g_scores[b], res.scores, dt, f"scores request {b}")
+        assert_close(down(x_probe)[b * P:(b + 1) * P], res.x, dt, f"probe rows request {b}")
+        ref = O.topk_anchors(res.scores, w.n_anchors)
+        overlaps.append(anchors_agree(g_anchors[b], ref, res.scores, w.n_anchors, TOL[dt]))
+        if norm == "affix":
+            np.testing.assert_allclose(g_scores[b].sum(), len(layers) * w.dims.n_heads * w.layout.mask_len,
+                                       rtol=1e-3 if dt == "bf16" else 1e-5)
+    assert min(overlaps) >= 0.99, f"anchor overlap {overlaps}"
+    # anchors from the GPU scores are exactly the oracle's top-K of those scores
+    for b in range(w.batch):
+        np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], w.n_anchors))
+
+
+def test_selective_refresh_with_common_anchors(case):
+    """Both sides refresh with the oracle's anchor set."""
+    w, s, layers, sk, sv, oc = case
+    dims = oracle_dims(w)
+    dt = w.dims.dtype
+    anchors = [oc.anchors(b) for b in range(w.batch)]
+    refs = [oc.selective(b) for b in range(w.batch)]
+    x, m = s.batch.refresh(up_i32(np.stack(anchors)), w.n_anchors)
+    R = w.rows_selective
+    gx = down(x)
+    wslots = m["write_slots"].cpu().numpy()
+    for b in range(w.batch):
+        assert_close(gx[b * R:(b + 1) * R], refs[b].x, dt, f"refresh rows request {b}")
+        rows = refs[b].rows
+        for n in range(len(layers)):
+            assert_close(_pool_rows(s.batch.k_pools[n], wslots[b * R:(b + 1) * R], w), refs[b].views_k[n][rows], dt,
+                         f"fresh K request {b} layer {n}")
+            assert_close(_pool_rows(s.batch.v_pools[n], wslots[b * R:(b + 1) * R], w), refs[b].views_v[n][rows], dt,
+                         f"fresh V request {b} layer {n}")
+
+
+def test_end_to_end_own_anchors(case):
+    """GPU probe -> GPU top-K -> GPU refresh, against the oracle's own chain;
+    compared on the request-specific rows (present in both)."""
+    from paper_2608_26140_amd import acache as A
+    w, s, layers, sk, sv, oc = case
+    dims = oracle_dims(w)
+    dt = w.dims.dtype
+    anchors, _ = s.batch.select_anchors(w.n_anchors)
+    x, m = s.batch.refresh(anchors, w.n_anchors)
+    R = w.rows_selective
+    gx = down(x)
+    pos = m["row_pos"].cpu().numpy()
+    for b in range(w.batch):
+        req = oc.req(b)
+        ref = oc.selective(b)
+        pb = pos[b * R:(b + 1) * R]
+        keep = np.isin(pb, req.nonaffix)
+        keep_ref = np.isin(ref.rows, req.nonaffix)
+        assert_close(gx[b * R:(b + 1) * R][keep], ref.x[keep_ref], dt, f"end-to-end request {b}")
+
+
+def test_ratio_one_equals_full_and_ignores_stale(case):
+    """Anchor ratio 1 is full recomputation: poisoning the whole shared
+    affix cache with NaN leaves the output finite and unchanged."""
+    import torch
+    w, s, layers, sk, sv, oc = case
+    L = w.layout.affix_len
+    x_full, _ = s.batch.full_refresh()
+    ref = down(x_full).copy()
+    saved = [(k[:L].clone(), v[:L].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
+    for k, v in zip(s.batch.k_pools, s.batch.v_pools):
+        k[:L] = float("nan")
+        v[:L] = float("nan")
+    every = torch.arange(L, dtype=torch.int32, device="cuda").repeat(w.batch, 1).contiguous()
+    x_sel, _ = s.batch.refresh(every, L)
+    got = down(x_sel)
+    for (k0, v0), k, v in zip(saved, s.batch.k_pools, s.batch.v_pools):
+        k[:L] = k0
+        v[:L] = v0
+    assert np.all(np.isfinite(got))
+    np.testing.assert_array_equal(got, ref)
+    # and it matches the oracle's full recompute
+    dims = oracle_dims(w)
+    S = w.layout.seq_len
+    for b in range(w.batch):
+        r = oc.full(b)
+        assert_close(got[b * S:(b + 1) * S], r.x, w.dims.dtype, f"full refresh request {b}")
+
+
+def test_ratio_zero_equals_direct_reuse(case):
+    """Anchor ratio 0 is direct reuse: the rows and outputs of the probe
+    forward (scoring does not change them)."""
+    w, s, layers, sk, sv, oc = case
+    x0, _ = s.batch.refresh(None, 0)
+    g0 = down_bits(x0)
+    _, x_probe, _ = s.batch.probe()
+    np.testing.assert_array_equal(g0, down_bits(x_probe))
+    x1, _ = s.batch.direct_reuse()
+    np.testing.assert_array_equal(g0, down_bits(x1))
+
+
+def test_anchor_stale_poison_and_determinism(case):
+    """NaN in the stale KV of the anchor slots must not reach any output;
+    repeated runs are bit-identical."""
+    import torch
+    w, s, layers, sk, sv, oc = case
+    anchors, scores = s.batch.select_anchors(w.n_anchors)
+    anchors2, scores2 = s.batch.select_anchors(w.n_anchors)
+    assert torch.equal(scores, scores2) and torch.equal(anchors, anchors2)
+    x_a, _ = s.batch.refresh(anchors, w.n_anchors)
+    ref = down_bits(x_a).copy()
+    if w.batch == 1:
+        a = anchors[0].long()
+        saved = [(k[a].clone(), v[a].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
+        for k, v in zip(s.batch.k_pools, s.batch.v_pools):
+            k[a] = float("nan")
+            v[a] = float("nan")
+        x_p, _ = s.batch.refresh(anchors, w.n_anchors)
+        for (k0, v0), k, v in zip(saved, s.batch.k_pools, s.batch.v_pools):
+            k[a] = k0
+            v[a] = v0
+        np.testing.assert_array_equal(down_bits(x_p), ref)
+    x_b, _ = s.batch.refresh(anchors, w.n_anchors)
+    np.testing.assert_array_equal(down_bits(x_b), ref)
+
+
+def test_materialized_chain_against_oracle_chain(case):
+    """Fully independent chains: the GPU materialises its own stale cache,
+    probes, selects and refreshes; the oracle does the same in fp64.  With
+    a bf16 KV cache the stale keys differ by their storage rounding, which
+    moves near-tied scores at the K-th place: every anchor in the symmetric
+    difference must lie in the tie band, and the overlap is recorded."""
+    import torch
+    w, s, layers, sk, sv, oc = case
+    L = w.layout.affix_len
+    dt = w.dims.dtype
+    common = [(k[:L].clone(), v[:L].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
+    for (k0, v0), k, v in zip(s.host["materialized"], s.batch.k_pools, s.batch.v_pools):
+        k[:L] = k0
+        v[:L] = v0
+    try:
+        anchors, scores = s.batch.select_anchors(w.n_anchors)
+        x, m = s.batch.refresh(anchors, w.n_anchors)
+        g_scores, g_anchors, gx = down(scores), anchors.cpu().numpy(), down(x)
+        pos = m["row_pos"].cpu().numpy()
+    finally:
+        for (k0, v0), k, v in zip(common, s.batch.k_pools, s.batch.v_pools):
+            k[:L] = k0
+            v[:L] = v0
+    sk64, sv64 = s.host["stale64"]
+    dims = oracle_dims(w)
+    R = w.rows_selective
+    overlaps = []
+    for b in range(w.batch):
+        req = oc.req(b)
+        a_ref, pr = O.select_anchors(layers, dims, req, sk64, sv64, w.n_anchors)
+        assert_close(g_scores[b], pr.scores, dt, f"scores request {b}")
+        overlaps.append(anchors_agree(g_anchors[b], a_ref, pr.scores, w.n_anchors, TOL[dt]))
+        ref = O.selective_refresh(layers, dims, req, a_ref, sk64, sv64)
+        keep = np.isin(pos[b * R:(b + 1) * R], req.nonaffix)
+        assert_close(gx[b * R:(b + 1) * R][keep], ref.x[np.isin(ref.rows, req.nonaffix)], dt, f"rows request {b}")
+    print(f"\n{w.name}: anchor overlap with the oracle chain {overlaps}")
+    assert min(overlaps) >= 0.95

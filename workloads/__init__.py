@@ -9,6 +9,7 @@ from .configs import CONFIGS, ModelDims, SeqLayout, Workload, get_config
 from .gen import (
     LayerWeightsBits,
     bf16_bits_from_f32,
+    draw_donor_rows,
     draw_embedding,
     draw_hidden_rows,
     draw_layer_weights,
@@ -29,6 +30,7 @@ __all__ = [
     "get_config",
     "LayerWeightsBits",
     "bf16_bits_from_f32",
+    "draw_donor_rows",
     "draw_embedding",
     "draw_hidden_rows",
     "draw_layer_weights",

@@ -132,5 +132,30 @@ CONFIGS: Dict[str, Workload] = {
 }
 
 
+# Small stacks for parity tests at sizes the oracle finishes in seconds.
+TEST_CONFIGS: Dict[str, Workload] = {
+    "mini-stack": Workload(
+        name="mini-stack", seed_id=11,
+        dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, d_ff=1024, n_layers=3,
+                       dtype="bf16", vocab=1000),
+        layout=SeqLayout(seq_len=330, affix_begin=0, affix_len=250, mask_begin=298, mask_len=32),
+        batch=3, ratio=0.2, stale="donor"),
+    "mini-gqa-infix": Workload(
+        name="mini-gqa-infix", seed_id=12,
+        dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ff=768, n_layers=2,
+                       dtype="bf16", vocab=1000),
+        layout=SeqLayout(seq_len=300, affix_begin=40, affix_len=200, mask_begin=260, mask_len=40),
+        batch=2, ratio=0.3, stale="donor"),
+    "mini-f32-stack": Workload(
+        name="mini-f32-stack", seed_id=13,
+        dims=ModelDims(d_model=128, n_heads=4, n_kv_heads=2, head_dim=32, d_ff=256, n_layers=2,
+                       dtype="f32", vocab=500),
+        layout=SeqLayout(seq_len=150, affix_begin=20, affix_len=100, mask_begin=130, mask_len=20),
+        batch=2, ratio=0.2, stale="donor"),
+}
+
+
 def get_config(name: str) -> Workload:
+    if name in TEST_CONFIGS:
+        return TEST_CONFIGS[name]
     return CONFIGS[name]

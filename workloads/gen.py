@@ -191,3 +191,16 @@ def draw_ints(shape, low: int, high: int, seed: int = 0, tag: int = 0) -> np.nda
 
 def draw_permutation(n: int, seed: int = 0, tag: int = 0) -> np.ndarray:
     return rng_for(96, 4, seed, tag).permutation(n).astype(np.int32)
+
+
+def draw_donor_rows(w: Workload, hidden_bits: np.ndarray) -> np.ndarray:
+    """Layer-0 inputs [L, d] of the context the shared affix cache was
+    materialised in, for the "perturb" recipe: the affix rows of request 0
+    plus N(0, 0.1^2) noise, stored in the workload's type.  (Input
+    preparation only: a float add and a rounding.)"""
+    lay = w.layout
+    if w.dims.dtype == "bf16":
+        base = (hidden_bits[0, lay.affix_begin:lay.affix_end].astype(np.uint32) << np.uint32(16)).view(np.float32)
+    else:
+        base = hidden_bits[0, lay.affix_begin:lay.affix_end].astype(np.float32)
+    return _store(base + draw_noise(w), w.dims.dtype)
