@@ -1,0 +1,263 @@
+"""Benchmark of the selective affix-KV recompute hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--no-cpu]
+
+A step is one pass of the whole hot path over one batch: the one-shot probe
+(gather the non-affix rows, every layer with masked-to-affix scoring),
+top-K anchor selection, the device-side write/read slot maps, the row
+gather and the selective refresh of anchors plus request rows through every
+layer.  Inputs, weights and the shared affix cache are resident in HBM
+before the timed region.  `value` is recomputed tokens per second: the
+refresh's recomputed rows (B * R) per step divided by the step time.
+
+The JSON line also carries the full-recompute baseline timed the same way,
+the per-kernel breakdown, the dominant kernel's roofline (algorithmic
+FLOPs per launch / its mean launch duration from HIP events recorded around
+each of its launches during the timed region) and the fp64 CPU oracle timed
+on this host's cores on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"bf16": (2500.0, "mfma"), "f32": (157.3, "alu")}  # TFLOP/s, dense
+KERNELS = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "attention", "score_lse", "score_colsum",
+           "score_reduce", "rmsnorm", "residual", "topk", "gather", "maps"]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="llada-layer")
+    ap.add_argument("--ratio", type=float, default=None)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--only-step", action="store_true",
+                    help="run only the warmup and timed steps (for profilers): no breakdown, phases or CPU leg")
+    return ap.parse_args()
+
+
+def flops_model(w):
+    """Algorithmic FLOPs of one step, by kernel (see the design notes):
+    linear 2 * params / layer / row, attention 4 * S * H * d_h / row / layer,
+    probe scoring 2 passes * 2 * G * L * H * d_h / request / layer."""
+    d = w.dims
+    lay = w.layout
+    B, S, L, G, N = w.batch, lay.seq_len, lay.affix_len, lay.mask_len, d.n_layers
+    P = lay.n_nonaffix
+    R = w.rows_selective
+    hq, hkv = d.n_heads * d.head_dim, d.n_kv_heads * d.head_dim
+    per_row = {
+        "gemm_qkv": 2 * d.d_model * (hq + 2 * hkv),
+        "gemm_o": 2 * hq * d.d_model,
+        "gemm_gate_up": 2 * d.d_model * 2 * d.d_ff,
+        "gemm_down": 2 * d.d_ff * d.d_model,
+        "attention": 4 * S * hq,
+    }
+    rows = {"probe": B * P, "refresh": B * R, "full": B * S}
+    out = {}
+    for phase, m in rows.items():
+        out[phase] = {k: v * m * N for k, v in per_row.items()}
+    score = 2 * 2 * G * L * hq * B * N
+    out["probe"]["score_lse"] = score / 2
+    out["probe"]["score_colsum"] = score / 2
+    return out, rows
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (--gpus {args.gpus} requested). "
+              "Requests are independent, so N GPUs would each run this workload on their own share.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2608_26140_amd import acache as A
+    from paper_2608_26140_amd import workload as WL
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = W.get_config(args.config)
+    if args.ratio is not None:
+        w = w.with_ratio(args.ratio)
+    d, lay = w.dims, w.layout
+    K = w.n_anchors
+    B, S, L = w.batch, lay.seq_len, lay.affix_len
+    R = w.rows_selective
+    print(f"[bench] building {w.name}: layers {d.n_layers} batch {B} S {S} L {L} K {K} R {R}", file=sys.stderr,
+          flush=True)
+    t0 = time.time()
+    setup = WL.build(w, keep_host=not args.no_cpu)
+    batch = setup.batch
+    torch.cuda.synchronize()
+    print(f"[bench] setup {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    every = torch.arange(L, dtype=torch.int32, device="cuda").repeat(B, 1).contiguous()
+
+    def step():
+        anchors, _ = batch.select_anchors(K)
+        batch.refresh(anchors, K)
+
+    def select():
+        batch.select_anchors(K)
+
+    anchors_fixed, _ = batch.select_anchors(K)
+
+    def refresh():
+        batch.refresh(anchors_fixed, K)
+
+    def full():
+        batch.refresh(every, L)
+
+    def timed(fn, n):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-kernel breakdown (one armed step per kernel, outside the timed region)
+    launches_per_step = 2 * d.n_layers + 4
+    breakdown = {}
+    for kname in ([] if args.only_step else KERNELS):
+        kt = A.KernelTimer(kname, 4 * launches_per_step)
+        with kt:
+            step()
+        torch.cuda.synchronize()
+        ds = kt.durations()
+        kt.close()
+        breakdown[kname] = {"launches": len(ds), "us_per_step": 1e3 * sum(ds)}
+    dominant = max(breakdown, key=lambda k: breakdown[k]["us_per_step"]) if breakdown else "gemm_gate_up"
+
+    # timed region: K steps, the dominant kernel's launches bracketed by events
+    fl, rows = flops_model(w)
+    kt = A.KernelTimer(dominant, args.steps * launches_per_step + 8)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with kt:
+        e0.record()
+        for _ in range(args.steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    durs = kt.durations()
+    kt.close()
+    dom_flops_step = fl["probe"].get(dominant, 0) + fl["refresh"].get(dominant, 0)
+    dom_launches_step = len(durs) / args.steps
+    dom_ms_step = sum(durs) / args.steps
+
+    # phases, each timed on its own
+    if args.only_step:
+        ms_select = ms_refresh = ms_full = None
+    else:
+        ms_select = timed(select, args.steps)
+        ms_refresh = timed(refresh, args.steps)
+        ms_full = timed(full, args.steps)
+
+    peak, bound = PEAK[d.dtype]
+    step_flops = sum(fl["probe"].values()) + sum(fl["refresh"].values())
+    achieved = dom_flops_step / (dom_ms_step * 1e-3) / 1e12 if dom_ms_step > 0 else 0.0
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tfile):
+        try:
+            rec = json.load(open(tfile)).get(f"{w.name}:{dominant}")
+            from paper_2608_26140_amd.build import source_digest
+            if rec and rec.get("source_digest") == source_digest():
+                traffic = rec["bytes_per_launch"]
+        except Exception:
+            traffic = None
+
+    result = {
+        "metric": "selective-recompute latency/request + recomputed tokens/s, MFMA util vs full recompute",
+        "value": round(B * R / (ms_step * 1e-3), 1),
+        "unit": "recomputed tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": d.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": d.n_layers, "batch": B, "seq_len": S, "affix_len": L,
+                   "masked": lay.mask_len, "ratio": w.ratio, "anchors": K, "recomputed_rows": R,
+                   "probe_rows": lay.n_nonaffix, "d_model": d.d_model, "heads": d.n_heads,
+                   "kv_heads": d.n_kv_heads, "d_ff": d.d_ff},
+        "latency_ms_per_request": round(ms_step / B, 4),
+        "phases_ms": None if ms_refresh is None else {
+            "select_anchors": round(ms_select, 4), "selective_refresh": round(ms_refresh, 4),
+            "full_refresh": round(ms_full, 4)},
+        "refresh_speedup_vs_full": None if ms_refresh is None else round(ms_full / ms_refresh, 3),
+        "speedup_target_S_over_R": round(S / R, 3),
+        "step_tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 1),
+        "step_mfma_util": round(step_flops / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "refresh_mfma_util": None if ms_refresh is None else round(
+            sum(fl["refresh"].values()) / (ms_refresh * 1e-3) / 1e12 / peak, 4),
+        "full_mfma_util": None if ms_full is None else round(
+            sum(fl["full"].values()) / (ms_full * 1e-3) / 1e12 / peak, 4),
+        "kernel_us_per_step": {k: round(v["us_per_step"], 2) for k, v in breakdown.items()},
+        "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 1), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "launches_per_step": dom_launches_step,
+                     "flops_per_launch": round(dom_flops_step / max(dom_launches_step, 1)),
+                     "mean_launch_us": round(1e3 * dom_ms_step / max(dom_launches_step, 1), 2)},
+    }
+
+    if not args.no_cpu and not args.only_step:
+        result["cpu_baseline"] = cpu_baseline(w, setup.host, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(w, host, budget_s):
+    """The fp64 oracle on this host's cores: probe + top-K + selective refresh
+    of request 0 (one request of the batch), repeated until about budget_s;
+    reported as recomputed tokens/s of that sample."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import acache_oracle as O
+    from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
+
+    layers = oracle_layers(w, host)
+    sk, sv = oracle_stale(w, host, layers)
+    dims = oracle_dims(w)
+    req = oracle_request(w, host, 0)
+    n, t = 0, 0.0
+    while t < budget_s and n < 100:
+        t0 = time.perf_counter()
+        a, _ = O.select_anchors(layers, dims, req, sk, sv, w.n_anchors)
+        O.selective_refresh(layers, dims, req, a, sk, sv)
+        t += time.perf_counter() - t0
+        n += 1
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": round(n * w.rows_selective / t, 2), "unit": "recomputed tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"request 0 of {w.batch}: probe + top-K + selective refresh ({w.rows_selective} rows), "
+                      f"{n} repetitions in {t:.1f}s, fp64 NumPy"}
+
+
+if __name__ == "__main__":
+    main()

@@ -15,9 +15,10 @@
  *  - Pointers are DEVICE pointers unless marked [host].  Host arrays are read
  *    during the call only.
  *  - Ownership: the caller owns every buffer.  The library allocates and
- *    frees no device memory, keeps no global state and never synchronises;
- *    work is enqueued on `stream` and the call returns.  Buffers must stay
- *    alive until the stream has passed the work.
+ *    frees no device memory and never synchronises; work is enqueued on
+ *    `stream` and the call returns.  Buffers must stay alive until the
+ *    stream has passed the work.  The only global state is the opt-in
+ *    measurement hook (acache_time_kernel).
  *  - Errors: host-checkable faults (NULL pointers, sizes, alignment,
  *    unsupported shapes, a workspace that is too small) return a non-zero
  *    status and enqueue nothing.  A failed launch returns ACACHE_ERR_DEVICE.
@@ -242,6 +243,35 @@ acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void*
 acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,
                             int32_t M, int32_t N, int32_t K, int32_t accumulate,
                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Measurement hook (benchmarks only).  While armed for kernel `kernel`,
+ * every launch of that kernel by any entry point records starts[i] before
+ * and stops[i] after it on the launch stream, i = *count, *count + 1, ...,
+ * up to `capacity` records; the caller reads the durations with
+ * hipEventElapsedTime.  The events are the caller's (hipEventCreate).
+ * kernel == ACACHE_K_NONE disarms.  This is the library's only mutable
+ * state: arming is not thread-safe and applies to all streams. */
+typedef enum {
+  ACACHE_K_NONE = -1,
+  ACACHE_K_GEMM_QKV = 0,     /* Q/K/V projection + rotary + K/V store */
+  ACACHE_K_GEMM_O = 1,       /* output projection (split-K partials) */
+  ACACHE_K_GEMM_GATE_UP = 2, /* gate/up projection + SwiGLU */
+  ACACHE_K_GEMM_DOWN = 3,    /* down projection (split-K partials) */
+  ACACHE_K_ATTENTION = 4,    /* read-slot attention */
+  ACACHE_K_SCORE_LSE = 5,    /* probe: affix-only log-sum-exp */
+  ACACHE_K_SCORE_COLSUM = 6, /* probe: per-head column sums */
+  ACACHE_K_SCORE_REDUCE = 7, /* probe: fixed-order head reduction */
+  ACACHE_K_RMSNORM = 8,      /* RMSNorm before attention */
+  ACACHE_K_RESIDUAL = 9,     /* split-K reduction + residual (+ RMSNorm) */
+  ACACHE_K_TOPK = 10,
+  ACACHE_K_GATHER = 11,
+  ACACHE_K_MAPS = 12,
+  ACACHE_K_SCATTER = 13,
+  ACACHE_K_COUNT = 14
+} acache_kernel_id;
+acache_status acache_time_kernel(int32_t kernel, hipEvent_t* starts, hipEvent_t* stops,
+                                 int32_t capacity, int32_t* count);
 
 /* Workspace bytes needed by acache_layer_recompute, acache_score and
  * acache_linear for up to max_rows rows, `batch` requests and affix length

@@ -262,3 +262,70 @@ def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[to
     _check("acache_linear", lib.acache_linear(ctypes.byref(dims), _ptr(a), _ptr(w), _ptr(out), M, N, K,
                                               int(accumulate), None, 0, _stream(stream)))
     return out
+
+
+# ---------------------------------------------------------------------------- measurement hook
+KERNEL_IDS = {"gemm_qkv": 0, "gemm_o": 1, "gemm_gate_up": 2, "gemm_down": 3, "attention": 4, "score_lse": 5,
+              "score_colsum": 6, "score_reduce": 7, "rmsnorm": 8, "residual": 9, "topk": 10, "gather": 11,
+              "maps": 12, "scatter": 13}
+lib.acache_time_kernel.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                   ctypes.POINTER(ctypes.c_int32)]
+lib.acache_time_kernel.restype = ctypes.c_int32
+
+
+def _hip_runtime():
+    """The HIP runtime already loaded in this process (the one torch and the
+    library share)."""
+    for line in open("/proc/self/maps"):
+        if "libamdhip64" in line:
+            path = line.split()[-1]
+            rt = ctypes.CDLL(path)
+            rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+            rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            return rt
+    raise RuntimeError("HIP runtime not loaded")
+
+
+class KernelTimer:
+    """Arms acache_time_kernel for one kernel id with `capacity` event pairs;
+    durations() returns the recorded launch durations in milliseconds."""
+
+    def __init__(self, kernel: str, capacity: int):
+        self.rt = _hip_runtime()
+        self.kernel = KERNEL_IDS[kernel]
+        self.capacity = capacity
+        self.starts = (ctypes.c_void_p * capacity)()
+        self.stops = (ctypes.c_void_p * capacity)()
+        for i in range(capacity):
+            for arr in (self.starts, self.stops):
+                ev = ctypes.c_void_p()
+                if self.rt.hipEventCreate(ctypes.byref(ev)) != 0:
+                    raise RuntimeError("hipEventCreate failed")
+                arr[i] = ev
+        self.count = ctypes.c_int32(0)
+
+    def __enter__(self):
+        self.count.value = 0
+        _check("acache_time_kernel", lib.acache_time_kernel(self.kernel, self.starts, self.stops, self.capacity,
+                                                             ctypes.byref(self.count)))
+        return self
+
+    def __exit__(self, *exc):
+        lib.acache_time_kernel(-1, None, None, 0, None)
+
+    def durations(self):
+        out = []
+        for i in range(self.count.value):
+            self.rt.hipEventSynchronize(self.stops[i])
+            ms = ctypes.c_float()
+            if self.rt.hipEventElapsedTime(ctypes.byref(ms), self.starts[i], self.stops[i]) != 0:
+                raise RuntimeError("hipEventElapsedTime failed")
+            out.append(ms.value)
+        return out
+
+    def close(self):
+        for arr in (self.starts, self.stops):
+            for ev in arr:
+                self.rt.hipEventDestroy(ev)

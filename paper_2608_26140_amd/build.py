@@ -36,6 +36,20 @@ FLAGS = [
 ]
 
 
+def source_digest() -> str:
+    """sha256 over the kernel sources and the public header (identifies the
+    kernels a stored counter measurement was taken on)."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".cpp", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(CSRC, name), "rb").read())
+    h.update(open(os.path.join(ROOT, "include", "acache.h"), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def _run(cmd):
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     lines = [ln for ln in r.stdout.splitlines() if "packed-fp32-ops" not in ln]

@@ -28,6 +28,33 @@ inline size_t elem_size(acache_dtype dt) { return dt == ACACHE_BF16 ? 2 : 4; }
     if ((expr) != hipSuccess) return ACACHE_ERR_DEVICE; \
   } while (0)
 
+// Opt-in measurement hook (acache_time_kernel): events around one kernel id.
+struct KernelTimer {
+  int kernel = ACACHE_K_NONE;
+  hipEvent_t* starts = nullptr;
+  hipEvent_t* stops = nullptr;
+  int capacity = 0;
+  int32_t* count = nullptr;
+};
+KernelTimer g_timer;
+
+inline bool timed(int id) {
+  return g_timer.kernel == id && g_timer.count && *g_timer.count < g_timer.capacity;
+}
+
+// LAUNCH with the kernel's start/stop events recorded when it is armed.
+#define LAUNCH_T(id, strm, expr)                                                            \
+  do {                                                                                      \
+    const bool t_ = timed(id);                                                              \
+    if (t_ && hipEventRecord(g_timer.starts[*g_timer.count], strm) != hipSuccess)           \
+      return ACACHE_ERR_DEVICE;                                                             \
+    if ((expr) != hipSuccess) return ACACHE_ERR_DEVICE;                                     \
+    if (t_) {                                                                               \
+      if (hipEventRecord(g_timer.stops[*g_timer.count], strm) != hipSuccess) return ACACHE_ERR_DEVICE; \
+      ++*g_timer.count;                                                                     \
+    }                                                                                       \
+  } while (0)
+
 acache_status check_dims(const acache_dims* d) {
   CHECK(d, ACACHE_ERR_NULL);
   CHECK(d->dtype == ACACHE_BF16 || d->dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
@@ -144,22 +171,22 @@ acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, co
   int by_qrow = 0;
   if (norm == ACACHE_NORM_AFFIX) {
     if (d->dtype == ACACHE_BF16)
-      LAUNCH(launch_score_lse_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
+      LAUNCH_T(ACACHE_K_SCORE_LSE, s, launch_score_lse_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
                                    n_slots, affix_slots, L, lse_aff, s));
     else
-      LAUNCH(launch_score_lse_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+      LAUNCH_T(ACACHE_K_SCORE_LSE, s, launch_score_lse_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
                                   (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse_aff, s));
     lse = lse_aff;
     by_qrow = 1;
   }
   if (d->dtype == ACACHE_BF16)
-    LAUNCH(launch_score_colsum_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
+    LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
                                     n_slots, affix_slots, L, lse, by_qrow, colsum, s));
   else
-    LAUNCH(launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+    LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
                                    (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
                                    colsum, s));
-  LAUNCH(launch_head_reduce(colsum, batch, H, L, scores, s));
+  LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, H, L, scores, s));
   return ACACHE_OK;
 }
 
@@ -182,6 +209,22 @@ const char* acache_status_string(acache_status st) {
   return "unknown status";
 }
 
+acache_status acache_time_kernel(int32_t kernel, hipEvent_t* starts, hipEvent_t* stops,
+                                 int32_t capacity, int32_t* count) {
+  if (kernel == ACACHE_K_NONE) {
+    g_timer = KernelTimer();
+    return ACACHE_OK;
+  }
+  CHECK(kernel >= 0 && kernel < ACACHE_K_COUNT && capacity >= 0, ACACHE_ERR_SHAPE);
+  CHECK(count && (capacity == 0 || (starts && stops)), ACACHE_ERR_NULL);
+  g_timer.kernel = kernel;
+  g_timer.starts = starts;
+  g_timer.stops = stops;
+  g_timer.capacity = capacity;
+  g_timer.count = count;
+  return ACACHE_OK;
+}
+
 size_t acache_workspace_size(const acache_dims* dims, int32_t max_rows, int32_t batch,
                              int32_t affix_len) {
   if (check_dims(dims) != ACACHE_OK || max_rows < 0 || batch < 0 || affix_len < 0) return 0;
@@ -194,7 +237,7 @@ acache_status acache_topk(const float* scores, int32_t batch, int32_t L, int32_t
   CHECK(L <= 16384, ACACHE_ERR_UNSUPPORTED);
   if (batch == 0 || k == 0) return ACACHE_OK;
   CHECK(scores && idx_out, ACACHE_ERR_NULL);
-  LAUNCH(launch_topk(scores, batch, L, k, idx_out, stream));
+  LAUNCH_T(ACACHE_K_TOPK, stream, launch_topk(scores, batch, L, k, idx_out, stream));
   return ACACHE_OK;
 }
 
@@ -209,7 +252,7 @@ acache_status acache_gather_rows(const void* src, int64_t src_ld_bytes, int64_t 
   CHECK(!remap || remap_len >= 0, ACACHE_ERR_SHAPE);
   CHECK(aligned16(src) && aligned16(dst) && src_ld_bytes % 16 == 0 && dst_ld_bytes % 16 == 0,
         ACACHE_ERR_ALIGN);
-  LAUNCH(launch_gather_rows(src, src_ld_bytes, src_rows, idx, remap, remap_len, n, row_bytes, dst,
+  LAUNCH_T(ACACHE_K_GATHER, stream, launch_gather_rows(src, src_ld_bytes, src_rows, idx, remap, remap_len, n, row_bytes, dst,
                             dst_ld_bytes, stream));
   return ACACHE_OK;
 }
@@ -228,7 +271,7 @@ acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t sr
   CHECK(aligned16(k_src) && aligned16(v_src) && aligned16(k_pool) && aligned16(v_pool) &&
             (src_ld * es) % 16 == 0 && (pool_ld * es) % 16 == 0,
         ACACHE_ERR_ALIGN);
-  LAUNCH(launch_kv_scatter(k_src, v_src, src_ld * es, n, dst_slots, k_pool, v_pool, pool_ld * es,
+  LAUNCH_T(ACACHE_K_SCATTER, stream, launch_kv_scatter(k_src, v_src, src_ld * es, n, dst_slots, k_pool, v_pool, pool_ld * es,
                            n_slots, (int)(row_elems * es), stream));
   return ACACHE_OK;
 }
@@ -252,7 +295,7 @@ acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const i
   if (batch == 0 || S == 0) return ACACHE_OK;
   CHECK(row_pos && row_src && write_slots && read_slots, ACACHE_ERR_NULL);
   CHECK(k == 0 || anchors, ACACHE_ERR_NULL);
-  LAUNCH(launch_build_maps(*lay, batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows,
+  LAUNCH_T(ACACHE_K_MAPS, stream, launch_build_maps(*lay, batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows,
                            stream));
   return ACACHE_OK;
 }
@@ -314,10 +357,10 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
   CHECK(aligned16(q) && aligned16(k_pool) && aligned16(v_pool) && aligned16(out) && (pool_ld * es) % 16 == 0,
         ACACHE_ERR_ALIGN);
   if (dims->dtype == ACACHE_BF16)
-    LAUNCH(launch_attention_bf16(r, dims->n_heads, dims->n_kv_heads, q, read_slots, k_pool, v_pool,
+    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, dims->n_heads, dims->n_kv_heads, q, read_slots, k_pool, v_pool,
                                  pool_ld, n_slots, out, lse, stream));
   else
-    LAUNCH(launch_attention_f32(r, dims->n_heads, dims->n_kv_heads, dims->head_dim, (const float*)q,
+    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_f32(r, dims->n_heads, dims->n_kv_heads, dims->head_dim, (const float*)q,
                                 read_slots, (const float*)k_pool, (const float*)v_pool, pool_ld, n_slots,
                                 (float*)out, lse, stream));
   return ACACHE_OK;
@@ -396,7 +439,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   const bool probe = score && L > 0 && score->cu_q[r.batch] > 0;
   float* lse = (probe && score->norm == ACACHE_NORM_FULL) ? at<float>(ws, p.lse) : nullptr;
 
-  LAUNCH(launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
+  LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
   if (dims->dtype == ACACHE_BF16) {
     GemmParams g = {};
     g.X = y;
@@ -415,14 +458,14 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     g.hq_cols = hq;
     g.hkv_cols = hkv;
     g.rope_base = dims->rope_base;
-    LAUNCH(launch_gemm_bf16(EPI_QKV, g, stream));
-    LAUNCH(launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse, stream));
+    LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
+    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse, stream));
   } else {
     float* qkv = at<float>(ws, p.qkv);
-    LAUNCH(launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));
+    LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));
     LAUNCH(launch_rope_scatter_f32(qkv, M, H, Hkv, dh, pos, dims->rope_base, (float*)q, write_slots,
                                    (float*)k_pool, (float*)v_pool, pool_ld, n_slots, stream));
-    LAUNCH(launch_attention_f32(r, H, Hkv, dh, (const float*)q, read_slots, (const float*)k_pool,
+    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_f32(r, H, Hkv, dh, (const float*)q, read_slots, (const float*)k_pool,
                                 (const float*)v_pool, pool_ld, n_slots, (float*)o, lse, stream));
   }
   if (probe) {
@@ -441,8 +484,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     g.K = hq;
     g.splits = gemm_bf16_splits(M, d, hq);
     g.P = part;
-    LAUNCH(launch_gemm_bf16(EPI_PARTIAL, g, stream));
-    LAUNCH(launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
+    LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
+    LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
     GemmParams u = {};
     u.X = y;
     u.W = w->w_gate_up;
@@ -452,7 +495,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     u.splits = 1;
     u.C = hb;
     u.ldc = F;
-    LAUNCH(launch_gemm_bf16(EPI_SWIGLU, u, stream));
+    LAUNCH_T(ACACHE_K_GEMM_GATE_UP, stream, launch_gemm_bf16(EPI_SWIGLU, u, stream));
     GemmParams dn = {};
     dn.X = hb;
     dn.W = w->w_down;
@@ -461,15 +504,15 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     dn.K = F;
     dn.splits = gemm_bf16_splits(M, d, F);
     dn.P = part;
-    LAUNCH(launch_gemm_bf16(EPI_PARTIAL, dn, stream));
-    LAUNCH(launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+    LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_PARTIAL, dn, stream));
+    LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
   } else {
     float* gu = at<float>(ws, p.gu);
-    LAUNCH(launch_gemm_f32((const float*)o, (const float*)w->w_o, (float*)x, d, M, d, hq, 1, stream));
+    LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_f32((const float*)o, (const float*)w->w_o, (float*)x, d, M, d, hq, 1, stream));
     LAUNCH(launch_rmsnorm(ACACHE_F32, x, w->mlp_norm, y, M, d, dims->rms_eps, stream));
-    LAUNCH(launch_gemm_f32((const float*)y, (const float*)w->w_gate_up, gu, 2 * F, M, 2 * F, d, 0, stream));
+    LAUNCH_T(ACACHE_K_GEMM_GATE_UP, stream, launch_gemm_f32((const float*)y, (const float*)w->w_gate_up, gu, 2 * F, M, 2 * F, d, 0, stream));
     LAUNCH(launch_swiglu_f32(gu, M, F, (float*)hb, stream));
-    LAUNCH(launch_gemm_f32((const float*)hb, (const float*)w->w_down, (float*)x, d, M, d, F, 1, stream));
+    LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_f32((const float*)hb, (const float*)w->w_down, (float*)x, d, M, d, F, 1, stream));
   }
   return ACACHE_OK;
 }

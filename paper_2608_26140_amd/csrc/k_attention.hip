@@ -108,36 +108,46 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     }
   }
 
-  // staging: K 8 chunks, V 2 items of 4 keys x 8 dims per thread
+  // staging: K 8 chunks, V 2 items of 4 keys x 8 dims per thread.  The
+  // slot indices of a tile are loaded one tile ahead of its K/V rows, so
+  // issuing the row loads never waits on a dependent index load.
   u32x4 kreg[8];
   u32x4 vreg[PV ? 8 : 1];
+  int64_t kslot[8];
+  int64_t vslot[PV ? 4 : 1];
   const int64_t head_off = (int64_t)g * kDh;
   auto slot_of = [&](int key) -> int64_t {
     if (key >= S) return -1;
     const int64_t s = slots[key];
     return (s >= 0 && s < a.n_slots) ? s : -1;
   };
-  auto load_tile = [&](int t) {
+  // thread's keys in a tile: K chunk i -> key (tid >> 4) + 8 i;
+  // V items -> keys 4 (tid & 15) + r (the same for both items)
+  auto load_slots = [&](int t) {
     const int k0 = t * kTileK;
 #pragma unroll
+    for (int i = 0; i < 8; ++i) kslot[i] = slot_of(k0 + (tid >> 4) + 8 * i);
+    if constexpr (PV) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) vslot[r] = slot_of(k0 + 4 * (tid & 15) + r);
+    }
+  };
+  auto load_tile = [&]() {
+#pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int c = tid + i * kThreads;
-      const int key = c >> 4, ch = c & 15;
-      const int64_t sl = slot_of(k0 + key);
+      const int ch = (tid + i * kThreads) & 15;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (sl >= 0) v = *reinterpret_cast<const u32x4*>(a.k_pool + sl * a.pool_ld + head_off + ch * 8);
+      if (kslot[i] >= 0) v = *reinterpret_cast<const u32x4*>(a.k_pool + kslot[i] * a.pool_ld + head_off + ch * 8);
       kreg[i] = v;
     }
     if constexpr (PV) {
 #pragma unroll
       for (int it = 0; it < 2; ++it) {
-        const int item = tid + it * kThreads;
-        const int kg = item & 15, dc = item >> 4;
+        const int dc = (tid + it * kThreads) >> 4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int64_t sl = slot_of(k0 + kg * 4 + r);
           u32x4 v = {0u, 0u, 0u, 0u};
-          if (sl >= 0) v = *reinterpret_cast<const u32x4*>(a.v_pool + sl * a.pool_ld + head_off + dc * 8);
+          if (vslot[r] >= 0) v = *reinterpret_cast<const u32x4*>(a.v_pool + vslot[r] * a.pool_ld + head_off + dc * 8);
           vreg[it * 4 + r] = v;
         }
       }
@@ -181,12 +191,15 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
   const int n_tiles = (S + kTileK - 1) / kTileK;
   const int krow = key_perm(lane & 31);
 
-  load_tile(0);
+  load_slots(0);
+  load_tile();
+  if (n_tiles > 1) load_slots(1);
   store_tile(0);
   __syncthreads();
   for (int t = 0; t < n_tiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1);
+    if (t + 1 < n_tiles) load_tile();
+    if (t + 2 < n_tiles) load_slots(t + 2);
     const bf16* ks = sK[buf];
     f32x16 st[2];
 #pragma unroll

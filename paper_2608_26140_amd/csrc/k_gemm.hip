@@ -19,6 +19,8 @@
 //
 // Epilogues: plain store, accumulate, fp32 split-K partials, Q/K/V with
 // rotary embedding and the K/V store to pool slots, and SwiGLU.
+#include <cstdlib>
+
 #include "device.h"
 #include "internal.h"
 
@@ -26,11 +28,26 @@ namespace acache {
 
 namespace {
 
-constexpr int BN = 256;       // weight rows per workgroup
-constexpr int BM = 128;       // activation rows per workgroup
-constexpr int BK = 64;        // K per LDS stage
-constexpr int LDK = BK + 8;   // padded LDS row (elements)
-constexpr int kThreads = 256;
+// Tile configurations.  Every wave covers 128 weight rows (one attention
+// head, or 64 gate + 64 up rows) and WAVE_M activation rows.
+template <int BN_, int BM_, int WN_, int WM_, int BK_>
+struct Cfg {
+  static constexpr int BN = BN_;       // weight rows per workgroup
+  static constexpr int BM = BM_;       // activation rows per workgroup
+  static constexpr int WN = WN_;       // waves along N
+  static constexpr int WM = WM_;       // waves along M
+  static constexpr int BK = BK_;       // K per LDS stage
+  static constexpr int LDK = BK + 8;   // padded LDS row (elements)
+  static constexpr int THREADS = 64 * WN * WM;
+  static constexpr int WAVE_M = BM / WM;
+  static constexpr int FM = WAVE_M / 32;  // activation fragments per wave
+  static constexpr int CPR = BK / 8;      // 16-byte chunks per row
+  static constexpr int W_CHUNKS = BN * CPR / THREADS;
+  static constexpr int X_CHUNKS = BM * CPR / THREADS;
+  static_assert(BN / WN == 128, "a wave spans 128 weight rows");
+  static_assert(WAVE_M % 32 == 0 && FM >= 1, "wave M extent");
+  static_assert(BN * CPR % THREADS == 0 && BM * CPR % THREADS == 0, "load split");
+};
 
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -51,12 +68,12 @@ __device__ __forceinline__ void tile_of(const TileMap& tm, int& nt, int& mt, int
   sp = rest / tm.n_tiles;
 }
 
-template <int EPI>
+template <int EPI, int BN>
 __device__ __forceinline__ int weight_row(int nt, int r, int F) {
   if constexpr (EPI == EPI_SWIGLU) {
     // per wave half: 64 gate rows, then the matching 64 up rows
     const int half = r >> 7, w = r & 127;
-    const int col = nt * 128 + half * 64 + (w & 63);
+    const int col = nt * (BN / 2) + half * 64 + (w & 63);
     return w < 64 ? col : F + col;
   } else {
     return nt * BN + r;
@@ -69,8 +86,9 @@ __device__ __forceinline__ void store4(bf16* p, const float v[4]) {
   *reinterpret_cast<bf16x4*>(p) = o;
 }
 
-template <int EPI>
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
+template <int EPI, class C>
+__global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
+  constexpr int BN = C::BN, BM = C::BM, BK = C::BK, LDK = C::LDK, FM = C::FM;
   __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDK];
   __shared__ __attribute__((aligned(16))) bf16 sX[2][BM * LDK];
   __shared__ double inv_freq[64];
@@ -78,7 +96,7 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
   int nt, mt, sp;
   tile_of(tm, nt, mt, sp);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave & 1, wm = wave >> 1;
+  const int wn = wave % C::WN, wm = wave / C::WN;
   const int F = p.N >> 1;
   const bf16* __restrict__ X = (const bf16*)p.X;
   const bf16* __restrict__ W = (const bf16*)p.W;
@@ -90,51 +108,65 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
     if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
   }
 
-  // global -> register staging: 8 W chunks and 4 X chunks of 16 B per thread
-  const bf16* wsrc[8];
-  const bf16* xsrc[4];
-  int wdst[8], xdst[4];
+  // global -> register staging, 16 B chunks
+  const bf16* wsrc[C::W_CHUNKS];
+  const bf16* xsrc[C::X_CHUNKS];
+  int wdst[C::W_CHUNKS], xdst[C::X_CHUNKS];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int q = tid + i * kThreads;
-    const int r = q >> 3, ch = q & 7;
-    wsrc[i] = W + (int64_t)weight_row<EPI>(nt, r, F) * K + k0 + ch * 8;
+  for (int i = 0; i < C::W_CHUNKS; ++i) {
+    const int q = tid + i * C::THREADS;
+    const int r = q / C::CPR, ch = q % C::CPR;
+    wsrc[i] = W + (int64_t)weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
     wdst[i] = r * LDK + ch * 8;
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = tid + i * kThreads;
-    const int r = q >> 3, ch = q & 7;
+  for (int i = 0; i < C::X_CHUNKS; ++i) {
+    const int q = tid + i * C::THREADS;
+    const int r = q / C::CPR, ch = q % C::CPR;
     const int m = min(mt * BM + r, p.M - 1);
     xsrc[i] = X + (int64_t)m * K + k0 + ch * 8;
     xdst[i] = r * LDK + ch * 8;
   }
-  u32x4 wreg[8], xreg[4];
+  u32x4 wreg[C::W_CHUNKS], xreg[C::X_CHUNKS];
   auto load_global = [&](int kt) {
     const int ko = kt * BK;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) wreg[i] = *reinterpret_cast<const u32x4*>(wsrc[i] + ko);
+    for (int i = 0; i < C::W_CHUNKS; ++i) wreg[i] = *reinterpret_cast<const u32x4*>(wsrc[i] + ko);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xreg[i] = *reinterpret_cast<const u32x4*>(xsrc[i] + ko);
+    for (int i = 0; i < C::X_CHUNKS; ++i) xreg[i] = *reinterpret_cast<const u32x4*>(xsrc[i] + ko);
   };
   auto store_lds = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = wreg[i];
+    for (int i = 0; i < C::W_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = wreg[i];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = xreg[i];
+    for (int i = 0; i < C::X_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = xreg[i];
   };
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][FM];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < FM; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
   const int arow = wn * 128 + (lane & 31);
-  const int brow = wm * 64 + (lane & 31);
+  const int brow = wm * C::WAVE_M + (lane & 31);
   const int kofs = (lane >> 5) * 8;
+
+  // MFMA fragments are double buffered in registers: the reads of k step
+  // s+1 are issued before the MFMAs of step s, so LDS latency overlaps with
+  // matrix work instead of stalling the wave.
+  constexpr int KS = BK / 16;
+  bf16x8 af[2][4], bfr[2][FM];
+  auto read_frags = [&](const bf16* w_s, const bf16* x_s, int s, int slot) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+      af[slot][a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
+#pragma unroll
+    for (int b = 0; b < FM; ++b)
+      bfr[slot][b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
+  };
 
   load_global(0);
   store_lds(0);
@@ -144,19 +176,16 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
     if (kt + 1 < nk) load_global(kt + 1);
     const bf16* w_s = sW[buf];
     const bf16* x_s = sX[buf];
+    read_frags(w_s, x_s, 0, 0);
 #pragma unroll
-    for (int s = 0; s < BK / 16; ++s) {
-      bf16x8 af[4], bfr[2];
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-        af[a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-        bfr[b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
+    for (int s = 0; s < KS; ++s) {
+      if (s + 1 < KS) read_frags(w_s, x_s, s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int a = 0; a < 4; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b) acc[a][b] = mfma32x32x16(af[a], bfr[b], acc[a][b]);
+        for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[s & 1][a], bfr[s & 1][b], acc[a][b]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (kt + 1 < nk) store_lds(buf ^ 1);
     __syncthreads();
@@ -165,9 +194,9 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
   // ------------------------------------------------------------ epilogue
   // acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
   const int hl = lane >> 5;
-  const int mbase = mt * BM + wm * 64 + (lane & 31);
+  const int mbase = mt * BM + wm * C::WAVE_M + (lane & 31);
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
+  for (int b = 0; b < FM; ++b) {
     const int m = mbase + b * 32;
     if (m >= p.M) continue;
     if constexpr (EPI == EPI_STORE || EPI == EPI_ACCUM || EPI == EPI_PARTIAL) {
@@ -193,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
           }
         }
     } else if constexpr (EPI == EPI_SWIGLU) {
-      const int cbase = nt * 128 + wn * 64;
+      const int cbase = nt * (BN / 2) + wn * 64;
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -253,34 +282,65 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams p, TileM
 
 }  // namespace
 
-int gemm_bf16_splits(int M, int N, int K) {
-  const int tiles = ((M + BM - 1) / BM) * (N / BN);
-  const int ksteps = K / BK;
+using CfgSmall = Cfg<256, 128, 2, 2, 64>;   // 4 waves, 1 per SIMD
+using CfgWide = Cfg<256, 256, 2, 4, 64>;    // 8 waves, 2 per SIMD
+using CfgDeep = Cfg<512, 128, 4, 2, 32>;    // 8 waves, 2 per SIMD, BK 32
+
+int gemm_cfg() {
+  static int c = [] {
+    const char* e = getenv("ACACHE_GEMM_CFG");
+    return e ? atoi(e) : 0;
+  }();
+  return c;
+}
+
+template <class C>
+int splits_for(int M, int N, int K) {
+  const int tiles = ((M + C::BM - 1) / C::BM) * (N / C::BN);
+  const int ksteps = K / C::BK;
   int best = 1;
-  // enough workgroups to cover 256 CUs about twice, K per split >= 8 steps
+  // enough workgroups to cover 256 CUs about twice, K per split >= 512
   for (int s = 1; s <= 8; ++s) {
-    if (ksteps % s || ksteps / s < 8) continue;
+    if (ksteps % s || (K / s) < 512) continue;
     best = s;
     if (tiles * s >= 448) break;
   }
   return best;
 }
 
-hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {
+int gemm_bf16_splits(int M, int N, int K) {
+  switch (gemm_cfg()) {
+    case 1: return splits_for<CfgWide>(M, N, K);
+    case 2: return splits_for<CfgDeep>(M, N, K);
+    default: return splits_for<CfgSmall>(M, N, K);
+  }
+}
+
+template <class C>
+hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
   TileMap tm;
-  tm.m_tiles = (p.M + BM - 1) / BM;
-  tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / 128 : p.N / BN;
+  tm.m_tiles = (p.M + C::BM - 1) / C::BM;
+  tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / (C::BN / 2) : p.N / C::BN;
   tm.splits = epi == EPI_PARTIAL ? p.splits : 1;
   tm.k_per_split = p.K / tm.splits;
   const dim3 grid(tm.m_tiles * tm.n_tiles * tm.splits);
+  const dim3 block(C::THREADS);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_STORE>, grid, dim3(kThreads), 0, s, p, tm); break;
-    case EPI_ACCUM: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_ACCUM>, grid, dim3(kThreads), 0, s, p, tm); break;
-    case EPI_PARTIAL: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_PARTIAL>, grid, dim3(kThreads), 0, s, p, tm); break;
-    case EPI_QKV: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_QKV>, grid, dim3(kThreads), 0, s, p, tm); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL(gemm_bf16_kernel<EPI_SWIGLU>, grid, dim3(kThreads), 0, s, p, tm); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
+    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
+    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {
+  switch (gemm_cfg()) {
+    case 1: return launch_cfg<CfgWide>(epi, p, s);
+    case 2: return launch_cfg<CfgDeep>(epi, p, s);
+    default: return launch_cfg<CfgSmall>(epi, p, s);
+  }
 }
 
 }  // namespace acache

@@ -63,15 +63,15 @@ __global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
 
   const int q0 = a.cu_q[b], nq = a.cu_q[b + 1] - q0;
   float col[2] = {0.f, 0.f};
-  for (int t = 0; t < nq; t += 32) {
-    // A operand: Q[query t + lane%32][16 s + 8 hl .. +7]
+  // query tile t: A operand Q[query t + lane%32][16 s + 8 hl .. +7].  Row
+  // indices run two tiles ahead and Q fragments one tile ahead of the MFMAs.
+  auto row_of = [&](int t) -> int64_t {
     const int qi = t + (lane & 31);
-    int64_t row = -1;
-    if (qi < nq) {
-      row = a.q_rows[q0 + qi];
-      if (row < 0 || row >= a.q_n_rows) row = -1;
-    }
-    bf16x8 qf[8];
+    if (qi >= nq) return -1;
+    const int64_t r = a.q_rows[q0 + qi];
+    return (r >= 0 && r < a.q_n_rows) ? r : -1;
+  };
+  auto load_q = [&](int64_t row, bf16x8* qf) {
     const bf16* qp = a.q + (row < 0 ? 0 : row) * a.q_ld + (int64_t)h * kDh + hl * 8;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -79,6 +79,13 @@ __global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
       if (row >= 0) v = *reinterpret_cast<const u32x4*>(qp + s * 16);
       qf[s] = __builtin_bit_cast(bf16x8, v);
     }
+  };
+  bf16x8 qcur[8], qnext[8];
+  int64_t row_next = row_of(32);
+  load_q(row_of(0), qcur);
+  for (int t = 0; t < nq; t += 32) {
+    if (t + 32 < nq) load_q(row_next, qnext);
+    if (t + 64 < nq) row_next = row_of(t + 64);
     // log-sum-exp (base 2) of the 16 queries this lane's registers hold
     float lse2[16];
 #pragma unroll
@@ -97,12 +104,14 @@ __global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) acc = mfma32x32x16(qf[s], kf[sub][s], acc);
+      for (int s = 0; s < 8; ++s) acc = mfma32x32x16(qcur[s], kf[sub][s], acc);
       float cs = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) cs += exp2f(acc[r] * scale - lse2[r]);
       col[sub] += cs;
     }
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qcur[s] = qnext[s];
   }
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
