@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--only-step", action="store_true",
                     help="run only the warmup and timed steps (for profilers): no breakdown, phases or CPU leg")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="instead of the workload, run the row-gather kernel as a plain copy of MIB MiB "
+                         "--steps times (the known-size reference for the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -90,6 +93,9 @@ def main():
     from paper_2608_26140_amd import workload as WL
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        copy_calibration(args, A)
+        return
     w = W.get_config(args.config)
     if args.ratio is not None:
         w = w.with_ratio(args.ratio)
@@ -229,6 +235,32 @@ def main():
     if not args.no_cpu and not args.only_step:
         result["cpu_baseline"] = cpu_baseline(w, setup.host, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def copy_calibration(args, A):
+    """Identity row gather of MIB MiB: each launch reads every source row once
+    (plus one int32 index per row) and writes it once."""
+    import torch
+    row = 8192
+    n = args.copy_calibration * (1 << 20) // row
+    src = torch.randint(0, 256, (n, row), dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    idx = torch.arange(n, dtype=torch.int32, device="cuda")
+    for _ in range(args.warmup):
+        A.acache_gather_rows(src, idx, out=dst)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        A.acache_gather_rows(src, idx, out=dst)
+    e1.record()
+    torch.cuda.synchronize()
+    assert torch.equal(src, dst)
+    ms = e0.elapsed_time(e1) / args.steps
+    print(json.dumps({"copy_calibration": {"kernel": "gather_rows_kernel", "bytes_read": n * row + 4 * n,
+                                           "bytes_written": n * row, "launches": args.warmup + args.steps,
+                                           "ms_per_launch": round(ms, 4),
+                                           "GB_per_s": round(2 * n * row / (ms * 1e-3) / 1e9, 1)}}), flush=True)
 
 
 def cpu_baseline(w, host, budget_s):

@@ -133,7 +133,8 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
   w.h = take(M * d->d_ff * es);
   if (d->dtype == ACACHE_BF16) {
     // largest splits x rows over every row count up to `rows`, so one
-    // workspace serves any smaller call (splits change only per 128 rows)
+    // workspace serves any smaller call (splits change only at row-tile
+    // boundaries, every one of which is a multiple of 128 rows)
     size_t part_rows = 0;
     for (int t = 1; (t - 1) * 128 < rows; ++t) {
       const int m = std::min(rows, t * 128);
@@ -353,6 +354,7 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
   if (rows == 0) return ACACHE_OK;
   CHECK(q && read_slots && k_pool && v_pool && out, ACACHE_ERR_NULL);
   CHECK(pool_ld >= (int64_t)dims->n_kv_heads * dims->head_dim && n_slots >= 0, ACACHE_ERR_SHAPE);
+  CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);  // 32-bit element offsets
   const int64_t es = (int64_t)elem_size(dims->dtype);
   CHECK(aligned16(q) && aligned16(k_pool) && aligned16(v_pool) && aligned16(out) && (pool_ld * es) % 16 == 0,
         ACACHE_ERR_ALIGN);
@@ -385,6 +387,7 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
   CHECK(norm == ACACHE_NORM_FULL ? row_lse != nullptr : row_lse == nullptr, ACACHE_ERR_NULL);
   CHECK(q_ld >= (int64_t)dims->n_heads * dims->head_dim && q_n_rows >= 0, ACACHE_ERR_SHAPE);
   CHECK(pool_ld >= (int64_t)dims->n_kv_heads * dims->head_dim && n_slots >= 0, ACACHE_ERR_SHAPE);
+  CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);  // 32-bit element offsets
   const int64_t es = (int64_t)elem_size(dims->dtype);
   CHECK(aligned16(q) && aligned16(k_pool) && (q_ld * es) % 16 == 0 && (pool_ld * es) % 16 == 0,
         ACACHE_ERR_ALIGN);
@@ -415,6 +418,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
             F = dims->d_ff;
   const int hq = H * dh, hkv = Hkv * dh, nqkv = (H + 2 * Hkv) * dh;
   CHECK(pool_ld >= hkv && n_slots > 0, ACACHE_ERR_SHAPE);
+  CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);  // 32-bit element offsets
   const int64_t es = (int64_t)elem_size(dims->dtype);
   CHECK(aligned16(x) && aligned16(k_pool) && aligned16(v_pool) && (pool_ld * es) % 16 == 0, ACACHE_ERR_ALIGN);
   CHECK(aligned16(w->attn_norm) && aligned16(w->w_qkv) && aligned16(w->w_o) && aligned16(w->mlp_norm) &&

@@ -70,8 +70,19 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[2][kTileK * kLdK];
   __shared__ __attribute__((aligned(16))) bf16 sV[PV ? 2 : 1][PV ? kDh * kLdV : 8];
 
-  // request of this workgroup
-  const int tile = blockIdx.x;
+  // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
+  // renumber them so each XCD gets a contiguous run of the head-major
+  // logical order: all query tiles of a head (and the heads sharing a KV
+  // head) run on one XCD and fetch that head's K/V into one L2.
+  const int n_tiles_q = a.tile_start[a.batch];
+  int h, tile;
+  {
+    const int nb = gridDim.x, i = blockIdx.x;
+    const int q8 = nb >> 3, r8 = nb & 7, x = i & 7;
+    const int t = x * q8 + min(x, r8) + (i >> 3);
+    h = t / n_tiles_q;
+    tile = t - h * n_tiles_q;
+  }
   int b = 0;
   {
     int lo = 0, hi = a.batch - 1;
@@ -81,7 +92,6 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     }
     b = lo;
   }
-  const int h = blockIdx.y;
   const int g = h / (a.H / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
   const int n_rows = a.row_start[b + 1] - a.row_start[b];
@@ -110,45 +120,59 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
 
   // staging: K 8 chunks, V 2 items of 4 keys x 8 dims per thread.  The
   // slot indices of a tile are loaded one tile ahead of its K/V rows, so
-  // issuing the row loads never waits on a dependent index load.
+  // issuing the row loads never waits on a dependent index load.  Offsets
+  // are 32-bit element offsets (the host checks n_slots * pool_ld < 2^31);
+  // an absent key (past the end, or an out-of-range slot) reads slot 0 and
+  // its data is zeroed, so the loads need no branches.
   u32x4 kreg[8];
   u32x4 vreg[PV ? 8 : 1];
-  int64_t kslot[8];
-  int64_t vslot[PV ? 4 : 1];
-  const int64_t head_off = (int64_t)g * kDh;
-  auto slot_of = [&](int key) -> int64_t {
-    if (key >= S) return -1;
-    const int64_t s = slots[key];
-    return (s >= 0 && s < a.n_slots) ? s : -1;
+  int kslot[8];
+  int vslot[PV ? 4 : 1];
+  const int head_off = g * kDh;
+  const int pool_ld = (int)a.pool_ld;
+  // Raw slot loads only (clamped index, unconditional): nothing consumes
+  // them until the next tile, so no wait is placed behind the K/V loads.
+  auto raw_slot = [&](int key) -> int { return slots[min(key, S - 1)]; };
+  // element offset of a key's row, or -1 when the key is absent
+  auto off_of = [&](int key, int slot) -> int {
+    return (key < S && slot >= 0 && slot < a.n_slots) ? slot * pool_ld + head_off : -1;
   };
+  int tile_loaded = 0;  // tile whose slots sit in kslot / vslot
   // thread's keys in a tile: K chunk i -> key (tid >> 4) + 8 i;
   // V items -> keys 4 (tid & 15) + r (the same for both items)
   auto load_slots = [&](int t) {
     const int k0 = t * kTileK;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) kslot[i] = slot_of(k0 + (tid >> 4) + 8 * i);
+    for (int i = 0; i < 8; ++i) kslot[i] = raw_slot(k0 + (tid >> 4) + 8 * i);
     if constexpr (PV) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) vslot[r] = slot_of(k0 + 4 * (tid & 15) + r);
+      for (int r = 0; r < 4; ++r) vslot[r] = raw_slot(k0 + 4 * (tid & 15) + r);
     }
+    tile_loaded = t;
   };
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  // absent keys of the staged tile, applied (zeroed) when the stage is
+  // written to LDS, so the loaded registers are not consumed early
+  unsigned absent = 0;
   auto load_tile = [&]() {
+    const int k0 = tile_loaded * kTileK;
+    absent = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int ch = (tid + i * kThreads) & 15;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (kslot[i] >= 0) v = *reinterpret_cast<const u32x4*>(a.k_pool + kslot[i] * a.pool_ld + head_off + ch * 8);
-      kreg[i] = v;
+      const int off = off_of(k0 + (tid >> 4) + 8 * i, kslot[i]);
+      absent |= (off < 0 ? 1u : 0u) << i;
+      kreg[i] = *reinterpret_cast<const u32x4*>(a.k_pool + (off < 0 ? 0 : off) + ch * 8);
     }
     if constexpr (PV) {
 #pragma unroll
-      for (int it = 0; it < 2; ++it) {
-        const int dc = (tid + it * kThreads) >> 4;
+      for (int r = 0; r < 4; ++r) {
+        const int off = off_of(k0 + 4 * (tid & 15) + r, vslot[r]);
+        absent |= (off < 0 ? 1u : 0u) << (8 + r);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          u32x4 v = {0u, 0u, 0u, 0u};
-          if (vslot[r] >= 0) v = *reinterpret_cast<const u32x4*>(a.v_pool + vslot[r] * a.pool_ld + head_off + dc * 8);
-          vreg[it * 4 + r] = v;
+        for (int it = 0; it < 2; ++it) {
+          const int dc = (tid + it * kThreads) >> 4;
+          vreg[it * 4 + r] = *reinterpret_cast<const u32x4*>(a.v_pool + (off < 0 ? 0 : off) + dc * 8);
         }
       }
     }
@@ -158,17 +182,17 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     for (int i = 0; i < 8; ++i) {
       const int c = tid + i * kThreads;
       const int key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sK[buf][key * kLdK + ch * 8]) = kreg[i];
+      *reinterpret_cast<u32x4*>(&sK[buf][key * kLdK + ch * 8]) = (absent >> i) & 1u ? zero4 : kreg[i];
     }
     if constexpr (PV) {
 #pragma unroll
       for (int it = 0; it < 2; ++it) {
         const int item = tid + it * kThreads;
         const int kg = item & 15, dc = item >> 4;
-        const bf16x8 v0 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 0]);
-        const bf16x8 v1 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 1]);
-        const bf16x8 v2 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 2]);
-        const bf16x8 v3 = __builtin_bit_cast(bf16x8, vreg[it * 4 + 3]);
+        const bf16x8 v0 = __builtin_bit_cast(bf16x8, (absent >> 8) & 1u ? zero4 : vreg[it * 4 + 0]);
+        const bf16x8 v1 = __builtin_bit_cast(bf16x8, (absent >> 9) & 1u ? zero4 : vreg[it * 4 + 1]);
+        const bf16x8 v2 = __builtin_bit_cast(bf16x8, (absent >> 10) & 1u ? zero4 : vreg[it * 4 + 2]);
+        const bf16x8 v3 = __builtin_bit_cast(bf16x8, (absent >> 11) & 1u ? zero4 : vreg[it * 4 + 3]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           bf16x4 w;
@@ -204,45 +228,65 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     f32x16 st[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      // all 8 K fragments of this 32-key block are read before its MFMAs
+      bf16x8 kf[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        kf[s] = *reinterpret_cast<const bf16x8*>(ks + (kb * 32 + krow) * kLdK + s * 16 + hl * 8);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int r = 0; r < 16; ++r) st[kb][r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const bf16x8 af = *reinterpret_cast<const bf16x8*>(ks + (kb * 32 + krow) * kLdK + s * 16 + hl * 8);
-        st[kb] = mfma32x32x16(af, qf[s], st[kb]);
-      }
+      for (int s = 0; s < 8; ++s) st[kb] = mfma32x32x16(kf[s], qf[s], st[kb]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     // register r of block kb holds key kb*32 + 16(r/8) + 8 hl + r%8
     const int kt0 = t * kTileK;
     float mx = -INFINITY;
+    if (kt0 + kTileK <= S) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
-        const float u = key < S ? st[kb][r] * scale : -INFINITY;
-        st[kb][r] = u;
-        mx = fmaxf(mx, u);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kb][r]);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
+          st[kb][r] = key < S ? st[kb][r] : -INFINITY;
+          mx = fmaxf(mx, st[kb][r]);
+        }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale;
+    // The running max moves only when a tile's max exceeds it by more than
+    // 2^8; exp2(u - m) then stays <= 256 (exact in fp32 and bf16), and the
+    // final normalisation uses the same m, so the result is unchanged.
+    const bool bump = mx > m_run + 8.f;
+    float alpha = 1.f;
+    if (__builtin_amdgcn_ballot_w64(bump)) {
+      const float m_new = bump ? mx : m_run;
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+      if constexpr (PV) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    }
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = exp2f(st[kb][r] - m_new);
+        const float e = __builtin_amdgcn_exp2f(fmaf(st[kb][r], scale, -m_run));
         st[kb][r] = e;
         psum += e;
       }
-    l_part = l_part * alpha + psum;
-    m_run = m_new;
+    l_part += psum;
     if constexpr (PV) {
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
       const bf16* vs = sV[buf];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -291,7 +335,7 @@ hipError_t launch(AttnArgs& a, hipStream_t s) {
   }
   a.tile_start[a.batch] = tiles;
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(attention_kernel<PV>, dim3(tiles, a.H), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL(attention_kernel<PV>, dim3(tiles * a.H), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -30,8 +30,9 @@ namespace {
 
 // Tile configurations.  Every wave covers 128 weight rows (one attention
 // head, or 64 gate + 64 up rows) and WAVE_M activation rows.
-template <int BN_, int BM_, int WN_, int WM_, int BK_>
+template <int BN_, int BM_, int WN_, int WM_, int BK_, int STAGES_ = 2>
 struct Cfg {
+  static constexpr int STAGES = STAGES_;  // register stages of global prefetch
   static constexpr int BN = BN_;       // weight rows per workgroup
   static constexpr int BM = BM_;       // activation rows per workgroup
   static constexpr int WN = WN_;       // waves along N
@@ -46,6 +47,7 @@ struct Cfg {
   static constexpr int X_CHUNKS = BM * CPR / THREADS;
   static_assert(BN / WN == 128, "a wave spans 128 weight rows");
   static_assert(WAVE_M % 32 == 0 && FM >= 1, "wave M extent");
+  static_assert(BK % 32 == 0, "an even number of 16-wide K slices per stage");
   static_assert(BN * CPR % THREADS == 0 && BM * CPR % THREADS == 0, "load split");
 };
 
@@ -55,17 +57,28 @@ struct TileMap {
   int n_tiles, m_tiles, splits, k_per_split;
 };
 
-// Workgroup -> (n tile, m tile, split): XCD-contiguous, M fastest.
+constexpr int kGroupM = 8;  // M tiles per raster group
+
+// Workgroup -> (n tile, m tile, split).  Workgroups are dealt round-robin to
+// the 8 XCDs, so renumber them to give each XCD a contiguous range of
+// logical tiles; inside a split, tiles run in groups of kGroupM M tiles with
+// the M index fastest, so the workgroups resident at one time on an XCD
+// share both their weight tiles and their activation tiles in its L2.
 __device__ __forceinline__ void tile_of(const TileMap& tm, int& nt, int& mt, int& sp) {
   const int nb = gridDim.x;
   const int i = blockIdx.x;
   const int q = nb >> 3, r = nb & 7;
   const int x = i & 7, slot = i >> 3;
   const int t = x * q + min(x, r) + slot;
-  mt = t % tm.m_tiles;
-  const int rest = t / tm.m_tiles;
-  nt = rest % tm.n_tiles;
-  sp = rest / tm.n_tiles;
+  const int per_split = tm.m_tiles * tm.n_tiles;
+  sp = t / per_split;
+  const int u = t - sp * per_split;
+  const int group = u / (kGroupM * tm.n_tiles);
+  const int first_m = group * kGroupM;
+  const int gm = min(tm.m_tiles - first_m, kGroupM);
+  const int v = u - group * kGroupM * tm.n_tiles;
+  mt = first_m + v % gm;
+  nt = v / gm;
 }
 
 template <int EPI, int BN>
@@ -108,15 +121,15 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
   }
 
-  // global -> register staging, 16 B chunks
-  const bf16* wsrc[C::W_CHUNKS];
-  const bf16* xsrc[C::X_CHUNKS];
+  // global -> register staging, 16 B chunks; 32-bit element offsets from
+  // uniform base pointers keep the address registers few
+  int woff[C::W_CHUNKS], xoff[C::X_CHUNKS];
   int wdst[C::W_CHUNKS], xdst[C::X_CHUNKS];
 #pragma unroll
   for (int i = 0; i < C::W_CHUNKS; ++i) {
     const int q = tid + i * C::THREADS;
     const int r = q / C::CPR, ch = q % C::CPR;
-    wsrc[i] = W + (int64_t)weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
+    woff[i] = weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
     wdst[i] = r * LDK + ch * 8;
   }
 #pragma unroll
@@ -124,22 +137,32 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     const int q = tid + i * C::THREADS;
     const int r = q / C::CPR, ch = q % C::CPR;
     const int m = min(mt * BM + r, p.M - 1);
-    xsrc[i] = X + (int64_t)m * K + k0 + ch * 8;
+    xoff[i] = m * K + k0 + ch * 8;
     xdst[i] = r * LDK + ch * 8;
   }
-  u32x4 wreg[C::W_CHUNKS], xreg[C::X_CHUNKS];
-  auto load_global = [&](int kt) {
+  // With two register stages the global loads of K step kt+2 are issued
+  // while step kt computes, and the stores of step kt+1 into LDS are spread
+  // over step kt's MFMA slices; with one stage, loads of step kt+1 are issued
+  // at the start of step kt and stored before its barrier.
+  constexpr int NCH = C::W_CHUNKS + C::X_CHUNKS;
+  u32x4 stage[C::STAGES][NCH];
+  auto load_global = [&](int kt, int st) {
     const int ko = kt * BK;
 #pragma unroll
-    for (int i = 0; i < C::W_CHUNKS; ++i) wreg[i] = *reinterpret_cast<const u32x4*>(wsrc[i] + ko);
+    for (int i = 0; i < C::W_CHUNKS; ++i) stage[st][i] = *reinterpret_cast<const u32x4*>(W + woff[i] + ko);
 #pragma unroll
-    for (int i = 0; i < C::X_CHUNKS; ++i) xreg[i] = *reinterpret_cast<const u32x4*>(xsrc[i] + ko);
+    for (int i = 0; i < C::X_CHUNKS; ++i)
+      stage[st][C::W_CHUNKS + i] = *reinterpret_cast<const u32x4*>(X + xoff[i] + ko);
   };
-  auto store_lds = [&](int buf) {
+  auto store_chunk = [&](int buf, int st, int i) {
+    if (i < C::W_CHUNKS)
+      *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = stage[st][i];
+    else
+      *reinterpret_cast<u32x4*>(&sX[buf][xdst[i - C::W_CHUNKS]]) = stage[st][i];
+  };
+  auto store_lds = [&](int buf, int st) {
 #pragma unroll
-    for (int i = 0; i < C::W_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = wreg[i];
-#pragma unroll
-    for (int i = 0; i < C::X_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = xreg[i];
+    for (int i = 0; i < NCH; ++i) store_chunk(buf, st, i);
   };
 
   f32x16 acc[4][FM];
@@ -168,28 +191,59 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
       bfr[slot][b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
   };
 
-  load_global(0);
-  store_lds(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_global(kt + 1);
-    const bf16* w_s = sW[buf];
-    const bf16* x_s = sX[buf];
-    read_frags(w_s, x_s, 0, 0);
+  auto mfma_step = [&](int slot) {
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if (s + 1 < KS) read_frags(w_s, x_s, s + 1, (s + 1) & 1);
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[slot][a], bfr[slot][b], acc[a][b]);
+  };
+  // K step kt (LDS buffer kt&1): its first fragments are already in
+  // registers.  The MFMAs of its last 16-wide slice are issued after the
+  // barrier, behind the fragment reads of the next K step, so the wait for
+  // those reads overlaps matrix work.
+  auto step = [&](int kt, int par) {
+    const bf16* w_s = sW[par];
+    const bf16* x_s = sX[par];
+    const bool more = kt + 1 < nk;
+    if constexpr (C::STAGES == 2) {
+      if (kt + 2 < nk) load_global(kt + 2, par);
+    } else {
+      if (more) load_global(kt + 1, 0);
+    }
+#pragma unroll
+    for (int s = 0; s + 1 < KS; ++s) {
+      read_frags(w_s, x_s, s + 1, (s + 1) & 1);
+      if constexpr (C::STAGES == 2) {
+        if (more) {
+#pragma unroll
+          for (int i = s * NCH / (KS - 1); i < (s + 1) * NCH / (KS - 1); ++i) store_chunk(par ^ 1, par ^ 1, i);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[s & 1][a], bfr[s & 1][b], acc[a][b]);
+      mfma_step(s & 1);
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (kt + 1 < nk) store_lds(buf ^ 1);
+    if constexpr (C::STAGES == 1) {
+      if (more) store_lds(par ^ 1, 0);
+    }
     __syncthreads();
+    if (more) read_frags(sW[par ^ 1], sX[par ^ 1], 0, KS & 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_step((KS - 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  load_global(0, 0);
+  store_lds(0, 0);
+  if (C::STAGES == 2 && nk > 1) load_global(1, C::STAGES - 1);
+  __syncthreads();
+  read_frags(sW[0], sX[0], 0, 0);
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, 0);
+    step(kt + 1, 1);
   }
+  if (kt < nk) step(kt, 0);
 
   // ------------------------------------------------------------ epilogue
   // acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
@@ -282,17 +336,9 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
 
 }  // namespace
 
-using CfgSmall = Cfg<256, 128, 2, 2, 64>;   // 4 waves, 1 per SIMD
-using CfgWide = Cfg<256, 256, 2, 4, 64>;    // 8 waves, 2 per SIMD
-using CfgDeep = Cfg<512, 128, 4, 2, 32>;    // 8 waves, 2 per SIMD, BK 32
-
-int gemm_cfg() {
-  static int c = [] {
-    const char* e = getenv("ACACHE_GEMM_CFG");
-    return e ? atoi(e) : 0;
-  }();
-  return c;
-}
+// 8 waves (2 per SIMD) on a 256 x 256 tile, each wave 128 x 64; BK 64 with one
+// register stage: measured fastest on every projection shape of the workloads.
+using GemmCfg = Cfg<256, 256, 2, 4, 64, 1>;
 
 template <class C>
 int splits_for(int M, int N, int K) {
@@ -308,13 +354,7 @@ int splits_for(int M, int N, int K) {
   return best;
 }
 
-int gemm_bf16_splits(int M, int N, int K) {
-  switch (gemm_cfg()) {
-    case 1: return splits_for<CfgWide>(M, N, K);
-    case 2: return splits_for<CfgDeep>(M, N, K);
-    default: return splits_for<CfgSmall>(M, N, K);
-  }
-}
+int gemm_bf16_splits(int M, int N, int K) { return splits_for<GemmCfg>(M, N, K); }
 
 template <class C>
 hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
@@ -336,11 +376,7 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
 }
 
 hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {
-  switch (gemm_cfg()) {
-    case 1: return launch_cfg<CfgWide>(epi, p, s);
-    case 2: return launch_cfg<CfgDeep>(epi, p, s);
-    default: return launch_cfg<CfgSmall>(epi, p, s);
-  }
+  return launch_cfg<GemmCfg>(epi, p, s);
 }
 
 }  // namespace acache
