@@ -31,7 +31,10 @@
  *  - Row-major layouts.  A KV pool is [n_slots, pool_ld] elements, one pool
  *    per layer for K and one for V; the row of a slot holds H_kv heads of
  *    head_dim elements (K after rotation).  Leading dimensions are in
- *    elements unless named *_bytes.
+ *    elements unless named *_bytes.  The kernels address a pool with 32-bit
+ *    element offsets: acache_score, acache_attention and
+ *    acache_layer_recompute return ACACHE_ERR_UNSUPPORTED unless
+ *    n_slots * pool_ld < 2^31.
  *  - The fused block is the LLaDA / Dream family's: RMSNorm, Q/K/V
  *    projections (no bias), rotary embedding on half-split pairs at the
  *    row's position, bidirectional attention with grouped KV heads, output

@@ -37,8 +37,8 @@ FLAGS = [
 
 
 def source_digest() -> str:
-    """sha256 over the kernel sources and the public header (identifies the
-    kernels a stored counter measurement was taken on)."""
+    """sha256 over the kernel and library sources (identifies the kernels a
+    stored counter measurement was taken on)."""
     import hashlib
 
     h = hashlib.sha256()
@@ -46,7 +46,6 @@ def source_digest() -> str:
         if name.endswith((".hip", ".cpp", ".h")):
             h.update(name.encode())
             h.update(open(os.path.join(CSRC, name), "rb").read())
-    h.update(open(os.path.join(ROOT, "include", "acache.h"), "rb").read())
     return h.hexdigest()[:16]
 
 
