@@ -240,7 +240,13 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
  * acache_rmsnorm: y[r] = x[r] / sqrt(mean(x[r]^2) + eps) * g, rows x [rows, d].
  * acache_linear:  c[m, n] = sum_k a[m, k] w[n, k] (+ c[m, n] when accumulate),
  *                 a [M, K], w [N, K], c [M, N], dims->dtype storage, fp32
- *                 accumulation.  bf16 requires K % 64 == 0, N % 256 == 0. */
+ *                 accumulation.  bf16 requires K % 64 == 0, N % 256 == 0.
+ *                 ws is optional: with a 16-byte aligned bf16 workspace of
+ *                 acache_workspace_size(dims, M, 1, 0) bytes or more, row
+ *                 counts that leave CUs idle in the last round of tiles are
+ *                 balanced by splitting K across workgroups (fp32 partials,
+ *                 summed in a fixed order); without it every tile runs whole.
+ *                 The two schedules agree up to fp32 summation order. */
 acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void* g, void* y,
                              int32_t rows, hipStream_t stream);
 acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,

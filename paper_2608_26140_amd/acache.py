@@ -254,13 +254,16 @@ def acache_rmsnorm(dims: Dims, x: torch.Tensor, g: torch.Tensor, out: Optional[t
 
 
 def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[torch.Tensor] = None,
-                  accumulate: bool = False, stream=None):
+                  accumulate: bool = False, ws: Optional[torch.Tensor] = None, stream=None):
+    """ws (optional, from `workspace`): lets bf16 balance small row counts by
+    splitting K across workgroups."""
     M, K = a.shape
     N = w.shape[0]
     if out is None:
         out = torch.empty((M, N), dtype=a.dtype, device=a.device)
     _check("acache_linear", lib.acache_linear(ctypes.byref(dims), _ptr(a), _ptr(w), _ptr(out), M, N, K,
-                                              int(accumulate), None, 0, _stream(stream)))
+                                              int(accumulate), _ptr(ws), 0 if ws is None else ws.numel(),
+                                              _stream(stream)))
     return out
 
 

@@ -141,7 +141,9 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
       const int sp = std::max(gemm_bf16_splits(m, d->d_model, (int)hq), gemm_bf16_splits(m, d->d_model, d->d_ff));
       part_rows = std::max(part_rows, (size_t)sp * (size_t)m);
     }
-    w.part = take(part_rows * d->d_model * sizeof(float));
+    // split-K partials of the O / down projections and the stream-K pieces
+    // of the QKV / gate-up projections are never live at the same time
+    w.part = take(std::max(part_rows * d->d_model * sizeof(float), gemm_bf16_sk_ws_bytes()));
     w.qkv = w.gu = 0;
   } else {
     w.qkv = take(M * (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim * es);
@@ -315,8 +317,6 @@ acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void*
 acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,
                             int32_t M, int32_t N, int32_t K, int32_t accumulate, void* ws,
                             size_t ws_bytes, hipStream_t stream) {
-  (void)ws;
-  (void)ws_bytes;
   CHECK(dims, ACACHE_ERR_NULL);
   CHECK(dims->dtype == ACACHE_BF16 || dims->dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
   CHECK(M >= 0 && N >= 0 && K >= 0, ACACHE_ERR_SHAPE);
@@ -334,6 +334,8 @@ acache_status acache_linear(const acache_dims* dims, const void* a, const void* 
     p.splits = 1;
     p.C = c;
     p.ldc = N;
+    // a workspace large enough for the stream-K partials enables stream-K
+    if (ws && aligned16(ws) && ws_bytes >= gemm_bf16_sk_ws_bytes()) p.sk_ws = (float*)ws;
     LAUNCH(launch_gemm_bf16(accumulate ? EPI_ACCUM : EPI_STORE, p, stream));
   } else {
     LAUNCH(launch_gemm_f32((const float*)a, (const float*)w, (float*)c, N, M, N, K, accumulate, stream));
@@ -462,6 +464,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     g.hq_cols = hq;
     g.hkv_cols = hkv;
     g.rope_base = dims->rope_base;
+    g.sk_ws = at<float>(ws, p.part);
     LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse, stream));
   } else {
@@ -499,6 +502,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     u.splits = 1;
     u.C = hb;
     u.ldc = F;
+    u.sk_ws = part;
     LAUNCH_T(ACACHE_K_GEMM_GATE_UP, stream, launch_gemm_bf16(EPI_SWIGLU, u, stream));
     GemmParams dn = {};
     dn.X = hb;

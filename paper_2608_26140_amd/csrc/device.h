@@ -29,6 +29,35 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// sin and cos of a rotary angle given in fp64.  The angle is reduced to
+// r = ang - q * pi/2, |r| <= pi/4, in fp64 (the product pos * theta_i is
+// exact enough there for any position), then both functions are Taylor
+// polynomials in r to degree 11 / 12 (truncation below 1e-9) evaluated in
+// fp32, and the quadrant q mod 4 picks signs and swaps.  Unlike the library
+// sincos, this has no large-argument path and no scratch table.
+__device__ __forceinline__ void rotary_sincos(double ang, float* sn, float* cs) {
+  const double q = rint(ang * 0.6366197723675814);  // 2 / pi
+  const float r = (float)(ang - q * 1.5707963267948966);
+  const float r2 = r * r;
+  // sin r = r (1 - r^2/3! (1 - r^2/(4*5) (1 - r^2/(6*7) (1 - r^2/(8*9) (1 - r^2/(10*11))))))
+  float ps = 1.f - r2 * (1.f / 110.f);
+  ps = 1.f - r2 * (1.f / 72.f) * ps;
+  ps = 1.f - r2 * (1.f / 42.f) * ps;
+  ps = 1.f - r2 * (1.f / 20.f) * ps;
+  ps = 1.f - r2 * (1.f / 6.f) * ps;
+  const float s = r * ps;
+  // cos r = 1 - r^2/2! (1 - r^2/(3*4) (1 - r^2/(5*6) (1 - r^2/(7*8) (1 - r^2/(9*10) (1 - r^2/(11*12))))))
+  float pc = 1.f - r2 * (1.f / 132.f);
+  pc = 1.f - r2 * (1.f / 90.f) * pc;
+  pc = 1.f - r2 * (1.f / 56.f) * pc;
+  pc = 1.f - r2 * (1.f / 30.f) * pc;
+  pc = 1.f - r2 * (1.f / 12.f) * pc;
+  const float c = 1.f - r2 * 0.5f * pc;
+  const int k = (int)((long long)q & 3);
+  *sn = k == 0 ? s : k == 1 ? c : k == 2 ? -s : -c;
+  *cs = k == 0 ? c : k == 1 ? -s : k == 2 ? -c : s;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));

@@ -51,6 +51,7 @@ struct GemmParams {
   void* C;          // STORE / ACCUM / SWIGLU output, [M, ldc]
   int64_t ldc;
   float* P;         // PARTIAL output [splits][M][N]
+  float* sk_ws;     // stream-K partials, gemm_bf16_sk_ws_bytes(); null: data-parallel only
   // QKV epilogue
   void* q_out;      // [M, hq_cols]
   void* k_pool;
@@ -64,6 +65,7 @@ struct GemmParams {
 };
 hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s);
 int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL
+size_t gemm_bf16_sk_ws_bytes();             // stream-K workspace (any shape)
 
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,

@@ -8,18 +8,28 @@
 // and puts both halves of every rotary pair (columns d and d + 64 of one
 // head) in the same lane.
 //
-// Workgroup tile: 256 weight rows x 128 activation rows x 64 K, 4 waves
-// (2 x 2), each wave 128 x 64 = 4 x 2 MFMA 32x32x16 tiles.  LDS is double
-// buffered with one barrier per K step; global loads for step k+1 are in
-// flight while step k computes.  Rows are padded to 144 bytes so the
-// 16-lane groups of a ds_read_b128 hit distinct banks.  Workgroups are
-// renumbered so that each XCD (8 per chip, own L2) receives a contiguous run
-// of tiles with the M index fastest: the tiles sharing one weight tile run on
-// the same L2.
+// Workgroup tile: 256 weight rows x 256 activation rows x 64 K, 8 waves
+// (2 along N x 4 along M, two per SIMD), each wave 128 x 64 = 4 x 2 MFMA
+// 32x32x16 tiles.  LDS is double buffered with one barrier per K step;
+// global loads for step k+1 are in flight while step k computes.  Rows are
+// padded to 144 bytes so the 16-lane groups of a ds_read_b128 hit distinct
+// banks.  Workgroups are renumbered so that each XCD (8 per chip, own L2)
+// receives a contiguous run of tiles with the M index fastest: the tiles
+// sharing one weight tile run on the same L2.
+//
+// Schedules.  Data-parallel: one tile (or one K split of a tile) per
+// workgroup.  Stream-K, for the recompute's small row counts where the
+// tile count is not a multiple of the CU count: the full rounds of tiles run
+// data-parallel, and the K steps of the remaining tiles are dealt evenly to
+// all workgroups.  A workgroup whose K range covers only part of a tile
+// writes its fp32 accumulators to a workspace slot; a fixup kernel (one
+// wave per wave-tile) sums the pieces of each such tile in workgroup order,
+// so the result does not depend on timing, and runs the same epilogue.
 //
 // Epilogues: plain store, accumulate, fp32 split-K partials, Q/K/V with
 // rotary embedding and the K/V store to pool slots, and SwiGLU.
-#include <cstdlib>
+#include <algorithm>
+#include <atomic>
 
 #include "device.h"
 #include "internal.h"
@@ -28,23 +38,24 @@ namespace acache {
 
 namespace {
 
-// Tile configurations.  Every wave covers 128 weight rows (one attention
+// Tile configuration.  Every wave covers 128 weight rows (one attention
 // head, or 64 gate + 64 up rows) and WAVE_M activation rows.
-template <int BN_, int BM_, int WN_, int WM_, int BK_, int STAGES_ = 2>
+template <int BN_, int BM_, int WN_, int WM_, int BK_>
 struct Cfg {
-  static constexpr int STAGES = STAGES_;  // register stages of global prefetch
   static constexpr int BN = BN_;       // weight rows per workgroup
   static constexpr int BM = BM_;       // activation rows per workgroup
   static constexpr int WN = WN_;       // waves along N
   static constexpr int WM = WM_;       // waves along M
   static constexpr int BK = BK_;       // K per LDS stage
   static constexpr int LDK = BK + 8;   // padded LDS row (elements)
-  static constexpr int THREADS = 64 * WN * WM;
+  static constexpr int WAVES = WN * WM;
+  static constexpr int THREADS = 64 * WAVES;
   static constexpr int WAVE_M = BM / WM;
   static constexpr int FM = WAVE_M / 32;  // activation fragments per wave
   static constexpr int CPR = BK / 8;      // 16-byte chunks per row
   static constexpr int W_CHUNKS = BN * CPR / THREADS;
   static constexpr int X_CHUNKS = BM * CPR / THREADS;
+  static constexpr int ACC4 = 4 * FM * 4;  // float4 accumulator chunks per lane
   static_assert(BN / WN == 128, "a wave spans 128 weight rows");
   static_assert(WAVE_M % 32 == 0 && FM >= 1, "wave M extent");
   static_assert(BK % 32 == 0, "an even number of 16-wide K slices per stage");
@@ -55,21 +66,31 @@ typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
 struct TileMap {
   int n_tiles, m_tiles, splits, k_per_split;
+  int dp_rounds;   // whole tiles per workgroup, logical tile j * dp_stride + w
+  int dp_stride;
+  int sk_first;    // first logical tile of the stream-K region
+  int sk_units;    // K steps in the stream-K region
+  int sk_groups;   // workgroups sharing the stream-K region (0: none)
+  float* sk_part;  // [sk_groups][2][THREADS * ACC4 * 4] partial accumulators
 };
 
-constexpr int kGroupM = 8;  // M tiles per raster group
+constexpr int kGroupM = 8;       // M tiles per raster group
+constexpr int kMaxSkGroups = 256;
+constexpr int kMinSkSteps = 4;   // K steps per tile for stream-K, at least
 
-// Workgroup -> (n tile, m tile, split).  Workgroups are dealt round-robin to
-// the 8 XCDs, so renumber them to give each XCD a contiguous range of
-// logical tiles; inside a split, tiles run in groups of kGroupM M tiles with
-// the M index fastest, so the workgroups resident at one time on an XCD
-// share both their weight tiles and their activation tiles in its L2.
-__device__ __forceinline__ void tile_of(const TileMap& tm, int& nt, int& mt, int& sp) {
-  const int nb = gridDim.x;
-  const int i = blockIdx.x;
+// Workgroups are dealt round-robin to the 8 XCDs; renumber them so that each
+// XCD holds a contiguous range of logical workgroup ids.
+__device__ __forceinline__ int logical_block() {
+  const int nb = gridDim.x, i = blockIdx.x;
   const int q = nb >> 3, r = nb & 7;
   const int x = i & 7, slot = i >> 3;
-  const int t = x * q + min(x, r) + slot;
+  return x * q + min(x, r) + slot;
+}
+
+// Logical tile -> (n tile, m tile, split).  Inside a split, tiles run in
+// groups of kGroupM M tiles with the M index fastest, so the workgroups
+// resident at one time on an XCD share their weight tiles in its L2.
+__device__ __forceinline__ void tile_coords(const TileMap& tm, int t, int& nt, int& mt, int& sp) {
   const int per_split = tm.m_tiles * tm.n_tiles;
   sp = t / per_split;
   const int u = t - sp * per_split;
@@ -79,6 +100,15 @@ __device__ __forceinline__ void tile_of(const TileMap& tm, int& nt, int& mt, int
   const int v = u - group * kGroupM * tm.n_tiles;
   mt = first_m + v % gm;
   nt = v / gm;
+}
+
+// Stream-K bookkeeping: workgroup w owns K steps [start(w), start(w + 1)) of
+// the stream-K region; the owner of step i is the largest w with start(w) <= i.
+__device__ __forceinline__ int sk_start(const TileMap& tm, int w) {
+  return (int)(((int64_t)w * tm.sk_units) / tm.sk_groups);
+}
+__device__ __forceinline__ int sk_owner(const TileMap& tm, int i) {
+  return (int)((((int64_t)i + 1) * tm.sk_groups - 1) / tm.sk_units);
 }
 
 template <int EPI, int BN>
@@ -99,154 +129,41 @@ __device__ __forceinline__ void store4(bf16* p, const float v[4]) {
   *reinterpret_cast<bf16x4*>(p) = o;
 }
 
-template <int EPI, class C>
-__global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
-  constexpr int BN = C::BN, BM = C::BM, BK = C::BK, LDK = C::LDK, FM = C::FM;
-  __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sX[2][BM * LDK];
-  __shared__ double inv_freq[64];
-
-  int nt, mt, sp;
-  tile_of(tm, nt, mt, sp);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn = wave % C::WN, wm = wave / C::WN;
-  const int F = p.N >> 1;
-  const bf16* __restrict__ X = (const bf16*)p.X;
-  const bf16* __restrict__ W = (const bf16*)p.W;
-  const int K = p.K;
-  const int k0 = sp * tm.k_per_split;
-  const int nk = tm.k_per_split / BK;
-
-  if constexpr (EPI == EPI_QKV) {
-    if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
-  }
-
-  // global -> register staging, 16 B chunks; 32-bit element offsets from
-  // uniform base pointers keep the address registers few
-  int woff[C::W_CHUNKS], xoff[C::X_CHUNKS];
-  int wdst[C::W_CHUNKS], xdst[C::X_CHUNKS];
-#pragma unroll
-  for (int i = 0; i < C::W_CHUNKS; ++i) {
-    const int q = tid + i * C::THREADS;
-    const int r = q / C::CPR, ch = q % C::CPR;
-    woff[i] = weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
-    wdst[i] = r * LDK + ch * 8;
-  }
-#pragma unroll
-  for (int i = 0; i < C::X_CHUNKS; ++i) {
-    const int q = tid + i * C::THREADS;
-    const int r = q / C::CPR, ch = q % C::CPR;
-    const int m = min(mt * BM + r, p.M - 1);
-    xoff[i] = m * K + k0 + ch * 8;
-    xdst[i] = r * LDK + ch * 8;
-  }
-  // With two register stages the global loads of K step kt+2 are issued
-  // while step kt computes, and the stores of step kt+1 into LDS are spread
-  // over step kt's MFMA slices; with one stage, loads of step kt+1 are issued
-  // at the start of step kt and stored before its barrier.
-  constexpr int NCH = C::W_CHUNKS + C::X_CHUNKS;
-  u32x4 stage[C::STAGES][NCH];
-  auto load_global = [&](int kt, int st) {
-    const int ko = kt * BK;
-#pragma unroll
-    for (int i = 0; i < C::W_CHUNKS; ++i) stage[st][i] = *reinterpret_cast<const u32x4*>(W + woff[i] + ko);
-#pragma unroll
-    for (int i = 0; i < C::X_CHUNKS; ++i)
-      stage[st][C::W_CHUNKS + i] = *reinterpret_cast<const u32x4*>(X + xoff[i] + ko);
-  };
-  auto store_chunk = [&](int buf, int st, int i) {
-    if (i < C::W_CHUNKS)
-      *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = stage[st][i];
-    else
-      *reinterpret_cast<u32x4*>(&sX[buf][xdst[i - C::W_CHUNKS]]) = stage[st][i];
-  };
-  auto store_lds = [&](int buf, int st) {
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) store_chunk(buf, st, i);
-  };
-
-  f32x16 acc[4][FM];
+// Partial accumulators of one wave: float4 chunk i of lane l at (i * 64 + l) * 4,
+// chunk i = (a * FM + b) * 4 + g holding acc[a][b][4g .. 4g + 3].
+template <class C>
+__device__ __forceinline__ void store_partial(float* base, const f32x16 (&acc)[4][C::FM], int lane) {
 #pragma unroll
   for (int a = 0; a < 4; ++a)
 #pragma unroll
-    for (int b = 0; b < FM; ++b)
+    for (int b = 0; b < C::FM; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-
-  const int arow = wn * 128 + (lane & 31);
-  const int brow = wm * C::WAVE_M + (lane & 31);
-  const int kofs = (lane >> 5) * 8;
-
-  // MFMA fragments are double buffered in registers: the reads of k step
-  // s+1 are issued before the MFMAs of step s, so LDS latency overlaps with
-  // matrix work instead of stalling the wave.
-  constexpr int KS = BK / 16;
-  bf16x8 af[2][4], bfr[2][FM];
-  auto read_frags = [&](const bf16* w_s, const bf16* x_s, int s, int slot) {
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-      af[slot][a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
-#pragma unroll
-    for (int b = 0; b < FM; ++b)
-      bfr[slot][b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
-  };
-
-  auto mfma_step = [&](int slot) {
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[slot][a], bfr[slot][b], acc[a][b]);
-  };
-  // K step kt (LDS buffer kt&1): its first fragments are already in
-  // registers.  The MFMAs of its last 16-wide slice are issued after the
-  // barrier, behind the fragment reads of the next K step, so the wait for
-  // those reads overlaps matrix work.
-  auto step = [&](int kt, int par) {
-    const bf16* w_s = sW[par];
-    const bf16* x_s = sX[par];
-    const bool more = kt + 1 < nk;
-    if constexpr (C::STAGES == 2) {
-      if (kt + 2 < nk) load_global(kt + 2, par);
-    } else {
-      if (more) load_global(kt + 1, 0);
-    }
-#pragma unroll
-    for (int s = 0; s + 1 < KS; ++s) {
-      read_frags(w_s, x_s, s + 1, (s + 1) & 1);
-      if constexpr (C::STAGES == 2) {
-        if (more) {
-#pragma unroll
-          for (int i = s * NCH / (KS - 1); i < (s + 1) * NCH / (KS - 1); ++i) store_chunk(par ^ 1, par ^ 1, i);
-        }
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v = {acc[a][b][4 * g], acc[a][b][4 * g + 1], acc[a][b][4 * g + 2], acc[a][b][4 * g + 3]};
+        *reinterpret_cast<f32x4*>(base + (((a * C::FM + b) * 4 + g) * 64 + lane) * 4) = v;
       }
-      __builtin_amdgcn_sched_barrier(0);
-      mfma_step(s & 1);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if constexpr (C::STAGES == 1) {
-      if (more) store_lds(par ^ 1, 0);
-    }
-    __syncthreads();
-    if (more) read_frags(sW[par ^ 1], sX[par ^ 1], 0, KS & 1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfma_step((KS - 1) & 1);
-    __builtin_amdgcn_sched_barrier(0);
-  };
+}
 
-  load_global(0, 0);
-  store_lds(0, 0);
-  if (C::STAGES == 2 && nk > 1) load_global(1, C::STAGES - 1);
-  __syncthreads();
-  read_frags(sW[0], sX[0], 0, 0);
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    step(kt, 0);
-    step(kt + 1, 1);
-  }
-  if (kt < nk) step(kt, 0);
+template <class C>
+__device__ __forceinline__ void add_partial(const float* base, f32x16 (&acc)[4][C::FM], int lane) {
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FM; ++b)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(base + (((a * C::FM + b) * 4 + g) * 64 + lane) * 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[a][b][4 * g + j] += v[j];
+      }
+}
 
-  // ------------------------------------------------------------ epilogue
-  // acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
+// Writes one wave's accumulators (wave (wn, wm) of tile (nt, mt), split sp).
+// acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
+template <int EPI, class C>
+__device__ __forceinline__ void epilogue(const GemmParams& p, const f32x16 (&acc)[4][C::FM], int nt, int mt,
+                                         int sp, int wn, int wm, int lane, const double* inv_freq) {
+  constexpr int BN = C::BN, BM = C::BM, FM = C::FM;
   const int hl = lane >> 5;
   const int mbase = mt * BM + wm * C::WAVE_M + (lane & 31);
 #pragma unroll
@@ -292,28 +209,6 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     } else if constexpr (EPI == EPI_QKV) {
       const int col0 = nt * BN + wn * 128;  // first weight row of this wave = one head
       const bool is_v = col0 >= p.hq_cols + p.hkv_cols;
-      float out[4][16];
-      if (!is_v) {
-        const double ang_pos = (double)p.pos[m];
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int d = a * 32 + 8 * (r >> 2) + 4 * hl + (r & 3);
-            double ang = ang_pos * inv_freq[d];
-            ang -= 6.283185307179586 * rint(ang * 0.15915494309189535);
-            float sn, cs;
-            sincosf((float)ang, &sn, &cs);
-            const float x1 = acc[a][b][r], x2 = acc[a + 2][b][r];
-            out[a][r] = x1 * cs - x2 * sn;
-            out[a + 2][r] = x2 * cs + x1 * sn;
-          }
-      } else {
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) out[a][r] = acc[a][b][r];
-      }
       bf16* dst;
       if (col0 < p.hq_cols) {
         dst = (bf16*)p.q_out + (int64_t)m * p.hq_cols + col0;
@@ -323,22 +218,263 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
         const int c = is_v ? col0 - p.hq_cols - p.hkv_cols : col0 - p.hq_cols;
         dst = (bf16*)(is_v ? p.v_pool : p.k_pool) + slot * p.pool_ld + c;
       }
+      if (!is_v) {
+        // rotate the pairs (d, d + 64): both halves sit in this lane, in
+        // fragments a and a + 2
+        const double ang_pos = (double)p.pos[m];
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
+        for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float v[4] = {out[a][4 * g], out[a][4 * g + 1], out[a][4 * g + 2], out[a][4 * g + 3]};
-          store4(dst + a * 32 + g * 8 + hl * 4, v);
-        }
+          for (int g = 0; g < 4; ++g) {
+            float lo[4], hi[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int r = 4 * g + j;
+              const int d = a * 32 + 8 * g + 4 * hl + j;
+              float sn, cs;
+              rotary_sincos(ang_pos * inv_freq[d], &sn, &cs);
+              const float x1 = acc[a][b][r], x2 = acc[a + 2][b][r];
+              lo[j] = x1 * cs - x2 * sn;
+              hi[j] = x2 * cs + x1 * sn;
+            }
+            store4(dst + a * 32 + g * 8 + hl * 4, lo);
+            store4(dst + (a + 2) * 32 + g * 8 + hl * 4, hi);
+          }
+      } else {
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float v[4] = {acc[a][b][4 * g], acc[a][b][4 * g + 1], acc[a][b][4 * g + 2], acc[a][b][4 * g + 3]};
+            store4(dst + a * 32 + g * 8 + hl * 4, v);
+          }
+      }
     }
   }
 }
 
+__device__ __forceinline__ void init_inv_freq(double* inv_freq, const GemmParams& p, int tid) {
+  if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
+}
+
+template <int EPI, class C>
+__global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
+  constexpr int BN = C::BN, BM = C::BM, BK = C::BK, LDK = C::LDK, FM = C::FM;
+  __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 sX[2][BM * LDK];
+  __shared__ double inv_freq[64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave % C::WN, wm = wave / C::WN;
+  const int F = p.N >> 1;
+  const bf16* __restrict__ X = (const bf16*)p.X;
+  const bf16* __restrict__ W = (const bf16*)p.W;
+  const int K = p.K;
+  const int nk_tile = tm.k_per_split / BK;
+  const int w = logical_block();
+  if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
+
+  const int arow = wn * 128 + (lane & 31);
+  const int brow = wm * C::WAVE_M + (lane & 31);
+  const int kofs = (lane >> 5) * 8;
+  constexpr int KS = BK / 16;
+  constexpr int NCH = C::W_CHUNKS + C::X_CHUNKS;
+
+  f32x16 acc[4][FM];
+  // Work items: dp_rounds whole tiles, then this workgroup's stream-K range.
+  int item = 0;
+  int u = 0, u_end = 0;
+  if (tm.sk_groups > 0 && w < tm.sk_groups) {
+    u = sk_start(tm, w);
+    u_end = sk_start(tm, w + 1);
+  }
+  int piece = 0;
+  while (true) {
+    int t, kb, kn;
+    bool sk = false;
+    if (item < tm.dp_rounds) {
+      t = item * tm.dp_stride + w;
+      kb = -1;  // from the split index
+      kn = nk_tile;
+      ++item;
+    } else if (u < u_end) {
+      const int tl = u / nk_tile;
+      kb = u - tl * nk_tile;
+      kn = min(nk_tile - kb, u_end - u);
+      t = tm.sk_first + tl;
+      u += kn;
+      sk = true;
+    } else {
+      break;
+    }
+    int nt, mt, sp;
+    tile_coords(tm, t, nt, mt, sp);
+    if (kb < 0) kb = sp * nk_tile;
+    const int k0 = kb * BK;
+    const int nk = kn;
+
+    // global -> register staging, 16 B chunks; 32-bit element offsets from
+    // uniform base pointers keep the address registers few
+    int woff[C::W_CHUNKS], xoff[C::X_CHUNKS];
+    int wdst[C::W_CHUNKS], xdst[C::X_CHUNKS];
+#pragma unroll
+    for (int i = 0; i < C::W_CHUNKS; ++i) {
+      const int q = tid + i * C::THREADS;
+      const int r = q / C::CPR, ch = q % C::CPR;
+      woff[i] = weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
+      wdst[i] = r * LDK + ch * 8;
+    }
+#pragma unroll
+    for (int i = 0; i < C::X_CHUNKS; ++i) {
+      const int q = tid + i * C::THREADS;
+      const int r = q / C::CPR, ch = q % C::CPR;
+      const int m = min(mt * BM + r, p.M - 1);
+      xoff[i] = m * K + k0 + ch * 8;
+      xdst[i] = r * LDK + ch * 8;
+    }
+    // loads of K step kt+1 are issued at the start of step kt and stored to
+    // the other LDS buffer before its barrier
+    u32x4 stage[NCH];
+    auto load_global = [&](int kt) {
+      const int ko = kt * BK;
+#pragma unroll
+      for (int i = 0; i < C::W_CHUNKS; ++i) stage[i] = *reinterpret_cast<const u32x4*>(W + woff[i] + ko);
+#pragma unroll
+      for (int i = 0; i < C::X_CHUNKS; ++i)
+        stage[C::W_CHUNKS + i] = *reinterpret_cast<const u32x4*>(X + xoff[i] + ko);
+    };
+    auto store_lds = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < C::W_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = stage[i];
+#pragma unroll
+      for (int i = 0; i < C::X_CHUNKS; ++i)
+        *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = stage[C::W_CHUNKS + i];
+    };
+
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < FM; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    // MFMA fragments are double buffered in registers: the reads of k slice
+    // s+1 are issued before the MFMAs of slice s, so LDS latency overlaps
+    // with matrix work instead of stalling the wave.
+    bf16x8 af[2][4], bfr[2][FM];
+    auto read_frags = [&](const bf16* w_s, const bf16* x_s, int s, int slot) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+        af[slot][a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
+#pragma unroll
+      for (int b = 0; b < FM; ++b)
+        bfr[slot][b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
+    };
+    auto mfma_step = [&](int slot) {
+#pragma unroll
+      for (int a = 0; a < 4; ++a)
+#pragma unroll
+        for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[slot][a], bfr[slot][b], acc[a][b]);
+    };
+    // K step kt (LDS buffer kt&1): its first fragments are already in
+    // registers.  The MFMAs of its last 16-wide slice are issued after the
+    // barrier, behind the fragment reads of the next K step, so the wait for
+    // those reads overlaps matrix work.
+    auto step = [&](int kt, int par) {
+      const bf16* w_s = sW[par];
+      const bf16* x_s = sX[par];
+      const bool more = kt + 1 < nk;
+      if (more) load_global(kt + 1);
+#pragma unroll
+      for (int s = 0; s + 1 < KS; ++s) {
+        read_frags(w_s, x_s, s + 1, (s + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_step(s & 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (more) store_lds(par ^ 1);
+      __syncthreads();
+      if (more) read_frags(sW[par ^ 1], sX[par ^ 1], 0, KS & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfma_step((KS - 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // every wave has finished reading LDS for the previous item
+    __syncthreads();
+    load_global(0);
+    store_lds(0);
+    __syncthreads();
+    read_frags(sW[0], sX[0], 0, 0);
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+      step(kt, 0);
+      step(kt + 1, 1);
+    }
+    if (kt < nk) step(kt, 0);
+
+    if (sk && kn < nk_tile) {
+      float* slot = tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4);
+      store_partial<C>(slot, acc, lane);
+      ++piece;
+    } else {
+      if (sk) ++piece;
+      epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane, inv_freq);
+    }
+  }
+}
+
+// Stream-K fixup: block = one wave of one split tile of the stream-K region.
+// Sums the tile's pieces in workgroup order and runs the epilogue.
+template <int EPI, class C>
+__global__ __launch_bounds__(64) void gemm_bf16_fixup(GemmParams p, TileMap tm) {
+  __shared__ double inv_freq[64];
+  const int lane = threadIdx.x;
+  const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
+  const int wn = wave % C::WN, wm = wave / C::WN;
+  const int nk_tile = tm.k_per_split / C::BK;
+  const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
+  if (first == last) return;  // the tile was finished by one workgroup
+  if constexpr (EPI == EPI_QKV) {
+    init_inv_freq(inv_freq, p, lane);
+    __syncthreads();
+  }
+  f32x16 acc[4][C::FM];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < C::FM; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+  for (int w = first; w <= last; ++w) {
+    // piece 0 of w if w's range starts in this tile, else its piece 1
+    const int piece = sk_start(tm, w) / nk_tile == s ? 0 : 1;
+    add_partial<C>(tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4), acc, lane);
+  }
+  int nt, mt, sp;
+  tile_coords(tm, tm.sk_first + s, nt, mt, sp);
+  epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane, inv_freq);
+}
+
 }  // namespace
 
-// 8 waves (2 per SIMD) on a 256 x 256 tile, each wave 128 x 64; BK 64 with one
-// register stage: measured fastest on every projection shape of the workloads.
-using GemmCfg = Cfg<256, 256, 2, 4, 64, 1>;
+// 8 waves (2 per SIMD) on a 256 x 256 tile, each wave 128 x 64; BK 64.
+using GemmCfg = Cfg<256, 256, 2, 4, 64>;
+
+namespace {
+
+int cu_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kMaxSkGroups;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = kMaxSkGroups;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 template <class C>
 int splits_for(int M, int N, int K) {
@@ -354,25 +490,77 @@ int splits_for(int M, int N, int K) {
   return best;
 }
 
-int gemm_bf16_splits(int M, int N, int K) { return splits_for<GemmCfg>(M, N, K); }
-
 template <class C>
 hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
-  TileMap tm;
+  TileMap tm = {};
   tm.m_tiles = (p.M + C::BM - 1) / C::BM;
   tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / (C::BN / 2) : p.N / C::BN;
   tm.splits = epi == EPI_PARTIAL ? p.splits : 1;
   tm.k_per_split = p.K / tm.splits;
-  const dim3 grid(tm.m_tiles * tm.n_tiles * tm.splits);
+  const int tiles = tm.m_tiles * tm.n_tiles * tm.splits;
+  const int nk = tm.k_per_split / C::BK;
+  int grid = tiles;
+  tm.dp_rounds = 1;
+  tm.dp_stride = tiles;
+  int sk_tiles = 0;
+  if (epi != EPI_PARTIAL && p.sk_ws && nk >= kMinSkSteps) {
+    // Cost in K steps of one workgroup.  Data-parallel: ceil(T / G) whole
+    // tiles.  Stream-K with g workgroups on the e tiles left after r full
+    // rounds: r whole tiles, ceil(e nk / g) steps, and the partial pieces
+    // (at most e + g, each 256 KB written and read back once), which cost
+    // about 1/16 of a K step each at HBM speed.  With g >= e every range
+    // spans at most nk steps and so touches at most two tiles (the two
+    // partial slots of a workgroup).
+    const int G = std::min(cu_count(), kMaxSkGroups);
+    const int r = tiles / G, e = tiles % G;
+    const double dp_cost = (double)((tiles + G - 1) / G) * nk;
+    double best = dp_cost;
+    int best_g = 0;
+    for (int g = e; e > 0 && g <= G; ++g) {
+      const double cost = (double)r * nk + (double)((e * nk + g - 1) / g) + (e + g) / 16.0;
+      if (cost < best) {
+        best = cost;
+        best_g = g;
+      }
+    }
+    if (best_g > 0) {
+      tm.dp_rounds = r;
+      tm.dp_stride = G;
+      tm.sk_first = r * G;
+      tm.sk_units = e * nk;
+      tm.sk_groups = best_g;
+      tm.sk_part = p.sk_ws;
+      grid = r > 0 ? G : best_g;
+      sk_tiles = e;
+    }
+  }
   const dim3 block(C::THREADS);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
-    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
-    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), dim3(grid), block, 0, s, p, tm); break;
+    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), dim3(grid), block, 0, s, p, tm); break;
+    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), dim3(grid), block, 0, s, p, tm); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), dim3(grid), block, 0, s, p, tm); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), dim3(grid), block, 0, s, p, tm); break;
+  }
+  if (sk_tiles > 0) {
+    const dim3 fgrid(sk_tiles * C::WAVES), fblock(64);
+    switch (epi) {
+      case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
+      case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
+      case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_QKV, C>), fgrid, fblock, 0, s, p, tm); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_SWIGLU, C>), fgrid, fblock, 0, s, p, tm); break;
+      default: break;
+    }
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+int gemm_bf16_splits(int M, int N, int K) { return splits_for<GemmCfg>(M, N, K); }
+
+size_t gemm_bf16_sk_ws_bytes() {
+  return (size_t)kMaxSkGroups * 2 * GemmCfg::WAVES * 64 * GemmCfg::ACC4 * 4 * sizeof(float);
 }
 
 hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {

@@ -116,16 +116,35 @@ def test_rmsnorm(A, dtype, d):
     assert_close(down(y), ref, dtype, "rmsnorm")
 
 
-@pytest.mark.parametrize("M,N,K", [(1, 256, 64), (77, 512, 256), (128, 256, 4096), (717, 768, 1024), (300, 4096, 128)])
-def test_linear_bf16(A, M, N, K):
+# Shapes and the schedule they take with a workspace on 256 CUs with
+# 256 x 256 tiles (T tiles, nk K steps of 64): (256, 3072, 4096) T = 12,
+# stream-K only; (520, 24576, 2048) T = 288, one data-parallel round +
+# stream-K over 32 tiles; (512, 32768, 256) T = 256, data-parallel;
+# (300, 4096, 128) nk = 2, too short for stream-K; the rest run data-parallel
+# by the cost model.
+@pytest.mark.parametrize("schedule", ["dp", "sk"])
+@pytest.mark.parametrize("M,N,K", [(1, 256, 64), (77, 512, 256), (128, 256, 4096), (717, 768, 1024), (300, 4096, 128),
+                                   (256, 3072, 4096), (520, 24576, 2048), (512, 32768, 256)])
+def test_linear_bf16(A, M, N, K, schedule):
     a = W.draw_tensor((M, K), "bf16", seed=M)
     w = W.draw_tensor((N, K), "bf16", std=0.05, seed=N + K)
     dims = A.make_dims(256, 2, 2, 128, 128, "bf16")
-    c = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"))
+    ws = A.workspace(dims, M, 1, 0) if schedule == "sk" else None
+    c = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"), ws=ws)
     ref = O.from_bits(a, "bf16") @ O.from_bits(w, "bf16").T
     assert_close(down(c), ref, "bf16", "linear")
-    c2 = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"), out=c, accumulate=True)
+    c2 = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"), out=c.clone(), accumulate=True, ws=ws)
     assert_close(down(c2), 2 * ref, "bf16", "linear accumulate")
+    if schedule == "sk":
+        # the pieces are summed in a fixed order: repeat calls agree bit for bit,
+        # and the data-parallel schedule differs by fp32 summation order only
+        again = A.acache_linear(dims, up(a, "bf16"), up(w, "bf16"), ws=ws)
+        assert _torch().equal(again, c)
+        dp = down(A.acache_linear(dims, up(a, "bf16"), up(w, "bf16")))
+        sk = down(c)
+        # one bf16 ulp, plus fp32 reordering error on outputs near zero
+        bound = 2.0 ** -7 * np.maximum(np.abs(dp), np.abs(sk)) + 1e-6 * np.abs(ref).max()
+        assert np.all(np.abs(sk - dp) <= bound)
 
 
 @pytest.mark.parametrize("M,N,K", [(90, 688, 256), (1, 5, 3), (65, 130, 77)])
