@@ -65,7 +65,9 @@ struct Cfg {
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
 struct TileMap {
-  int n_tiles, m_tiles, splits, k_per_split;
+  int n_tiles, m_tiles;
+  int splits;      // K splits (split-K partial epilogue); split i owns K steps [i nk / splits, (i+1) nk / splits)
+  int nk;          // K steps of a whole tile
   int dp_rounds;   // whole tiles per workgroup, logical tile j * dp_stride + w
   int dp_stride;
   int sk_first;    // first logical tile of the stream-K region
@@ -76,7 +78,8 @@ struct TileMap {
 
 constexpr int kGroupM = 8;       // M tiles per raster group
 constexpr int kMaxSkGroups = 256;
-constexpr int kMinSkSteps = 4;   // K steps per tile for stream-K, at least
+constexpr int kMinSkSteps = 4;   // K steps per tile for stream-K, and per split, at least
+constexpr int kMaxSplits = 16;
 
 // Workgroups are dealt round-robin to the 8 XCDs; renumber them so that each
 // XCD holds a contiguous range of logical workgroup ids.
@@ -270,7 +273,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
   const bf16* __restrict__ X = (const bf16*)p.X;
   const bf16* __restrict__ W = (const bf16*)p.W;
   const int K = p.K;
-  const int nk_tile = tm.k_per_split / BK;
+  const int nk_tile = tm.nk;
   const int w = logical_block();
   if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
 
@@ -295,7 +298,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     if (item < tm.dp_rounds) {
       t = item * tm.dp_stride + w;
       kb = -1;  // from the split index
-      kn = nk_tile;
+      kn = 0;
       ++item;
     } else if (u < u_end) {
       const int tl = u / nk_tile;
@@ -309,7 +312,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     }
     int nt, mt, sp;
     tile_coords(tm, t, nt, mt, sp);
-    if (kb < 0) kb = sp * nk_tile;
+    if (kb < 0) {
+      kb = sp * nk_tile / tm.splits;
+      kn = (sp + 1) * nk_tile / tm.splits - kb;
+    }
     const int k0 = kb * BK;
     const int nk = kn;
 
@@ -432,7 +438,7 @@ __global__ __launch_bounds__(64) void gemm_bf16_fixup(GemmParams p, TileMap tm) 
   const int lane = threadIdx.x;
   const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
   const int wn = wave % C::WN, wm = wave / C::WN;
-  const int nk_tile = tm.k_per_split / C::BK;
+  const int nk_tile = tm.nk;
   const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
   if (first == last) return;  // the tile was finished by one workgroup
   if constexpr (EPI == EPI_QKV) {
@@ -476,16 +482,26 @@ int cu_count() {
   return n;
 }
 
+// K splits for the split-K partial epilogue.  Cost in K steps of one
+// workgroup, on kMaxSkGroups CUs (fixed, so the workspace plan and the
+// launch agree on any device): ceil(T s / G) rounds of ceil(nk / s) steps,
+// plus s fp32 slices of M x N written here and read back by the reduction,
+// about M N 8 / 9.5e6 K steps each at HBM speed.  Splits need not divide
+// nk; each keeps at least kMinSkSteps steps.
 template <class C>
 int splits_for(int M, int N, int K) {
   const int tiles = ((M + C::BM - 1) / C::BM) * (N / C::BN);
-  const int ksteps = K / C::BK;
+  const int nk = K / C::BK;
+  const int G = kMaxSkGroups;
+  const double slice = (double)M * N * 8.0 / 9.5e6;
   int best = 1;
-  // enough workgroups to cover 256 CUs about twice, K per split >= 512
-  for (int s = 1; s <= 8; ++s) {
-    if (ksteps % s || (K / s) < 512) continue;
-    best = s;
-    if (tiles * s >= 448) break;
+  double best_cost = 1e30;
+  for (int s = 1; s <= kMaxSplits && nk / s >= kMinSkSteps; ++s) {
+    const double cost = (double)((tiles * s + G - 1) / G) * ((nk + s - 1) / s) + s * slice;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = s;
+    }
   }
   return best;
 }
@@ -496,9 +512,9 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
   tm.m_tiles = (p.M + C::BM - 1) / C::BM;
   tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / (C::BN / 2) : p.N / C::BN;
   tm.splits = epi == EPI_PARTIAL ? p.splits : 1;
-  tm.k_per_split = p.K / tm.splits;
+  tm.nk = p.K / C::BK;
   const int tiles = tm.m_tiles * tm.n_tiles * tm.splits;
-  const int nk = tm.k_per_split / C::BK;
+  const int nk = tm.nk;
   int grid = tiles;
   tm.dp_rounds = 1;
   tm.dp_stride = tiles;
