@@ -1,9 +1,14 @@
 // Read-slot flash attention for gfx950 (Appendix C.1): bidirectional, no
 // mask, grouped KV heads, keys and values gathered through a slot map.
 //
-// Each wavefront owns 32 queries of one head; a workgroup of 2 wavefronts
-// shares the K/V tiles (64 keys) in LDS, double buffered, with the loads of
-// tile t+1 in flight while tile t computes.  Per tile:
+// Each wavefront owns 32 queries of one head.  A workgroup holds 64 queries
+// and KS key groups of 2 wavefronts: group g streams its own contiguous
+// range of the key tiles (64 keys each) through its own LDS tiles, double
+// buffered, with the loads of tile t+1 in flight while tile t computes.  At
+// the end the groups merge their (max, sum, O) through LDS.  Splitting the
+// keys inside the workgroup fills the SIMDs when there are few queries per
+// head (the recompute has a few hundred rows) at no extra HBM traffic.
+// Per tile:
 //
 //   S^T = K Q^T       MFMA 32x32x16, K tile as the A operand, the wave's Q
 //                     fragments (registers) as B.  Lane l then holds query
@@ -30,12 +35,11 @@ namespace acache {
 namespace {
 
 constexpr int kDh = 128;
-constexpr int kWaves = 2;
-constexpr int kTileQ = 32 * kWaves;  // queries per workgroup
+constexpr int kTileQ = 64;           // queries per workgroup (2 waves per key group)
 constexpr int kTileK = 64;           // keys per LDS stage
 constexpr int kLdK = kDh + 8;        // K tile row (elements)
 constexpr int kLdV = kTileK + 8;     // transposed V tile row (elements)
-constexpr int kThreads = 64 * kWaves;
+constexpr int kGroupThreads = 128;   // threads of one key group
 
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -65,10 +69,13 @@ __device__ __forceinline__ int key_perm(int i) {
   return (i & 16) | (8 * ((r >> 2) & 1) + (r & 3) + 4 * (r >> 3));
 }
 
-template <bool PV>
-__global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16 sK[2][kTileK * kLdK];
-  __shared__ __attribute__((aligned(16))) bf16 sV[PV ? 2 : 1][PV ? kDh * kLdV : 8];
+template <bool PV, int KS>
+__global__ __launch_bounds__(kGroupThreads * KS) void attention_kernel(AttnArgs a) {
+  constexpr int kKBytes = 2 * kTileK * kLdK * 2;      // one group's double-buffered K tiles
+  constexpr int kVBytes = PV ? 2 * kDh * kLdV * 2 : 0;
+  constexpr int kMergeBytes = (KS - 1) * 2 * 64 * (2 + (PV ? 64 : 0)) * 4;
+  constexpr int kTileBytes = KS * (kKBytes + kVBytes);
+  __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
 
   // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
   // renumber them so each XCD gets a contiguous run of the head-major
@@ -93,9 +100,15 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     b = lo;
   }
   const int g = h / (a.H / a.Hkv);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5;
+  const int gk = wave >> 1, wq = wave & 1;    // key group, query half
+  const int tid = threadIdx.x & (kGroupThreads - 1);  // thread within the key group
+  bf16* const sK0 = reinterpret_cast<bf16*>(smem + gk * (kKBytes + kVBytes));
+  bf16* const sV0 = reinterpret_cast<bf16*>(smem + gk * (kKBytes + kVBytes) + kKBytes);
+  auto sK = [&](int buf) { return sK0 + buf * (kTileK * kLdK); };
+  auto sV = [&](int buf) { return sV0 + buf * (kDh * kLdV); };
   const int n_rows = a.row_start[b + 1] - a.row_start[b];
-  const int qi = (tile - a.tile_start[b]) * kTileQ + wave * 32 + (lane & 31);
+  const int qi = (tile - a.tile_start[b]) * kTileQ + wq * 32 + (lane & 31);
   const bool q_ok = qi < n_rows;
   const int S = a.key_len[b];
   const int32_t* slots = a.slots + a.key_start[b];
@@ -159,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
     absent = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int ch = (tid + i * kThreads) & 15;
+      const int ch = (tid + i * kGroupThreads) & 15;
       const int off = off_of(k0 + (tid >> 4) + 8 * i, kslot[i]);
       absent |= (off < 0 ? 1u : 0u) << i;
       kreg[i] = *reinterpret_cast<const u32x4*>(a.k_pool + (off < 0 ? 0 : off) + ch * 8);
@@ -171,7 +184,7 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
         absent |= (off < 0 ? 1u : 0u) << (8 + r);
 #pragma unroll
         for (int it = 0; it < 2; ++it) {
-          const int dc = (tid + it * kThreads) >> 4;
+          const int dc = (tid + it * kGroupThreads) >> 4;
           vreg[it * 4 + r] = *reinterpret_cast<const u32x4*>(a.v_pool + (off < 0 ? 0 : off) + dc * 8);
         }
       }
@@ -180,14 +193,14 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
   auto store_tile = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int c = tid + i * kThreads;
+      const int c = tid + i * kGroupThreads;
       const int key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sK[buf][key * kLdK + ch * 8]) = (absent >> i) & 1u ? zero4 : kreg[i];
+      *reinterpret_cast<u32x4*>(sK(buf) + key * kLdK + ch * 8) = (absent >> i) & 1u ? zero4 : kreg[i];
     }
     if constexpr (PV) {
 #pragma unroll
       for (int it = 0; it < 2; ++it) {
-        const int item = tid + it * kThreads;
+        const int item = tid + it * kGroupThreads;
         const int kg = item & 15, dc = item >> 4;
         const bf16x8 v0 = __builtin_bit_cast(bf16x8, (absent >> 8) & 1u ? zero4 : vreg[it * 4 + 0]);
         const bf16x8 v1 = __builtin_bit_cast(bf16x8, (absent >> 9) & 1u ? zero4 : vreg[it * 4 + 1]);
@@ -197,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
         for (int e = 0; e < 8; ++e) {
           bf16x4 w;
           w[0] = v0[e]; w[1] = v1[e]; w[2] = v2[e]; w[3] = v3[e];
-          *reinterpret_cast<bf16x4*>(&sV[buf][(dc * 8 + e) * kLdV + kg * 4]) = w;
+          *reinterpret_cast<bf16x4*>(sV(buf) + (dc * 8 + e) * kLdV + kg * 4) = w;
         }
       }
     }
@@ -215,16 +228,24 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
   const int n_tiles = (S + kTileK - 1) / kTileK;
   const int krow = key_perm(lane & 31);
 
-  load_slots(0);
-  load_tile();
-  if (n_tiles > 1) load_slots(1);
-  store_tile(0);
+  // key group gk owns tiles [t_lo, t_hi); every group runs n_it iterations
+  // so the barriers line up, idle in the ones past its range
+  const int t_lo = gk * n_tiles / KS, t_hi = (gk + 1) * n_tiles / KS;
+  const int n_it = (n_tiles + KS - 1) / KS;
+  if (t_lo < t_hi) {
+    load_slots(t_lo);
+    load_tile();
+    if (t_lo + 1 < t_hi) load_slots(t_lo + 1);
+    store_tile(0);
+  }
   __syncthreads();
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < n_tiles) load_tile();
-    if (t + 2 < n_tiles) load_slots(t + 2);
-    const bf16* ks = sK[buf];
+  for (int it = 0; it < n_it; ++it) {
+    const int t = t_lo + it;
+    const int buf = it & 1;
+    if (t < t_hi) {
+    if (t + 1 < t_hi) load_tile();
+    if (t + 2 < t_hi) load_slots(t + 2);
+    const bf16* ks = sK(buf);
     f32x16 st[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -287,7 +308,7 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
       }
     l_part += psum;
     if constexpr (PV) {
-      const bf16* vs = sV[buf];
+      const bf16* vs = sV(buf);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -303,8 +324,45 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
           }
         }
     }
-    if (t + 1 < n_tiles) store_tile(buf ^ 1);
+    if (t + 1 < t_hi) store_tile(buf ^ 1);
+    }
     __syncthreads();
+  }
+
+  if constexpr (KS > 1) {
+    // groups 1.. hand (max, partial sum, O) to group 0 through LDS, per lane
+    float* xch = reinterpret_cast<float*>(smem);
+    constexpr int kVals = 2 + (PV ? 64 : 0);
+    if (gk > 0) {
+      float* dst = xch + ((gk - 1) * 2 + wq) * kVals * 64 + lane;
+      dst[0] = m_run;
+      dst[64] = l_part;
+      if constexpr (PV) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dst[(2 + d * 16 + r) * 64] = o_acc[d][r];
+      }
+    }
+    __syncthreads();
+    if (gk > 0) return;
+#pragma unroll
+    for (int o = 1; o < KS; ++o) {
+      const float* src = xch + ((o - 1) * 2 + wq) * kVals * 64 + lane;
+      const float m_o = src[0];
+      const float m_new = fmaxf(m_run, m_o);
+      // a group that saw no key has m = -inf and contributes nothing
+      const float a_self = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+      const float a_o = m_o == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_o - m_new);
+      l_part = l_part * a_self + src[64] * a_o;
+      if constexpr (PV) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o_acc[d][r] = o_acc[d][r] * a_self + src[(2 + d * 16 + r) * 64] * a_o;
+      }
+      m_run = m_new;
+    }
   }
 
   const float l_tot = l_part + __shfl_xor(l_part, 32);
@@ -326,6 +384,11 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(AttnArgs a) {
   }
 }
 
+// Key groups per workgroup: with V, two groups (2 x 70 KB of LDS, one
+// 4-wave workgroup per CU, one wave per SIMD at this register count); the
+// log-sum-exp-only variant has no V tiles and takes four.  Requests with
+// fewer key tiles than groups leave the extra groups idle, which is
+// harmless.
 template <bool PV>
 hipError_t launch(AttnArgs& a, hipStream_t s) {
   int tiles = 0;
@@ -335,7 +398,8 @@ hipError_t launch(AttnArgs& a, hipStream_t s) {
   }
   a.tile_start[a.batch] = tiles;
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(attention_kernel<PV>, dim3(tiles * a.H), dim3(kThreads), 0, s, a);
+  constexpr int KS = PV ? 2 : 4;
+  hipLaunchKernelGGL((attention_kernel<PV, KS>), dim3(tiles * a.H), dim3(kGroupThreads * KS), 0, s, a);
   return hipGetLastError();
 }
 
