@@ -225,7 +225,9 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
  *   ws          at least acache_workspace_size(dims, rows, batch, L) bytes
  * bf16 requires head_dim == 128, d_model % 256 == 0, (H*d_h) % 256 == 0,
  * (H_kv*d_h) % 128 == 0, d_ff % 128 == 0; f32 requires head_dim % 2 == 0,
- * head_dim <= 128. */
+ * head_dim <= 128.  The projections use 32-bit element offsets: rows times
+ * max(d, H*d_h, d_ff) and every weight matrix must stay below 2^31 elements
+ * (ACACHE_ERR_UNSUPPORTED otherwise; split a larger batch into calls). */
 acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer_weights* w,
                                      const acache_ragged* rg, void* x, const int32_t* pos,
                                      const int32_t* write_slots, const int32_t* read_slots,
@@ -246,7 +248,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
  *                 counts that leave CUs idle in the last round of tiles are
  *                 balanced by splitting K across workgroups (fp32 partials,
  *                 summed in a fixed order); without it every tile runs whole.
- *                 The two schedules agree up to fp32 summation order. */
+ *                 The two schedules agree up to fp32 summation order.
+ *                 M * K and N * K must be below 2^31 (32-bit offsets). */
 acache_status acache_rmsnorm(const acache_dims* dims, const void* x, const void* g, void* y,
                              int32_t rows, hipStream_t stream);
 acache_status acache_linear(const acache_dims* dims, const void* a, const void* w, void* c,

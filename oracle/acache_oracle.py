@@ -157,6 +157,18 @@ def silu(a: np.ndarray) -> np.ndarray:
     return a / (1.0 + np.exp(-a))
 
 
+def layer_kv(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray):
+    """The K and V a block writes for rows x [R, d] at positions pos: RMSNorm,
+    the K and V projections, rotation of K (Section 4.3).  Row-local, so
+    layer 0's affix K/V depend only on the affix rows' own inputs.
+    Returns (k, v), each [R, H_kv, d_h]."""
+    r = x.shape[0]
+    h = rms_norm(x, w.g1, dims.rms_eps)
+    k = (h @ w.wk.T).reshape(r, dims.n_kv_heads, dims.head_dim)
+    v = (h @ w.wv.T).reshape(r, dims.n_kv_heads, dims.head_dim)
+    return rope(k, pos, dims.rope_base), v
+
+
 def layer_forward(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray,
                   rows: np.ndarray, view_k: np.ndarray, view_v: np.ndarray):
     """One block over the recomputed rows (Section 4.3, Appendix C.1).
@@ -169,11 +181,8 @@ def layer_forward(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray,
     r = x.shape[0]
     nh, nkv, dh = dims.n_heads, dims.n_kv_heads, dims.head_dim
     h = rms_norm(x, w.g1, dims.rms_eps)
-    q = (h @ w.wq.T).reshape(r, nh, dh)
-    k = (h @ w.wk.T).reshape(r, nkv, dh)
-    v = (h @ w.wv.T).reshape(r, nkv, dh)
-    q = rope(q, pos, dims.rope_base)
-    k = rope(k, pos, dims.rope_base)
+    q = rope((h @ w.wq.T).reshape(r, nh, dh), pos, dims.rope_base)
+    k, v = layer_kv(w, dims, x, pos)
     view_k[rows] = k
     view_v[rows] = v
     o, lse = attention(q, view_k, view_v)

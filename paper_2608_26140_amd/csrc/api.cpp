@@ -322,6 +322,8 @@ acache_status acache_linear(const acache_dims* dims, const void* a, const void* 
   CHECK(M >= 0 && N >= 0 && K >= 0, ACACHE_ERR_SHAPE);
   if (M == 0 || N == 0) return ACACHE_OK;
   CHECK(a && w && c, ACACHE_ERR_NULL);
+  // operands are addressed with 32-bit element offsets
+  CHECK((int64_t)M * K < ((int64_t)1 << 31) && (int64_t)N * K < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
   if (dims->dtype == ACACHE_BF16) {
     CHECK(K > 0 && K % 64 == 0 && N % 256 == 0, ACACHE_ERR_UNSUPPORTED);
     CHECK(aligned16(a) && aligned16(w) && aligned16(c), ACACHE_ERR_ALIGN);
@@ -421,6 +423,9 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   const int hq = H * dh, hkv = Hkv * dh, nqkv = (H + 2 * Hkv) * dh;
   CHECK(pool_ld >= hkv && n_slots > 0, ACACHE_ERR_SHAPE);
   CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);  // 32-bit element offsets
+  // the projections address their operands with 32-bit element offsets
+  CHECK((int64_t)M * std::max({d, hq, F}) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK((int64_t)std::max({nqkv, 2 * F, d}) * std::max({d, hq, F}) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
   const int64_t es = (int64_t)elem_size(dims->dtype);
   CHECK(aligned16(x) && aligned16(k_pool) && aligned16(v_pool) && (pool_ld * es) % 16 == 0, ACACHE_ERR_ALIGN);
   CHECK(aligned16(w->attn_norm) && aligned16(w->w_qkv) && aligned16(w->w_o) && aligned16(w->mlp_norm) &&

@@ -83,14 +83,30 @@ class AffixBatch:
     def gather_inputs(self, m: dict, stream=None) -> torch.Tensor:
         return A.acache_gather_rows(self.x_src, m["row_src"], self.remap, stream=stream)
 
+    def request_groups(self, R: int):
+        """Requests per layer call: the library addresses projection operands
+        with 32-bit element offsets, so a batch whose rows times the widest
+        projection input reach 2^31 elements runs in groups of requests."""
+        d = self.model.dims
+        widest = max(d.d_model, d.n_heads * d.head_dim, d.d_ff)
+        per = max(1, ((1 << 31) - 1) // max(1, R * widest))
+        return [(b0, min(self.B, b0 + per)) for b0 in range(0, self.B, per)]
+
     def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None, stream=None):
         R = self.rows_per_request(k)
-        cu_rows = [b * R for b in range(self.B + 1)]
-        cu_keys = [b * self.S for b in range(self.B + 1)]
+        groups = self.request_groups(R)
+        if score is not None and len(groups) > 1:
+            raise ValueError("probe batch too large for one call")
         for n in range(self.model.n_layers):
-            A.acache_layer_recompute(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x, m["row_pos"],
-                                     m["write_slots"], m["read_slots"], self.k_pools[n], self.v_pools[n],
-                                     self.ws, score=score, stream=stream)
+            for b0, b1 in groups:
+                nb = b1 - b0
+                cu_rows = [b * R for b in range(nb + 1)]
+                cu_keys = [b * self.S for b in range(nb + 1)]
+                rows = slice(b0 * R, b1 * R)
+                A.acache_layer_recompute(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows],
+                                         m["row_pos"][rows], m["write_slots"][rows],
+                                         m["read_slots"][b0 * self.S:b1 * self.S], self.k_pools[n],
+                                         self.v_pools[n], self.ws, score=score, stream=stream)
         return x
 
     # ------------------------------------------------------------------ the method

@@ -109,3 +109,20 @@ def test_layer_recompute_validation(A):
     big = A.Ragged(65, cu_rows, cu_keys2)
     assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(big), p, p, p, p, p, p,
                                       4096, 100, None, p, 1 << 30, None) == 2
+
+
+def test_offset_limits(A):
+    """Operands whose element offsets would not fit 32 bits are rejected
+    before any launch."""
+    lib = A.lib
+    dims = A.make_dims(4096, 32, 32, 128, 12288, "bf16")
+    p = ctypes.c_void_p(16)
+    # acache_linear: M * K >= 2^31
+    assert lib.acache_linear(ctypes.byref(dims), p, p, p, 1 << 20, 256, 4096, 0, None, 0, None) == 4
+    # acache_layer_recompute: rows * d_ff >= 2^31 (200000 rows of a 12288-wide MLP)
+    cu_rows = (ctypes.c_int32 * 2)(0, 200000)
+    cu_keys = (ctypes.c_int32 * 2)(0, 200000)
+    rg = A.Ragged(1, cu_rows, cu_keys)
+    w = A.LayerWeights(16, 16, 16, 16, 16, 16)
+    assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(rg), p, p, p, p, p, p,
+                                      4096, 100, None, p, 1 << 62, None) == 4
