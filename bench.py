@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"bf16": (2500.0, "mfma"), "f32": (157.3, "alu")}  # TFLOP/s, dense
+HBM_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 KERNELS = ["gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down", "attention", "score_lse", "score_colsum",
            "score_reduce", "rmsnorm", "residual", "topk", "gather", "maps"]
 
@@ -75,6 +76,26 @@ def flops_model(w):
     out["probe"]["score_lse"] = score / 2
     out["probe"]["score_colsum"] = score / 2
     return out, rows
+
+
+def bytes_model(w):
+    """Algorithmic HBM bytes of one step for the data-movement kernels: each
+    operand read once and each result written once (the split-K partials of
+    the residual kernel are an implementation choice and not counted)."""
+    d = w.dims
+    lay = w.layout
+    B, S, L, N = w.batch, lay.seq_len, lay.affix_len, d.n_layers
+    es = 2 if d.dtype == "bf16" else 4
+    rows = B * lay.n_nonaffix + B * w.rows_selective  # probe + refresh rows
+    return {
+        "gather": 2 * rows * d.d_model * es,
+        "rmsnorm": 2 * rows * d.d_model * es * N,
+        # after the O projection: x in, x out, RMSNorm y out; after down: x in, x out
+        "residual": 5 * rows * d.d_model * es * N,
+        "topk": B * L * 4 + B * w.n_anchors * 4,
+        "maps": 4 * (3 * rows + 2 * B * S),
+        "score_reduce": 4 * (d.n_heads + 1) * B * L * N,
+    }
 
 
 def main():
@@ -183,6 +204,21 @@ def main():
 
     peak, bound = PEAK[d.dtype]
     step_flops = sum(fl["probe"].values()) + sum(fl["refresh"].values())
+    by = bytes_model(w)
+    kernel_roofline = {}
+    for k, v in breakdown.items():
+        sec = v["us_per_step"] * 1e-6
+        if sec <= 0:
+            continue
+        f = fl["probe"].get(k, 0) + fl["refresh"].get(k, 0)
+        if f:
+            a = f / sec / 1e12
+            kernel_roofline[k] = {"us": round(v["us_per_step"], 2), "achieved": round(a, 1), "unit": "TFLOP/s",
+                                  "frac": round(a / peak, 4)}
+        elif k in by:
+            a = by[k] / sec / 1e9
+            kernel_roofline[k] = {"us": round(v["us_per_step"], 2), "achieved": round(a, 1), "unit": "GB/s",
+                                  "frac": round(a / HBM_GBS, 4)}
     achieved = dom_flops_step / (dom_ms_step * 1e-3) / 1e12 if dom_ms_step > 0 else 0.0
     traffic = None
     tfile = os.path.join(ROOT, "profiles", "traffic.json")
@@ -225,6 +261,7 @@ def main():
         "full_mfma_util": None if ms_full is None else round(
             sum(fl["full"].values()) / (ms_full * 1e-3) / 1e12 / peak, 4),
         "kernel_us_per_step": {k: round(v["us_per_step"], 2) for k, v in breakdown.items()},
+        "kernel_roofline": kernel_roofline,
         "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 1), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
                      "launches_per_step": dom_launches_step,
@@ -266,17 +303,28 @@ def copy_calibration(args, A):
 def cpu_baseline(w, host, budget_s):
     """The fp64 oracle on this host's cores: probe + top-K + selective refresh
     of request 0 (one request of the batch), repeated until about budget_s;
-    reported as recomputed tokens/s of that sample."""
+    reported as recomputed tokens/s of that sample.  For a stack the sample
+    is layer 0 only (its shared affix cache is the layer-0 K/V of the affix
+    rows, which are row-local), and the rate is extrapolated to all layers."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import acache_oracle as O
     from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
 
-    layers = oracle_layers(w, host)
-    sk, sv = oracle_stale(w, host, layers)
     dims = oracle_dims(w)
     req = oracle_request(w, host, 0)
+    n_layers = w.dims.n_layers
+    if n_layers == 1:
+        layers = oracle_layers(w, host)
+        sk, sv = oracle_stale(w, host, layers)
+    else:
+        lay = w.layout
+        layers = [O.layer_from_bits(host["layers"][0], dims, w.dims.dtype)]
+        affix = np.arange(lay.affix_begin, lay.affix_end)
+        k0, v0 = O.layer_kv(layers[0], dims, O.from_bits(host["embedding"][host["donor_ids"][affix]],
+                                                          w.dims.dtype), affix)
+        sk, sv = [k0], [v0]
     n, t = 0, 0.0
     while t < budget_s and n < 100:
         t0 = time.perf_counter()
@@ -285,10 +333,12 @@ def cpu_baseline(w, host, budget_s):
         t += time.perf_counter() - t0
         n += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    return {"value": round(n * w.rows_selective / t, 2), "unit": "recomputed tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"request 0 of {w.batch}: probe + top-K + selective refresh ({w.rows_selective} rows), "
-                      f"{n} repetitions in {t:.1f}s, fp64 NumPy"}
+    sample = (f"request 0 of {w.batch}: probe + top-K + selective refresh ({w.rows_selective} rows), "
+              f"{n} repetitions in {t:.1f}s, fp64 NumPy")
+    if n_layers > 1:
+        sample += f"; layer 0 only, rate extrapolated to {n_layers} layers (time x {n_layers})"
+    return {"value": round(n * w.rows_selective / (t * n_layers), 2), "unit": "recomputed tokens/s",
+            "cores": threads, "kind": "oracle", "sample": sample}
 
 
 if __name__ == "__main__":
