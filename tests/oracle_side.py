@@ -57,3 +57,16 @@ def anchors_agree(got, ref, scores_ref, k, tol_rel):
     for j in got ^ ref:
         assert abs(scores_ref[j] - kth) <= band, f"anchor {j} outside the tie band ({scores_ref[j]} vs {kth})"
     return overlap
+
+
+def assert_overlap(overlap, scores_ref, k, tol_rel, what=""):
+    """The anchor-set overlap must reach 99%, except where the oracle's own
+    K-th and (K+1)-th scores are closer than the tie band: then swapping
+    them is within the scores' tolerance and anchors_agree has already
+    checked that every swap lies in the band."""
+    if overlap >= 0.99 or k == 0 or k >= len(scores_ref):
+        return
+    s = np.sort(np.asarray(scores_ref, dtype=np.float64))[::-1]
+    gap = s[k - 1] - s[k]
+    assert gap <= tol_rel * abs(s[k - 1]), (
+        f"{what}: anchor overlap {overlap:.3f} < 0.99 with a clear boundary (K-th/K+1-th gap {gap:.3e})")

@@ -17,7 +17,7 @@ import pytest
 import workloads as W
 from oracle import acache_oracle as O
 from tests.gpu_util import assert_close, down, up, up_i32
-from tests.oracle_side import anchors_agree, oracle_dims, oracle_request
+from tests.oracle_side import anchors_agree, assert_overlap, oracle_dims, oracle_request
 
 pytestmark = pytest.mark.gpu
 
@@ -64,7 +64,7 @@ def test_layer0_full_size(case):
     assert_close(down(scores)[b], probe.scores, "f32" if dt == "f32" else "bf16", f"scores request {b}")
     ref_anchors = O.topk_anchors(probe.scores, K)
     overlap = anchors_agree(down(anchors)[b], ref_anchors, probe.scores, K, 2e-2)
-    assert overlap >= 0.99, f"anchor overlap {overlap:.3f}"
+    assert_overlap(overlap, probe.scores, K, 2e-2, f"request {b}")
 
     a = down(anchors).astype(np.int32)
     a[b] = ref_anchors
