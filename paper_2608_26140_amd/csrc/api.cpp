@@ -114,6 +114,7 @@ acache_status check_cu(const int32_t* cu, int batch) {
 // Workspace plan for `rows` rows (layer_recompute / score / linear).
 struct WsPlan {
   size_t y, q, o, h, part, qkv, gu, lse, lse_aff, colsum, total;
+  size_t part_bytes;  // size of the part region (split-K / stream-K / attention key-split partials)
 };
 
 WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
@@ -143,7 +144,8 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
     }
     // split-K partials of the O / down projections and the stream-K pieces
     // of the QKV / gate-up projections are never live at the same time
-    w.part = take(std::max(part_rows * d->d_model * sizeof(float), gemm_bf16_sk_ws_bytes()));
+    w.part_bytes = std::max(part_rows * d->d_model * sizeof(float), gemm_bf16_sk_ws_bytes());
+    w.part = take(w.part_bytes);
     w.qkv = w.gu = 0;
   } else {
     w.qkv = take(M * (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim * es);
@@ -364,7 +366,7 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
         ACACHE_ERR_ALIGN);
   if (dims->dtype == ACACHE_BF16)
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, dims->n_heads, dims->n_kv_heads, q, read_slots, k_pool, v_pool,
-                                 pool_ld, n_slots, out, lse, stream));
+                                 pool_ld, n_slots, out, lse, nullptr, 0, stream));
   else
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_f32(r, dims->n_heads, dims->n_kv_heads, dims->head_dim, (const float*)q,
                                 read_slots, (const float*)k_pool, (const float*)v_pool, pool_ld, n_slots,
@@ -471,7 +473,9 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     g.rope_base = dims->rope_base;
     g.sk_ws = at<float>(ws, p.part);
     LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
-    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse, stream));
+    // the part region is idle between the QKV fixup and the O projection
+    LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse,
+                                                                at<float>(ws, p.part), p.part_bytes, stream));
   } else {
     float* qkv = at<float>(ws, p.qkv);
     LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));

@@ -68,10 +68,11 @@ int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL
 size_t gemm_bf16_sk_ws_bytes();             // stream-K workspace (any shape)
 
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
+// part / part_bytes: optional fp32 space for key splits (null: one split)
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,
-                                 hipStream_t s);
+                                 float* part, size_t part_bytes, hipStream_t s);
 int attention_tile_rows();
 // Per masked row and head, natural-log LSE over the affix keys.
 hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,

@@ -27,6 +27,8 @@
 // base 2 on log2(e)/sqrt(d_h)-prescaled logits (hardware exp2).  The same
 // kernel without the V half computes only the row log-sum-exp; it serves the
 // affix-only normalisation of the probe scores (Eq. 4).
+#include <algorithm>
+
 #include "device.h"
 #include "internal.h"
 
@@ -403,15 +405,356 @@ hipError_t launch(AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+
+// ============================================================================
+// Read-slot attention with the K/V tiles loaded straight into LDS.
+//
+// A workgroup holds 128 queries of one head (4 wavefronts x 32) and streams
+// a contiguous range of the request's key tiles (64 keys) through a
+// two-stage LDS ring; two workgroups fit one CU, two wavefronts per SIMD.
+// Loads are global -> LDS (16 bytes per lane, no staging registers):
+//   K tile [64 keys][256 B], 16-byte chunk c of key row r at c ^ (r & 15):
+//     the 16 rows read by one ds_read_b128 pass hit 16 distinct chunks;
+//   V tile [64 keys][256 B] untransposed, chunk c at c ^ 2 (r & 3).
+// The A operand of O^T = V^T P^T (8 consecutive keys of one dimension per
+// lane) comes from two transposing LDS reads (ds_read_b64_tr_b16): in each
+// 16-lane group, lane l receives element l % 4 of the 8-byte runs addressed
+// by lanes l / 4, l / 4 + 4, l / 4 + 8, l / 4 + 12; lane i therefore points
+// at key key0 + i / 4, dimensions dgroup + 4 (i % 4) .. + 3, and receives
+// keys key0 .. key0 + 3 of dimension dgroup + l.
+// Keys that are absent (past the request's end, or an out-of-range slot)
+// load slot 0 and the loading lane zeroes its LDS chunk once the data has
+// landed; keys past the end are also masked to -inf in the softmax.
+// With several key splits the workgroup writes its unnormalised O and its
+// (max, sum) in fp32 and attention_merge_kernel combines the splits.
+// ============================================================================
+
+typedef short v4i16 __attribute__((__vector_size__(4 * sizeof(short))));
+
+constexpr int kPvWaves = 4;
+constexpr int kPvTileQ = 32 * kPvWaves;
+constexpr int kPvThreads = 64 * kPvWaves;
+constexpr int kRowB = kDh * 2;                    // bytes per key row
+constexpr int kTileB = kTileK * kRowB;            // 16 KB: one K or V tile
+constexpr int kStageB = 2 * kTileB;               // K tile + V tile
+constexpr int kDmaPerTile = kTileB / 1024 / kPvWaves;  // 1 KB loads per wave per tile
+
+struct PvArgs {
+  AttnArgs a;
+  int splits;
+  float* part_o;   // [splits][rows][H][128] unnormalised O (splits > 1)
+  float* part_ml;  // [splits][rows][H][2] (running max in log2 units, sum)
+};
+
+__device__ __forceinline__ void dma16(const char* g, char* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+__device__ __forceinline__ v4i16 ds_read_tr16(const char* lds) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)lds);
+}
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) {
+  __shared__ __attribute__((aligned(1024))) char ring[2 * kStageB];
+  const AttnArgs& a = pa.a;
+  const int splits = pa.splits;
+
+  // XCD-contiguous, head-major order of (head, query tile, key split)
+  const int n_tiles_q = a.tile_start[a.batch];
+  int h, tile, split;
+  {
+    const int nb = gridDim.x, i = blockIdx.x;
+    const int q8 = nb >> 3, r8 = nb & 7, x = i & 7;
+    const int t = x * q8 + min(x, r8) + (i >> 3);
+    h = t / (n_tiles_q * splits);
+    const int rem = t - h * n_tiles_q * splits;
+    tile = rem / splits;
+    split = rem - tile * splits;
+  }
+  int b = 0;
+  {
+    int lo = 0, hi = a.batch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+  }
+  const int g = h / (a.H / a.Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
+  const int n_rows = a.row_start[b + 1] - a.row_start[b];
+  const int qi = (tile - a.tile_start[b]) * kPvTileQ + wave * 32 + (lane & 31);
+  const bool q_ok = qi < n_rows;
+  const int S = a.key_len[b];
+  const int32_t* slots = a.slots + a.key_start[b];
+  const int n_kt = (S + kTileK - 1) / kTileK;
+  const int t_lo = split * n_kt / splits, t_hi = (split + 1) * n_kt / splits;
+
+  bf16x8 qf[8];
+  {
+    int64_t qrow = q_ok ? (int64_t)a.row_start[b] + qi : -1;
+    const bf16* qp = a.q + (qrow < 0 ? 0 : qrow) * a.q_ld + h * kDh + hl * 8;
+#pragma unroll
+    for (int s2 = 0; s2 < 8; ++s2) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (qrow >= 0) v = *reinterpret_cast<const u32x4*>(qp + s2 * 16);
+      qf[s2] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  // this lane's 4 keys of a tile (one per load): key 16 wave + 4 i + lane / 16,
+  // 16-byte chunk position lane % 16
+  const int pch = lane & 15;
+  const uint32_t head_b = (uint32_t)g * kRowB;
+  const uint32_t ld_b = (uint32_t)a.pool_ld * 2u;
+  int slot_next[kDmaPerTile];   // slots of the tile to issue next
+  unsigned absent_bits = 0;     // bit i: this lane's key i of the in-flight tile is absent
+  auto key_of = [&](int t, int i) { return t * kTileK + wave * 16 + 4 * i + (lane >> 4); };
+  auto load_slots = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < kDmaPerTile; ++i) slot_next[i] = slots[min(key_of(t, i), S - 1)];
+  };
+  auto issue = [&](int t) {
+    char* st = ring + (t & 1) * kStageB;
+    unsigned ab = 0;
+#pragma unroll
+    for (int i = 0; i < kDmaPerTile; ++i) {
+      const int key = key_of(t, i);
+      const int sl = slot_next[i];
+      const bool ok = key < S && sl >= 0 && sl < a.n_slots;
+      ab |= (ok ? 0u : 1u) << i;
+      const uint32_t base = (ok ? (uint32_t)sl : 0u) * ld_b + head_b;
+      const int r = key & (kTileK - 1);
+      const int ck = pch ^ (r & 15), cv = pch ^ ((r & 3) << 1);
+      const int dst = (wave * kDmaPerTile + i) * 1024;
+      dma16((const char*)a.k_pool + base + ck * 16, st + dst);
+      dma16((const char*)a.v_pool + base + cv * 16, st + kTileB + dst);
+    }
+    absent_bits = ab;
+  };
+  // zero the chunks this lane loaded for absent keys (after they landed)
+  auto fix_absent = [&](int t) {
+    if (absent_bits) {
+      char* st = ring + (t & 1) * kStageB;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int i = 0; i < kDmaPerTile; ++i)
+        if ((absent_bits >> i) & 1u) {
+          const int dst = (wave * kDmaPerTile + i) * 1024 + lane * 16;
+          *reinterpret_cast<u32x4*>(st + dst) = z;
+          *reinterpret_cast<u32x4*>(st + kTileB + dst) = z;
+        }
+    }
+  };
+
+  f32x16 o_acc[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o_acc[d][r] = 0.f;
+  float m_run = -INFINITY, l_part = 0.f;
+  const float scale = kLog2e * rsqrtf((float)kDh);
+  const int krow = key_perm(lane & 31);
+  // K fragment byte offsets inside a tile for key block 0 (block 1: + 32 rows)
+  const int k_row_off = krow * kRowB;
+  const int k_sw = krow & 15;  // same for krow + 32
+  // transposing V reads: this lane's 16-lane group and index in it
+  const int grp = lane >> 4, gi = lane & 15;
+  const int v_key = 8 * (grp >> 1) + (gi >> 2);  // + 32 kb + 16 g2 (+ 4 for the second read)
+  const int v_chunk_lo = 2 * (grp & 1) + ((gi & 3) >> 1);  // + 4 d
+  const int v_byte = (gi & 1) * 8;
+  const int v_sw = (gi >> 2) << 1;  // 2 (row & 3), row & 3 == gi / 4 (key0 is a multiple of 4)
+
+  if (t_lo < t_hi) {
+    load_slots(t_lo);
+    issue(t_lo);
+    if (t_lo + 1 < t_hi) load_slots(t_lo + 1);
+  }
+  for (int t = t_lo; t < t_hi; ++t) {
+    // tile t (and the slot indices of t + 1) have landed in this wave
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    fix_absent(t);
+    lds_barrier();
+    if (t + 1 < t_hi) {
+      issue(t + 1);  // into the slot of tile t - 1, which every wave has finished
+      if (t + 2 < t_hi) load_slots(t + 2);
+    }
+    const char* ks = ring + (t & 1) * kStageB;
+    const char* vs = ks + kTileB;
+    f32x16 st[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 kf[8];
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2)
+        kf[s2] = *reinterpret_cast<const bf16x8*>(ks + kb * 32 * kRowB + k_row_off + (((2 * s2 + hl) ^ k_sw) << 4));
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[kb][r] = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) st[kb] = mfma32x32x16(kf[s2], qf[s2], st[kb]);
+    }
+    const int kt0 = t * kTileK;
+    float mx = -INFINITY;
+    if (kt0 + kTileK <= S) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kb][r]);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
+          st[kb][r] = key < S ? st[kb][r] : -INFINITY;
+          mx = fmaxf(mx, st[kb][r]);
+        }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale;
+    // lazy rescale: the running max moves only when exceeded by more than 2^8
+    const bool bump = mx > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(bump)) {
+      const float m_new = bump ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(fmaf(st[kb][r], scale, -m_run));
+        st[kb][r] = e;
+        psum += e;
+      }
+    l_part += psum;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int g2 = 0; g2 < 2; ++g2) {
+        bf16x8 pb;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pb[j] = (bf16)st[kb][8 * g2 + j];
+        const int row0 = kb * 32 + g2 * 16 + v_key;  // first of this lane's 4 address rows
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const int off = ((4 * d + v_chunk_lo) ^ v_sw) * 16 + v_byte;
+          const v4i16 lo = ds_read_tr16(vs + row0 * kRowB + off);
+          const v4i16 hi = ds_read_tr16(vs + (row0 + 4) * kRowB + off);
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          o_acc[d] = mfma32x32x16(vf, pb, o_acc[d]);
+        }
+      }
+  }
+
+  const float l_tot = l_part + __shfl_xor(l_part, 32);
+  if (!q_ok) return;
+  const int64_t row = a.row_start[b] + qi;
+  if (splits > 1) {
+    // unnormalised partial: O^T register r of block d holds dims 32 d + 8 (r / 4) + 4 hl + r % 4
+    float* po = pa.part_o + (((int64_t)split * a.row_start[a.batch] + row) * a.H + h) * kDh;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const f32x4 v = {o_acc[d][4 * gq], o_acc[d][4 * gq + 1], o_acc[d][4 * gq + 2], o_acc[d][4 * gq + 3]};
+        *reinterpret_cast<f32x4*>(po + d * 32 + 8 * gq + 4 * hl) = v;
+      }
+    if (hl == 0) {
+      float* pm = pa.part_ml + (((int64_t)split * a.row_start[a.batch] + row) * a.H + h) * 2;
+      pm[0] = m_run;
+      pm[1] = l_tot;
+    }
+    return;
+  }
+  if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run + __log2f(l_tot)) * kLn2;
+  const float inv = 1.f / l_tot;
+  bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      bf16x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = (bf16)(o_acc[d][4 * gq + j] * inv);
+      *reinterpret_cast<bf16x4*>(op + d * 32 + 8 * gq + 4 * hl) = w;
+    }
+}
+
+// Combines the key splits of each (row, head): m = max_s m_s,
+// O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.  32 threads per
+// (row, head), 4 dimensions each.
+__global__ __launch_bounds__(256) void attention_merge_kernel(const float* __restrict__ part_o,
+                                                              const float* __restrict__ part_ml, int splits,
+                                                              int64_t rows, int H, bf16* __restrict__ out,
+                                                              float* __restrict__ lse) {
+  const int64_t pair = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
+  if (pair >= rows * H) return;
+  const int c = (threadIdx.x & 31) * 4;
+  float m = -INFINITY;
+  for (int s2 = 0; s2 < splits; ++s2) m = fmaxf(m, part_ml[((int64_t)s2 * rows * H + pair) * 2]);
+  float l = 0.f;
+  f32x4 o = {0.f, 0.f, 0.f, 0.f};
+  for (int s2 = 0; s2 < splits; ++s2) {
+    const float* ml = part_ml + ((int64_t)s2 * rows * H + pair) * 2;
+    const float w = ml[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ml[0] - m);
+    l += w * ml[1];
+    const f32x4 v = *reinterpret_cast<const f32x4*>(part_o + ((int64_t)s2 * rows * H + pair) * kDh + c);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] += w * v[j];
+  }
+  const float inv = 1.f / l;
+  bf16x4 w;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) w[j] = (bf16)(o[j] * inv);
+  *reinterpret_cast<bf16x4*>(out + pair * kDh + c) = w;
+  if (lse && c == 0) lse[pair] = (m + __log2f(l)) * kLn2;
+}
+
 }  // namespace
 
 int attention_tile_rows() { return kTileQ; }
 
+
+// Key splits for the read-slot attention.  Cost in 64-key tiles of one
+// workgroup (about 1 us each): rounds of 512 resident workgroups (two per
+// CU) times the tiles per split, plus the merge traffic (each split's fp32
+// O and (m, l) written and read back at about 4 TB/s).  The partials must
+// fit in part_bytes.
+static int attention_splits(int n_wg, int n_kt, int64_t rows, int H, size_t part_bytes) {
+  const int64_t per_split = rows * H * (kDh * 4 + 8);
+  int best = 1;
+  double best_cost = 1e30;
+  for (int s = 1; s <= 8 && s <= n_kt; ++s) {
+    if (s > 1 && (size_t)(per_split * s) > part_bytes) break;
+    const double rounds = (double)((n_wg * s + 511) / 512);
+    const double tiles = (double)((n_kt + s - 1) / s);
+    // merge: 2 x per_split x s bytes at ~4 TB/s, one 64-key tile of a workgroup ~1 us
+    const double merge = s > 1 ? 2.0 * per_split * s / 4e12 / 1e-6 : 0.0;
+    const double cost = rounds * tiles + merge;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = s;
+    }
+  }
+  return best;
+}
+
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,
-                                 hipStream_t s) {
-  AttnArgs a = {};
+                                 float* part, size_t part_bytes, hipStream_t s) {
+  PvArgs pa = {};
+  AttnArgs& a = pa.a;
   a.q = (const bf16*)q;
   a.q_ld = (int64_t)H * kDh;
   a.q_n_rows = rg.cu_rows[rg.batch];
@@ -426,12 +769,31 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   a.H = H;
   a.Hkv = Hkv;
   a.batch = rg.batch;
+  int tiles = 0, max_kt = 0;
   for (int b = 0; b <= rg.batch; ++b) {
     a.row_start[b] = rg.cu_rows[b];
     a.key_start[b] = rg.cu_keys[b];
   }
-  for (int b = 0; b < rg.batch; ++b) a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
-  return launch<true>(a, s);
+  for (int b = 0; b < rg.batch; ++b) {
+    a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
+    a.tile_start[b] = tiles;
+    tiles += (a.row_start[b + 1] - a.row_start[b] + kPvTileQ - 1) / kPvTileQ;
+    max_kt = std::max(max_kt, (a.key_len[b] + kTileK - 1) / kTileK);
+  }
+  a.tile_start[rg.batch] = tiles;
+  if (tiles == 0) return hipSuccess;
+  const int64_t rows = rg.cu_rows[rg.batch];
+  const int splits = part ? attention_splits(tiles * H, max_kt, rows, H, part_bytes) : 1;
+  pa.splits = splits;
+  pa.part_o = part;
+  pa.part_ml = part ? part + (size_t)splits * rows * H * kDh : nullptr;
+  hipLaunchKernelGGL(attention_pv_kernel, dim3(tiles * H * splits), dim3(kPvThreads), 0, s, pa);
+  if (splits > 1) {
+    const int64_t pairs = rows * H;
+    hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s,
+                       (const float*)pa.part_o, (const float*)pa.part_ml, splits, rows, H, (bf16*)out, lse);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
