@@ -236,6 +236,19 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
                                      hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_argmax_commit — the commit half of the predict-then-commit loop
+ * (Section 3.1; the online loop of Section 4.3), in its greedy form: for
+ * every row i < rows, out[i] = the index of the largest of x[i, 0 .. n),
+ * comparing values as numbers with -0 == +0 and NaN below everything, the
+ * lowest index among equal values.  With commit_pos (nullable) the index is
+ * also written to ids[commit_pos[i]]; positions outside [0, ids_len) are
+ * skipped.  x [rows, ld] of `dtype` (logits).  rows == 0: no-op; n == 0
+ * with rows > 0: ACACHE_ERR_SHAPE. */
+acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
+                                   int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                   hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Building blocks of acache_layer_recompute, exported so each can be checked
  * on its own.
  *
@@ -280,7 +293,8 @@ typedef enum {
   ACACHE_K_GATHER = 11,
   ACACHE_K_MAPS = 12,
   ACACHE_K_SCATTER = 13,
-  ACACHE_K_COUNT = 14
+  ACACHE_K_ARGMAX = 14,
+  ACACHE_K_COUNT = 15
 } acache_kernel_id;
 acache_status acache_time_kernel(int32_t kernel, hipEvent_t* starts, hipEvent_t* stops,
                                  int32_t capacity, int32_t* count);

@@ -235,6 +235,19 @@ def topk_anchors(s: np.ndarray, k: int) -> np.ndarray:
     return np.sort(order[:k])
 
 
+def greedy_commit(logits: np.ndarray) -> np.ndarray:
+    """The commit step of the predict-then-commit loop (Section 3.1) in its
+    greedy form, as the serving schedule uses it: per row of logits, the
+    index of the largest value, -0 == +0, NaN below every value, the lowest
+    index among equal values (int64)."""
+    x = np.asarray(logits, dtype=np.float64)
+    out = np.empty(x.shape[0], dtype=np.int64)
+    for i, row in enumerate(x):
+        nan = np.isnan(row)
+        out[i] = np.lexsort((np.arange(row.size), -np.where(nan, 0.0, row), nan))[0]
+    return out
+
+
 # ----------------------------------------------------------------------------
 # requests: probe, selective refresh, full refresh, direct reuse
 # ----------------------------------------------------------------------------

@@ -64,6 +64,7 @@ def _load():
         "acache_topk": [P, I32, I32, I32, P, P],
         "acache_gather_rows": [P, I64, I64, P, P, I64, I32, I32, P, I64, P],
         "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
+        "acache_argmax_commit": [I32, P, I64, I32, I32, P, P, P, I64, P],
         "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
@@ -267,10 +268,28 @@ def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[to
     return out
 
 
+def acache_argmax_commit(x: torch.Tensor, out: Optional[torch.Tensor] = None,
+                         commit_pos: Optional[torch.Tensor] = None, ids: Optional[torch.Tensor] = None,
+                         stream=None) -> torch.Tensor:
+    """Row argmax of x [rows, n] (lowest index on ties, NaN lowest); with
+    commit_pos, also ids[commit_pos[i]] = argmax of row i."""
+    rows, n = x.shape
+    if out is None:
+        out = torch.empty(rows, dtype=torch.int32, device=x.device)
+    if commit_pos is not None:
+        _dev_i32(commit_pos, "commit_pos")
+        _dev_i32(ids, "ids")
+    dt = ACACHE_BF16 if x.dtype == torch.bfloat16 else ACACHE_F32
+    _check("acache_argmax_commit", lib.acache_argmax_commit(
+        dt, _ptr(x), x.stride(0), rows, n, _ptr(out), _ptr(commit_pos), _ptr(ids),
+        0 if ids is None else ids.numel(), _stream(stream)))
+    return out
+
+
 # ---------------------------------------------------------------------------- measurement hook
 KERNEL_IDS = {"gemm_qkv": 0, "gemm_o": 1, "gemm_gate_up": 2, "gemm_down": 3, "attention": 4, "score_lse": 5,
               "score_colsum": 6, "score_reduce": 7, "rmsnorm": 8, "residual": 9, "topk": 10, "gather": 11,
-              "maps": 12, "scatter": 13}
+              "maps": 12, "scatter": 13, "argmax": 14}
 lib.acache_time_kernel.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                    ctypes.POINTER(ctypes.c_int32)]
 lib.acache_time_kernel.restype = ctypes.c_int32

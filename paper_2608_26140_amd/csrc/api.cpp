@@ -281,6 +281,18 @@ acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t sr
   return ACACHE_OK;
 }
 
+acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
+                                   int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                   hipStream_t stream) {
+  CHECK(dtype == ACACHE_BF16 || dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
+  CHECK(rows >= 0 && n >= 0 && ld >= n && ids_len >= 0, ACACHE_ERR_SHAPE);
+  if (rows == 0) return ACACHE_OK;
+  CHECK(n > 0, ACACHE_ERR_SHAPE);
+  CHECK(x && out && (!commit_pos || ids), ACACHE_ERR_NULL);
+  LAUNCH_T(ACACHE_K_ARGMAX, stream, launch_argmax_commit(dtype, x, ld, rows, n, out, commit_pos, ids, ids_len, stream));
+  return ACACHE_OK;
+}
+
 acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const int32_t* anchors,
                                 int32_t k, int32_t* row_pos, int32_t* row_src,
                                 int32_t* write_slots, int32_t* read_slots, int32_t* q_rows,

@@ -29,6 +29,14 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Order-preserving 32-bit key of an fp32 bit pattern: larger float, larger
+// key; -0 is folded onto +0 and NaN maps below -inf (key 0).
+__device__ __forceinline__ uint32_t order_key(uint32_t u) {
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0u;  // NaN: below everything
+  if (u == 0x80000000u) u = 0u;                     // -0 == +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 // sin and cos of a rotary angle given in fp64.  The angle is reduced to
 // r = ang - q * pi/2, |r| <= pi/4, in fp64 (the product pos * theta_i is
 // exact enough there for any position), then both functions are Taylor

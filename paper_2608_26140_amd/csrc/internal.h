@@ -67,6 +67,9 @@ hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s);
 int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL
 size_t gemm_bf16_sk_ws_bytes();             // stream-K workspace (any shape)
 
+hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int rows, int n, int32_t* out,
+                               const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s);
+
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
 // part / part_bytes: optional fp32 space for key splits (null: one split)
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,

@@ -199,6 +199,68 @@ inline int grid_for(int64_t work, int per_block = 256, int cap = 65535) {
   return (int)(g > cap ? cap : g);
 }
 
+
+// ---------------------------------------------------------------- greedy commit
+// One workgroup per row: the index of the largest element by order_key (NaN
+// lowest, -0 == +0), the lowest index among equal keys.  out[row] = index and,
+// with commit_pos, ids[commit_pos[row]] = index (an out-of-range position is
+// skipped).
+__device__ __forceinline__ void argmax_take(uint32_t key, int idx, uint32_t& bk, int& bi) {
+  if (key > bk || (key == bk && idx < bi)) {
+    bk = key;
+    bi = idx;
+  }
+}
+__device__ __forceinline__ uint32_t elem_bits(bf16 v) { return (uint32_t)__builtin_bit_cast(uint16_t, v) << 16; }
+__device__ __forceinline__ uint32_t elem_bits(float v) { return __builtin_bit_cast(uint32_t, v); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void argmax_commit_kernel(const T* __restrict__ x, int64_t ld, int n, int vec,
+                                                            int32_t* __restrict__ out,
+                                                            const int32_t* __restrict__ commit_pos,
+                                                            int32_t* __restrict__ ids, int64_t ids_len) {
+  constexpr int PER = 16 / sizeof(T);
+  const int64_t row = blockIdx.x;
+  const T* xr = x + row * ld;
+  uint32_t bk = 0u;
+  int bi = 0x7FFFFFFF;
+  int start = 0;
+  if (vec) {
+    const int chunks = n / PER;
+    for (int c = threadIdx.x; c < chunks; c += 256) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(xr + (int64_t)c * PER);
+      T v[PER];
+      __builtin_memcpy(v, &raw, 16);
+#pragma unroll
+      for (int j = 0; j < PER; ++j) argmax_take(order_key(elem_bits(v[j])), c * PER + j, bk, bi);
+    }
+    start = chunks * PER;
+  }
+  for (int i = start + threadIdx.x; i < n; i += 256) argmax_take(order_key(elem_bits(xr[i])), i, bk, bi);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t ok = __shfl_xor(bk, o);
+    const int oi = __shfl_xor(bi, o);
+    argmax_take(ok, oi, bk, bi);
+  }
+  __shared__ uint32_t sk[4];
+  __shared__ int si[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    sk[wave] = bk;
+    si[wave] = bi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int w = 1; w < 4; ++w) argmax_take(sk[w], si[w], bk, bi);
+    out[row] = bi;
+    if (commit_pos) {
+      const int64_t p = commit_pos[row];
+      if (p >= 0 && p < ids_len) ids[p] = bi;
+    }
+  }
+}
 }  // namespace
 
 hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
@@ -245,6 +307,19 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
                                   const void* g, void* y, float eps, hipStream_t s) {
   hipLaunchKernelGGL(reduce_residual_kernel, dim3(M), dim3(256), 0, s, (bf16*)x, part, splits, M, d,
                      (const bf16*)g, (bf16*)y, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int rows, int n, int32_t* out,
+                               const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s) {
+  const int es = dt == ACACHE_BF16 ? 2 : 4;
+  const int vec = ((uintptr_t)x % 16 == 0 && (ld * es) % 16 == 0) ? 1 : 0;
+  if (dt == ACACHE_BF16)
+    hipLaunchKernelGGL(argmax_commit_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x, ld, n, vec, out,
+                       commit_pos, ids, ids_len);
+  else
+    hipLaunchKernelGGL(argmax_commit_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x, ld, n, vec, out,
+                       commit_pos, ids, ids_len);
   return hipGetLastError();
 }
 

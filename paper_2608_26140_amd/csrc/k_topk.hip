@@ -17,12 +17,6 @@ namespace {
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
 
-__device__ __forceinline__ uint32_t order_key(uint32_t u) {
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0u;  // NaN: below everything
-  if (u == 0x80000000u) u = 0u;                     // -0 == +0
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
 // Exclusive prefix sum of one int per thread over the workgroup.
 __device__ int block_excl_scan(int v, int* wsum) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;

@@ -156,3 +156,69 @@ class AffixBatch:
 
     def direct_reuse(self, stream=None):
         return self.refresh(None, 0, stream)
+
+
+class Head:
+    """Final RMSNorm gain [d] and LM head [vocab, d] for the decode schedule."""
+
+    def __init__(self, norm_g: torch.Tensor, w: torch.Tensor):
+        self.norm_g = norm_g
+        self.w = w
+
+
+def block_row_index(batch: AffixBatch, k: int, block_begin: int, block_len: int) -> torch.Tensor:
+    """Rows of the refresh output (k anchors per request) that hold logical
+    positions [block_begin, block_begin + block_len) of every request.  A
+    request's rows are its anchors then its non-affix positions, each in
+    ascending order; the block lies in the masked span, after the affix."""
+    import numpy as np
+    S, ab, L, B = batch.S, batch.ab, batch.L, batch.B
+    assert block_begin >= ab + L, "the generation block follows the affix"
+    nonaffix = np.concatenate([np.arange(0, ab), np.arange(ab + L, S)])
+    R = batch.rows_per_request(k)
+    local = k + np.searchsorted(nonaffix, np.arange(block_begin, block_begin + block_len))
+    rows = (np.arange(B)[:, None] * R + local[None, :]).reshape(-1)
+    return torch.from_numpy(rows.astype(np.int32)).to(batch.device)
+
+
+class DecodePlan:
+    """Index arrays of the decode schedule, built on the host once: for each
+    block, the refresh-output rows holding it and the token-id positions its
+    commits go to."""
+
+    def __init__(self, batch: AffixBatch, k: int, block_len: int, n_blocks: int, full: bool):
+        import numpy as np
+        B, S, dev = batch.B, batch.S, batch.device
+        self.full, self.block_len, self.n_blocks = full, block_len, n_blocks
+        self.k = batch.L if full else k
+        self.anchors = (torch.arange(batch.L, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
+                        if full else None)
+        self.rows, self.pos = [], []
+        for blk in range(n_blocks):
+            p0 = batch.mb + blk * block_len
+            self.rows.append(block_row_index(batch, self.k, p0, block_len))
+            pos = (np.arange(B)[:, None] * S + np.arange(p0, p0 + block_len)[None, :]).reshape(-1)
+            self.pos.append(torch.from_numpy(pos.astype(np.int32)).to(dev))
+
+
+def decode_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, logits: torch.Tensor,
+                    committed: torch.Tensor, anchors: Optional[torch.Tensor] = None, stream=None):
+    """The serving schedule over the masked span (Sections 3.1 and 4.3): one
+    probe and top-K per request (selective mode), then per block a refresh
+    (selective, or full recomputation), the final norm and LM head on the
+    block's rows, and a greedy commit of every position of the block into the
+    token ids the next refresh embeds.  committed [n_blocks, B * block_len]
+    receives the chosen ids; logits [B * block_len, vocab] is scratch.
+    anchors: a given anchor set [B, k] instead of the probe's (selective)."""
+    if plan.full:
+        anchors = plan.anchors
+    elif anchors is None:
+        anchors, _ = batch.select_anchors(k, stream=stream)
+    for blk in range(plan.n_blocks):
+        x, _ = batch.refresh(anchors, plan.k, stream=stream)
+        h = A.acache_gather_rows(x, plan.rows[blk], stream=stream)
+        y = A.acache_rmsnorm(batch.model.dims, h, head.norm_g, stream=stream)
+        A.acache_linear(batch.model.dims, y, head.w, out=logits, ws=batch.ws, stream=stream)
+        A.acache_argmax_commit(logits, out=committed[blk], commit_pos=plan.pos[blk], ids=batch.remap,
+                               stream=stream)
+    return committed

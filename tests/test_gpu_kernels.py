@@ -244,3 +244,36 @@ def test_score(A, dtype, H, Hkv, dh, norm):
     A.acache_score(dims, up(q, dtype), up_i32(q_rows), cu_q, up(kp, dtype), up_i32(affix_slots), s2,
                    norm=A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL, row_lse=row_lse)
     assert torch.equal(s2, s1)
+
+
+# ----------------------------------------------------------------------------- greedy commit (Section 3.1)
+
+@pytest.mark.parametrize("dtype,rows,n,ld", [
+    ("bf16", 64, 126464, 126464),   # the serving workload's vocabulary
+    ("bf16", 33, 1001, 1008),       # ragged width (scalar tail), padded rows
+    ("bf16", 5, 7, 7),              # unaligned rows: scalar path only
+    ("f32", 17, 4099, 4100),
+])
+def test_argmax_commit(A, dtype, rows, n, ld):
+    torch = _torch()
+    rng = np.random.default_rng(rows + n)
+    vals = rng.integers(-20, 20, size=(rows, ld)).astype(np.float32) / 4  # many exact ties
+    vals[0, :] = -np.inf
+    vals[1, :5] = [np.nan, -0.0, 0.0, np.nan, -1.0]
+    if n > 8:
+        vals[1, 5:] = -2.0
+        vals[2, n // 2] = np.inf
+    vals[3, :] = np.nan
+    bits = W.bf16_bits_from_f32(vals) if dtype == "bf16" else vals
+    x = up(bits, dtype)
+    ref = O.greedy_commit(O.from_bits(bits, dtype)[:, :n])
+    ids = torch.full((3 * rows,), -7, dtype=torch.int32, device="cuda")
+    pos = np.arange(rows, dtype=np.int32) * 2
+    pos[1] = -1            # skipped
+    pos[2] = 3 * rows      # skipped
+    out = A.acache_argmax_commit(x[:, :n] if ld == n else x.narrow(1, 0, n), commit_pos=up_i32(pos), ids=ids)
+    np.testing.assert_array_equal(out.cpu().numpy(), ref)
+    want = np.full(3 * rows, -7)
+    ok = (pos >= 0) & (pos < 3 * rows)
+    want[pos[ok]] = ref[ok]
+    np.testing.assert_array_equal(ids.cpu().numpy(), want)

@@ -1,0 +1,83 @@
+"""The serving schedule (Sections 3.1 and 4.3) on a small stack: per block of
+the masked span a selective refresh, the final norm and LM head on the
+block's rows, and a greedy commit whose ids the next refresh embeds.
+
+Both sides start from the oracle's shared affix cache (rounded to storage)
+and the oracle's anchor sets, then each runs the whole schedule on its own
+(the oracle commits its own picks).  A pick is an argmax of logits that
+carry bf16 rounding, so it is compared where the oracle's top two logits are
+further apart than the tolerance; after the first near-tie of a request the
+two schedules may legitimately diverge and that request is no longer
+compared.
+"""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import acache_oracle as O
+from tests.gpu_util import TOL, up, up_i32
+from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
+
+pytestmark = pytest.mark.gpu
+
+
+def test_decode_schedule_against_oracle():
+    import torch
+    from paper_2608_26140_amd import driver as D
+    from paper_2608_26140_amd import workload as WL
+
+    w = W.get_config("mini-serve")
+    s = WL.build(w)
+    dt, lay = w.dims.dtype, w.layout
+    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    G, blk = lay.mask_len, w.decode_block
+    n_blocks = G // blk
+    layers = oracle_layers(w, s.host)
+    dims = oracle_dims(w)
+    sk64, sv64 = oracle_stale(w, s.host, layers)
+    sk, sv = [], []
+    for n in range(len(layers)):
+        kb = W.bf16_bits_from_f32(sk64[n].astype(np.float32))
+        vb = W.bf16_bits_from_f32(sv64[n].astype(np.float32))
+        s.batch.k_pools[n][:L] = up(kb.reshape(L, -1), dt)
+        s.batch.v_pools[n][:L] = up(vb.reshape(L, -1), dt)
+        sk.append(O.from_bits(kb, dt))
+        sv.append(O.from_bits(vb, dt))
+    anchors = [O.topk_anchors(O.probe(layers, dims, oracle_request(w, s.host, b), sk, sv).scores, K)
+               for b in range(B)]
+
+    g_bits, head_bits = W.draw_lm_head(w)
+    head = D.Head(up(g_bits, dt), up(head_bits, dt))
+    plan = D.DecodePlan(s.batch, K, blk, n_blocks, full=False)
+    logits = torch.empty((B * blk, w.dims.vocab), dtype=torch.bfloat16, device="cuda")
+    committed = torch.empty((n_blocks, B * blk), dtype=torch.int32, device="cuda")
+    D.decode_schedule(s.batch, head, plan, K, logits, committed, anchors=up_i32(np.stack(anchors)))
+    got = committed.cpu().numpy().reshape(n_blocks, B, blk)
+    # the committed ids also landed in the token ids the refreshes embed
+    ids_dev = s.batch.remap.cpu().numpy().reshape(B, lay.seq_len)
+    np.testing.assert_array_equal(ids_dev[:, lay.mask_begin:lay.mask_begin + G],
+                                  got.transpose(1, 0, 2).reshape(B, G))
+
+    g64, head64 = O.from_bits(g_bits, dt), O.from_bits(head_bits, dt)
+    emb = O.from_bits(s.host["embedding"], dt)
+    compared = 0
+    for b in range(B):
+        ids = s.host["ids"][b].copy()
+        base = oracle_request(w, s.host, b)
+        for k in range(n_blocks):
+            req = O.Request(x0=emb[ids], pos=base.pos, affix=base.affix, masked=base.masked)
+            ref = O.selective_refresh(layers, dims, req, anchors[b], sk, sv)
+            positions = np.arange(lay.mask_begin + k * blk, lay.mask_begin + (k + 1) * blk)
+            rows = np.searchsorted(ref.rows, positions)
+            lg = O.rms_norm(ref.x[rows], g64, dims.rms_eps) @ head64.T
+            pick = O.greedy_commit(lg)
+            top2 = np.sort(lg, axis=1)[:, -2:]
+            near = (top2[:, 1] - top2[:, 0]) <= TOL[dt] * np.abs(lg).max()
+            clear = ~near
+            np.testing.assert_array_equal(got[k, b][clear], pick[clear], err_msg=f"request {b} block {k}")
+            compared += int(clear.sum())
+            if near.any():
+                break  # from here the two schedules may commit different tokens
+            ids[positions] = pick
+    assert compared >= B * blk // 2, f"only {compared} picks compared"

@@ -301,3 +301,31 @@ def test_topk_signed_zero_nan_inf():
     assert list(O.topk_anchors(s, 4)) == [1, 2, 4, 5]
     assert list(O.topk_anchors(s, 5)) == [0, 1, 2, 4, 5]
     assert list(O.topk_anchors(s, 6)) == [0, 1, 2, 3, 4, 5]
+
+
+# ----------------------------------------------------------------------------- greedy commit (Section 3.1)
+
+def test_greedy_commit_special_rows():
+    nan, inf = np.nan, np.inf
+    rows = [
+        [1.0, 3.0, 3.0, 2.0],      # tie: lowest index
+        [-0.0, 0.0, -1.0, -2.0],   # -0 == +0: index 0
+        [nan, -inf, nan, -5.0],    # NaN below everything
+        [nan, nan, nan, nan],      # all NaN: lowest index
+        [-inf, -inf, -inf, -inf],
+        [inf, 1.0, inf, nan],
+    ]
+    np.testing.assert_array_equal(O.greedy_commit(np.array(rows)), [1, 0, 3, 0, 0, 0])
+
+
+def test_greedy_commit_brute_force_and_numpy():
+    rng = np.random.default_rng(7)
+    x = rng.integers(-3, 4, size=(50, 37)).astype(np.float64)  # many ties
+    got = O.greedy_commit(x)
+    for i, row in enumerate(x):
+        best = 0
+        for j in range(1, row.size):
+            if row[j] > row[best]:
+                best = j
+        assert got[i] == best
+    np.testing.assert_array_equal(got, np.argmax(x, axis=1))  # first maximum, as numpy defines it

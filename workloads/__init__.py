@@ -13,6 +13,7 @@ from .gen import (
     draw_embedding,
     draw_hidden_rows,
     draw_layer_weights,
+    draw_lm_head,
     draw_noise,
     draw_scores,
     draw_ints,
@@ -28,6 +29,7 @@ __all__ = [
     "SeqLayout",
     "Workload",
     "get_config",
+    "draw_lm_head",
     "LayerWeightsBits",
     "bf16_bits_from_f32",
     "draw_donor_rows",

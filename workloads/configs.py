@@ -81,6 +81,7 @@ class Workload:
     stale: str  # "perturb": stale KV from affix inputs + N(0, 0.1^2); "donor": from a donor request
     mask_rows: str = "random"  # "random": N(0,1) per masked row; "shared": one mask vector
     ratios: Tuple[float, ...] = field(default=())
+    decode_block: int = 0  # serving schedule: commit the masked span in blocks of this many tokens (0: none)
 
     @property
     def n_anchors(self) -> int:
@@ -128,12 +129,18 @@ CONFIGS: Dict[str, Workload] = {
         name="llada-serve-b32", seed_id=5,
         dims=ModelDims(n_layers=32, dtype="bf16", vocab=126464, **LLADA),
         layout=SeqLayout(seq_len=8704, affix_begin=0, affix_len=8192, mask_begin=8448, mask_len=256),
-        batch=32, ratio=0.2, stale="donor"),
+        batch=32, ratio=0.2, stale="donor", decode_block=32),
 }
 
 
 # Small stacks for parity tests at sizes the oracle finishes in seconds.
 TEST_CONFIGS: Dict[str, Workload] = {
+    "mini-serve": Workload(
+        name="mini-serve", seed_id=14,
+        dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, d_ff=1024, n_layers=3,
+                       dtype="bf16", vocab=1024),  # the LM head needs a multiple of 256 rows
+        layout=SeqLayout(seq_len=330, affix_begin=0, affix_len=250, mask_begin=298, mask_len=32),
+        batch=3, ratio=0.2, stale="donor", decode_block=8),
     "mini-stack": Workload(
         name="mini-stack", seed_id=11,
         dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=4, head_dim=128, d_ff=1024, n_layers=3,

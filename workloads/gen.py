@@ -148,6 +148,14 @@ def draw_embedding(w: Workload, std: float = 0.02) -> np.ndarray:
     return _store(_normal_f32((d.vocab, d.d_model), std, w.seed_id, 1, 0, 7), d.dtype)
 
 
+def draw_lm_head(w: Workload, std: float = 0.02):
+    """Final RMSNorm gain (ones) and LM head [vocab, d] N(0, std^2) of a stack
+    for the serving schedule; weights stream, layer index n_layers."""
+    d = w.dims
+    head = _store(_normal_f32((d.vocab, d.d_model), std, w.seed_id, 0, d.n_layers, 0), d.dtype)
+    return _store(np.ones(d.d_model, dtype=np.float32), d.dtype), head
+
+
 def draw_scores(n_req: int, L: int, seed: int, kind: str = "normal") -> np.ndarray:
     """float32 score arrays [n_req, L] for selection tests.
 
