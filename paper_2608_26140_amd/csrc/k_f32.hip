@@ -20,16 +20,29 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int m0 = blockIdx.y * TM, n0 = blockIdx.x * TN;
   float c[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += TK) {
+  // the next K tile is loaded into registers while the current one computes
+  float ra[4], rb[4];
+  auto load = [&](int k0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = threadIdx.x + i * 256;
       const int r = idx / TK, kk = idx % TK;
       const int m = m0 + r, n = n0 + r, k = k0 + kk;
-      sA[kk][r] = (m < M && k < K) ? X[(int64_t)m * K + k] : 0.f;
-      sB[kk][r] = (n < N && k < K) ? W[(int64_t)n * K + k] : 0.f;
+      ra[i] = (m < M && k < K) ? X[(int64_t)m * K + k] : 0.f;
+      rb[i] = (n < N && k < K) ? W[(int64_t)n * K + k] : 0.f;
+    }
+  };
+  load(0);
+  for (int k0 = 0; k0 < K; k0 += TK) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = threadIdx.x + i * 256;
+      const int r = idx / TK, kk = idx % TK;
+      sA[kk][r] = ra[i];
+      sB[kk][r] = rb[i];
     }
     __syncthreads();
+    if (k0 + TK < K) load(k0 + TK);
 #pragma unroll
     for (int kk = 0; kk < TK; ++kk) {
       float av[4], bv[4];

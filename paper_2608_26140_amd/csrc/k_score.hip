@@ -1,8 +1,9 @@
 // Probe scoring, column-sum pass (Section 3.2, Eq. 4-5), bf16 MFMA.
 //
-// One wavefront per (request, 64 affix keys, head).  It keeps its keys' K
-// fragments in registers and streams the request's masked queries in tiles of
-// 32: S = Q K^T with Q as the MFMA A operand puts one key column per lane
+// One workgroup per (request, 64 affix keys, head), kQSplit wavefronts that
+// take the request's masked queries in interleaved tiles of 32 and add their
+// column sums in a fixed order at the end.  Each wavefront keeps the keys' K
+// fragments in registers and streams its query tiles: S = Q K^T with Q as the MFMA A operand puts one key column per lane
 // (the 16 accumulator registers are 16 queries), so a key's attention mass
 // over the tile is an in-register sum; the two lane halves are combined once
 // at the end.  a = exp2(s * log2(e) / sqrt(d_h) - lse2) with the row's
@@ -17,6 +18,7 @@ namespace acache {
 namespace {
 
 constexpr int kDh = 128;
+constexpr int kQSplit = 4;  // wavefronts per workgroup, each a quarter of the query tiles
 
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -36,9 +38,11 @@ struct ColsumArgs {
   int cu_q[kMaxBatch + 1];
 };
 
-__global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
+__global__ __launch_bounds__(64 * kQSplit) void colsum_kernel(ColsumArgs a) {
   const int kt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int lane = threadIdx.x, hl = lane >> 5;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5;
+  constexpr int STEP = 32 * kQSplit;  // query stride between a wavefront's tiles
+  __shared__ float red[kQSplit][64];
   const int g = h / (a.H / a.Hkv);
   const float scale = kLog2e * rsqrtf((float)kDh);
 
@@ -81,11 +85,12 @@ __global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
     }
   };
   bf16x8 qcur[8], qnext[8];
-  int64_t row_next = row_of(32);
-  load_q(row_of(0), qcur);
-  for (int t = 0; t < nq; t += 32) {
-    if (t + 32 < nq) load_q(row_next, qnext);
-    if (t + 64 < nq) row_next = row_of(t + 64);
+  const int t0 = wave * 32;
+  int64_t row_next = row_of(t0 + STEP);
+  load_q(row_of(t0), qcur);
+  for (int t = t0; t < nq; t += STEP) {
+    if (t + STEP < nq) load_q(row_next, qnext);
+    if (t + 2 * STEP < nq) row_next = row_of(t + 2 * STEP);
     // log-sum-exp (base 2) of the 16 queries this lane's registers hold
     float lse2[16];
 #pragma unroll
@@ -113,11 +118,19 @@ __global__ __launch_bounds__(64) void colsum_kernel(ColsumArgs a) {
 #pragma unroll
     for (int s = 0; s < 8; ++s) qcur[s] = qnext[s];
   }
+  // key (lane & 31) + 32 sub: lane halves, then the wavefronts in order
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
     const float tot = col[sub] + __shfl_xor(col[sub], 32);
-    const int j = kt * 64 + sub * 32 + (lane & 31);
-    if (hl == 0 && j < a.L) a.part[((int64_t)b * a.H + h) * a.L + j] = tot;
+    if (hl == sub) red[wave][lane] = tot;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float tot = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < kQSplit; ++w) tot += red[w][lane];
+    const int j = kt * 64 + lane;
+    if (j < a.L) a.part[((int64_t)b * a.H + h) * a.L + j] = tot;
   }
 }
 
@@ -144,7 +157,7 @@ hipError_t launch_score_colsum_bf16(int batch, const int* cu_q, int H, int Hkv, 
   a.Hkv = Hkv;
   a.L = L;
   for (int b = 0; b <= batch; ++b) a.cu_q[b] = cu_q[b];
-  hipLaunchKernelGGL(colsum_kernel, dim3((L + 63) / 64, H, batch), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(colsum_kernel, dim3((L + 63) / 64, H, batch), dim3(64 * kQSplit), 0, s, a);
   return hipGetLastError();
 }
 
