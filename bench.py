@@ -153,6 +153,9 @@ def main():
     def full():
         batch.refresh(every, L)
 
+    def refresh_dropna():
+        batch.refresh(anchors_fixed, K, drop_non_anchor=True)
+
     def timed(fn, n):
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -200,11 +203,12 @@ def main():
 
     # phases, each timed on its own
     if args.only_step:
-        ms_select = ms_refresh = ms_full = None
+        ms_select = ms_refresh = ms_full = ms_drop = None
     else:
         ms_select = timed(select, args.steps)
         ms_refresh = timed(refresh, args.steps)
         ms_full = timed(full, args.steps)
+        ms_drop = timed(refresh_dropna, args.steps)
 
     peak, bound = PEAK[d.dtype]
     step_flops = sum(fl["probe"].values()) + sum(fl["refresh"].values())
@@ -255,7 +259,7 @@ def main():
         "latency_ms_per_request": round(ms_step / B, 4),
         "phases_ms": None if ms_refresh is None else {
             "select_anchors": round(ms_select, 4), "selective_refresh": round(ms_refresh, 4),
-            "full_refresh": round(ms_full, 4)},
+            "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4)},
         "refresh_speedup_vs_full": None if ms_refresh is None else round(ms_full / ms_refresh, 3),
         "speedup_target_S_over_R": round(S / R, 3),
         "step_tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 1),

@@ -326,6 +326,17 @@ def selective_refresh(layers, dims, req: Request, anchors, stale_k, stale_v) -> 
     return run_request(layers, dims, req, selective_rows(req, anchors), stale_k, stale_v)
 
 
+def drop_non_anchor_refresh(layers, dims, req: Request, anchors) -> Result:
+    """DropNA, the ablation of Section 5.4: the same anchors and request rows
+    are recomputed, but the non-anchor affix entries are discarded, so
+    attention sees only the recomputed rows (at their original positions).
+    That is a full recomputation of the request restricted to those rows."""
+    rows = selective_rows(req, anchors)
+    sub = Request(x0=req.x0[rows], pos=np.asarray(req.pos)[rows], affix=np.arange(0), masked=np.arange(0))
+    res = full_refresh(layers, dims, sub)
+    return Result(rows=rows, x=res.x, views_k=res.views_k, views_v=res.views_v, scores=None)
+
+
 def full_refresh(layers, dims, req: Request) -> Result:
     """Periodic full recomputation (Section 2.2): every position."""
     return run_request(layers, dims, req, np.arange(req.x0.shape[0]))

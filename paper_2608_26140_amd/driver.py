@@ -92,20 +92,25 @@ class AffixBatch:
         per = max(1, ((1 << 31) - 1) // max(1, R * widest))
         return [(b0, min(self.B, b0 + per)) for b0 in range(0, self.B, per)]
 
-    def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None, stream=None):
+    def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None,
+                   drop_non_anchor: bool = False, stream=None):
+        """drop_non_anchor: attention reads only the recomputed rows (DropNA,
+        Section 5.4): their write slots serve as the read slots, R keys per
+        request, and the non-anchor affix entries are never read."""
         R = self.rows_per_request(k)
         groups = self.request_groups(R)
+        read, nk = (m["write_slots"], R) if drop_non_anchor else (m["read_slots"], self.S)
         if score is not None and len(groups) > 1:
             raise ValueError("probe batch too large for one call")
         for n in range(self.model.n_layers):
             for b0, b1 in groups:
                 nb = b1 - b0
                 cu_rows = [b * R for b in range(nb + 1)]
-                cu_keys = [b * self.S for b in range(nb + 1)]
+                cu_keys = [b * nk for b in range(nb + 1)]
                 rows = slice(b0 * R, b1 * R)
                 A.acache_layer_recompute(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows],
                                          m["row_pos"][rows], m["write_slots"][rows],
-                                         m["read_slots"][b0 * self.S:b1 * self.S], self.k_pools[n],
+                                         read[b0 * nk:b1 * nk], self.k_pools[n],
                                          self.v_pools[n], self.ws, score=score, stream=stream)
         return x
 
@@ -142,12 +147,13 @@ class AffixBatch:
             return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
         return A.acache_topk(scores, k, stream=stream), scores
 
-    def refresh(self, anchors: Optional[torch.Tensor], k: int, stream=None):
+    def refresh(self, anchors: Optional[torch.Tensor], k: int, drop_non_anchor: bool = False, stream=None):
         """Selective recomputation (Section 3.3): anchors plus every
-        request-specific row through all layers.  Returns (x rows [B*R, d], maps)."""
+        request-specific row through all layers; with drop_non_anchor the
+        DropNA ablation (Section 5.4).  Returns (x rows [B*R, d], maps)."""
         m = self.maps(anchors, k, stream)
         x = self.gather_inputs(m, stream)
-        self.run_layers(x, m, k, stream=stream)
+        self.run_layers(x, m, k, drop_non_anchor=drop_non_anchor, stream=stream)
         return x, m
 
     def full_refresh(self, stream=None):

@@ -80,6 +80,10 @@ class OracleCache:
         return self._get(("sel", b), lambda: O.selective_refresh(self.layers, self.dims, self.req(b), self.anchors(b),
                                                                    self.sk, self.sv))
 
+    def drop(self, b):
+        return self._get(("drop", b), lambda: O.drop_non_anchor_refresh(self.layers, self.dims, self.req(b),
+                                                                          self.anchors(b)))
+
     def full(self, b):
         return self._get(("full", b), lambda: O.full_refresh(self.layers, self.dims, self.req(b)))
 
@@ -208,6 +212,42 @@ def test_ratio_zero_equals_direct_reuse(case):
     np.testing.assert_array_equal(g0, down_bits(x_probe))
     x1, _ = s.batch.direct_reuse()
     np.testing.assert_array_equal(g0, down_bits(x1))
+
+
+def test_dropna_against_oracle_and_never_reads_non_anchors(case):
+    """DropNA (Section 5.4): the same anchors, attention over the recomputed
+    rows only.  The shared affix region is poisoned with NaN: no non-anchor
+    entry may be read."""
+    w, s, layers, sk, sv, oc = case
+    dt = w.dims.dtype
+    L, R = w.layout.affix_len, w.rows_selective
+    anchors = np.stack([oc.anchors(b) for b in range(w.batch)])
+    saved = [(k[:L].clone(), v[:L].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
+    for k, v in zip(s.batch.k_pools, s.batch.v_pools):
+        k[:L] = float("nan")
+        v[:L] = float("nan")
+    try:
+        x, _ = s.batch.refresh(up_i32(anchors), w.n_anchors, drop_non_anchor=True)
+        gx = down(x)
+    finally:
+        for (k0, v0), k, v in zip(saved, s.batch.k_pools, s.batch.v_pools):
+            k[:L] = k0
+            v[:L] = v0
+    for b in range(w.batch):
+        assert_close(gx[b * R:(b + 1) * R], oc.drop(b).x, dt, f"DropNA rows request {b}")
+
+
+def test_keepna_equals_dropna_at_ratio_one(case):
+    """With every affix token an anchor there is no non-anchor entry left:
+    KeepNA and DropNA read the same keys in the same order."""
+    import torch
+    w, s, layers, sk, sv, oc = case
+    L = w.layout.affix_len
+    every = torch.arange(L, dtype=torch.int32, device="cuda").repeat(w.batch, 1).contiguous()
+    keep, _ = s.batch.refresh(every, L)
+    keep = down_bits(keep).copy()
+    drop, _ = s.batch.refresh(every, L, drop_non_anchor=True)
+    np.testing.assert_array_equal(down_bits(drop), keep)
 
 
 def test_anchor_stale_poison_and_determinism(case):

@@ -231,3 +231,37 @@ def test_maps_properties(layout, k):
                 assert rslots[b * S + p] == p - ab  # shared region
         np.testing.assert_array_equal(row_pos[q_rows[b * G:(b + 1) * G]], np.arange(mb, mb + G))
         assert np.all((q_rows[b * G:(b + 1) * G] >= b * R) & (q_rows[b * G:(b + 1) * G] < (b + 1) * R))
+
+
+# ----------------------------------------------------------------------------- DropNA (Section 5.4)
+
+def test_dropna_equals_keepna_and_full_at_ratio_one(setup2):
+    dims, layers, req, sk, sv = setup2
+    L = len(req.affix)
+    drop = O.drop_non_anchor_refresh(layers, dims, req, np.arange(L))
+    keep = O.selective_refresh(layers, dims, req, np.arange(L), sk, sv)
+    full = O.full_refresh(layers, dims, req)
+    np.testing.assert_array_equal(drop.rows, full.rows)
+    np.testing.assert_allclose(drop.x, keep.x, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(drop.x, full.x, rtol=1e-13, atol=1e-13)
+
+
+def test_dropna_one_layer_matches_torch_block_over_recomputed_rows():
+    """Attention sees exactly the recomputed rows' fresh K/V, nothing else."""
+    dims = tiny_dims(nkv=2)
+    layers = tiny_layers(dims, 1, seed=40)
+    req = tiny_request(dims, seed=41)
+    anchors = np.array([1, 4, 5, 9])
+    drop = O.drop_non_anchor_refresh(layers, dims, req, anchors)
+    rows = O.selective_rows(req, anchors)
+    ref = layer_torch(layers[0], dims, req.x0[rows], req.pos[rows], lambda k, v: (k, v))
+    np.testing.assert_allclose(drop.x, ref, rtol=1e-10, atol=1e-11)
+
+
+def test_dropna_differs_from_keepna_below_ratio_one(setup2):
+    dims, layers, req, sk, sv = setup2
+    anchors = np.arange(0, len(req.affix), 5)
+    drop = O.drop_non_anchor_refresh(layers, dims, req, anchors)
+    keep = O.selective_refresh(layers, dims, req, anchors, sk, sv)
+    np.testing.assert_array_equal(drop.rows, keep.rows)
+    assert np.max(np.abs(drop.x - keep.x)) > 1e-3
