@@ -202,13 +202,21 @@ def main():
     dom_ms_step = sum(durs) / args.steps
 
     # phases, each timed on its own
+    shift_dir = [1]
+
+    def shift():
+        # reuse of the shared cache one position away and back (re-rotation of its K, all layers)
+        batch.shift_affix(shift_dir[0])
+        shift_dir[0] = -shift_dir[0]
+
     if args.only_step:
-        ms_select = ms_refresh = ms_full = ms_drop = None
+        ms_select = ms_refresh = ms_full = ms_drop = ms_shift = None
     else:
         ms_select = timed(select, args.steps)
         ms_refresh = timed(refresh, args.steps)
         ms_full = timed(full, args.steps)
         ms_drop = timed(refresh_dropna, args.steps)
+        ms_shift = timed(shift, 2 * max(1, args.steps // 2))
 
     peak, bound = PEAK[d.dtype]
     step_flops = sum(fl["probe"].values()) + sum(fl["refresh"].values())
@@ -259,7 +267,10 @@ def main():
         "latency_ms_per_request": round(ms_step / B, 4),
         "phases_ms": None if ms_refresh is None else {
             "select_anchors": round(ms_select, 4), "selective_refresh": round(ms_refresh, 4),
-            "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4)},
+            "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4),
+            "shift_affix": round(ms_shift, 4)},
+        "shift_affix_GB_per_s": None if ms_shift is None else round(
+            2 * L * d.n_kv_heads * d.head_dim * (2 if d.dtype == "bf16" else 4) * d.n_layers / (ms_shift * 1e-3) / 1e9, 1),
         "refresh_speedup_vs_full": None if ms_refresh is None else round(ms_full / ms_refresh, 3),
         "speedup_target_S_over_R": round(S / R, 3),
         "step_tflops": round(step_flops / (ms_step * 1e-3) / 1e12, 1),

@@ -236,6 +236,22 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
                                      hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_rerotate_k — reuse of a cached span at shifted positions (the
+ * runtime piece Section 4 and the Limitations leave to future work: the
+ * cache is stored after rotation).  Rotations compose, so the K a row would
+ * have at position p + delta is its cached K (position p) turned by delta:
+ * for every row i < n, k_dst[dst_slots[i]] = rotate(k_src[src_slots[i]],
+ * delta[i]), each half-split pair (j, j + d_h/2) of every KV head by
+ * delta[i] * theta_j, theta_j = base^(-2j/d_h), the angle reduced in fp64.
+ * V is position-free and is not touched.  Pools [n_slots, pool_ld] of
+ * dims->dtype, one row = H_kv heads x head_dim; src and dst may be the same
+ * pool and the same slots (in place).  Rows whose slots fall outside
+ * [0, n_slots) are skipped.  n == 0: no-op. */
+acache_status acache_rerotate_k(const acache_dims* dims, const void* k_src, const int32_t* src_slots, void* k_dst,
+                                const int32_t* dst_slots, const int32_t* delta, int32_t n, int64_t pool_ld,
+                                int64_t n_slots, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * acache_argmax_commit — the commit half of the predict-then-commit loop
  * (Section 3.1; the online loop of Section 4.3), in its greedy form: for
  * every row i < rows, out[i] = the index of the largest of x[i, 0 .. n),

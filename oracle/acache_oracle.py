@@ -326,6 +326,14 @@ def selective_refresh(layers, dims, req: Request, anchors, stale_k, stale_v) -> 
     return run_request(layers, dims, req, selective_rows(req, anchors), stale_k, stale_v)
 
 
+def rerotate_keys(k: np.ndarray, delta: np.ndarray, base: float) -> np.ndarray:
+    """Cached K moved by delta positions (reuse of a span at other positions;
+    the cache holds K after rotation, Section 4): the half-split pairs of
+    every head turn by delta * theta_i, i.e. the rotation at position delta
+    applied to the cached K.  k [n, H_kv, d_h], delta [n]."""
+    return rope(k, np.asarray(delta), base)
+
+
 def drop_non_anchor_refresh(layers, dims, req: Request, anchors) -> Result:
     """DropNA, the ablation of Section 5.4: the same anchors and request rows
     are recomputed, but the non-anchor affix entries are discarded, so

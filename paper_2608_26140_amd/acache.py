@@ -65,6 +65,7 @@ def _load():
         "acache_gather_rows": [P, I64, I64, P, P, I64, I32, I32, P, I64, P],
         "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
         "acache_argmax_commit": [I32, P, I64, I32, I32, P, P, P, I64, P],
+        "acache_rerotate_k": [ctypes.POINTER(Dims), P, P, P, P, P, I32, I64, I64, P],
         "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
@@ -266,6 +267,17 @@ def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[to
                                               int(accumulate), _ptr(ws), 0 if ws is None else ws.numel(),
                                               _stream(stream)))
     return out
+
+
+def acache_rerotate_k(dims: Dims, k_src: torch.Tensor, src_slots: torch.Tensor, k_dst: torch.Tensor,
+                      dst_slots: torch.Tensor, delta: torch.Tensor, stream=None):
+    """k_dst[dst_slots[i]] = k_src[src_slots[i]] rotated by delta[i] positions."""
+    for t, n in ((src_slots, "src_slots"), (dst_slots, "dst_slots"), (delta, "delta")):
+        _dev_i32(t, n)
+    assert k_src.stride(0) == k_dst.stride(0) and k_src.shape[0] == k_dst.shape[0]
+    _check("acache_rerotate_k", lib.acache_rerotate_k(
+        ctypes.byref(dims), _ptr(k_src), _ptr(src_slots), _ptr(k_dst), _ptr(dst_slots), _ptr(delta),
+        src_slots.numel(), k_src.stride(0), k_src.shape[0], _stream(stream)))
 
 
 def acache_argmax_commit(x: torch.Tensor, out: Optional[torch.Tensor] = None,

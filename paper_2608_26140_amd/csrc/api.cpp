@@ -281,6 +281,20 @@ acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t sr
   return ACACHE_OK;
 }
 
+acache_status acache_rerotate_k(const acache_dims* dims, const void* k_src, const int32_t* src_slots, void* k_dst,
+                                const int32_t* dst_slots, const int32_t* delta, int32_t n, int64_t pool_ld,
+                                int64_t n_slots, hipStream_t stream) {
+  acache_status st = check_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(n >= 0 && n_slots >= 0, ACACHE_ERR_SHAPE);
+  if (n == 0) return ACACHE_OK;
+  CHECK(k_src && src_slots && k_dst && dst_slots && delta, ACACHE_ERR_NULL);
+  CHECK(pool_ld >= (int64_t)dims->n_kv_heads * dims->head_dim, ACACHE_ERR_SHAPE);
+  LAUNCH(launch_rerotate(dims->dtype, k_src, pool_ld, src_slots, k_dst, pool_ld, dst_slots, delta, n, n_slots,
+                         dims->n_kv_heads, dims->head_dim, dims->rope_base, stream));
+  return ACACHE_OK;
+}
+
 acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
                                    int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
                                    hipStream_t stream) {

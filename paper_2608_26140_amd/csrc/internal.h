@@ -70,6 +70,10 @@ size_t gemm_bf16_sk_ws_bytes();             // stream-K workspace (any shape)
 hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int rows, int n, int32_t* out,
                                const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s);
 
+hipError_t launch_rerotate(acache_dtype dt, const void* src, int64_t src_ld, const int32_t* src_slots, void* dst,
+                           int64_t dst_ld, const int32_t* dst_slots, const int32_t* delta, int n, int64_t n_slots,
+                           int heads, int dh, float rope_base, hipStream_t s);
+
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
 // part / part_bytes: optional fp32 space for key splits (null: one split)
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,

@@ -261,6 +261,36 @@ __global__ __launch_bounds__(256) void argmax_commit_kernel(const T* __restrict_
     }
   }
 }
+
+// ---------------------------------------------------------------- shifted reuse
+// Cached K is stored after rotation, so a span reused delta positions away
+// is re-rotated in place of recomputation: each half-split pair (i, i + d_h/2)
+// of every KV head turns by delta * theta_i (rotations compose).  One
+// workgroup per row; each thread owns pairs, reading both halves before
+// writing, so src and dst may be the same slot.
+template <typename T>
+__global__ __launch_bounds__(256) void rerotate_kernel(const T* __restrict__ src, int64_t src_ld,
+                                                       const int32_t* __restrict__ src_slots, T* __restrict__ dst,
+                                                       int64_t dst_ld, const int32_t* __restrict__ dst_slots,
+                                                       const int32_t* __restrict__ delta, int64_t n_slots,
+                                                       int heads, int dh, double log2_base) {
+  const int row = blockIdx.x;
+  const int64_t ss = src_slots[row], ds = dst_slots[row];
+  if (ss < 0 || ss >= n_slots || ds < 0 || ds >= n_slots) return;
+  const double dpos = (double)delta[row];
+  const int half = dh >> 1;
+  const T* sr = src + ss * src_ld;
+  T* dr = dst + ds * dst_ld;
+  for (int t = threadIdx.x; t < heads * half; t += blockDim.x) {
+    const int h = t / half, i = t - h * half;
+    const double inv_freq = exp2(-(2.0 * i / dh) * log2_base);
+    float sn, cs;
+    rotary_sincos(dpos * inv_freq, &sn, &cs);
+    const float x1 = to_f32(sr[h * dh + i]), x2 = to_f32(sr[h * dh + i + half]);
+    dr[h * dh + i] = from_f32<T>(x1 * cs - x2 * sn);
+    dr[h * dh + i + half] = from_f32<T>(x2 * cs + x1 * sn);
+  }
+}
 }  // namespace
 
 hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
@@ -320,6 +350,19 @@ hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int 
   else
     hipLaunchKernelGGL(argmax_commit_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x, ld, n, vec, out,
                        commit_pos, ids, ids_len);
+  return hipGetLastError();
+}
+
+hipError_t launch_rerotate(acache_dtype dt, const void* src, int64_t src_ld, const int32_t* src_slots, void* dst,
+                           int64_t dst_ld, const int32_t* dst_slots, const int32_t* delta, int n, int64_t n_slots,
+                           int heads, int dh, float rope_base, hipStream_t s) {
+  const double l2b = log2((double)rope_base);
+  if (dt == ACACHE_BF16)
+    hipLaunchKernelGGL(rerotate_kernel<bf16>, dim3(n), dim3(256), 0, s, (const bf16*)src, src_ld, src_slots,
+                       (bf16*)dst, dst_ld, dst_slots, delta, n_slots, heads, dh, l2b);
+  else
+    hipLaunchKernelGGL(rerotate_kernel<float>, dim3(n), dim3(256), 0, s, (const float*)src, src_ld, src_slots,
+                       (float*)dst, dst_ld, dst_slots, delta, n_slots, heads, dh, l2b);
   return hipGetLastError();
 }
 

@@ -128,6 +128,14 @@ class AffixBatch:
                                      stream=stream)
         return donor_x
 
+    def shift_affix(self, delta: int, stream=None):
+        """Reuse the shared affix cache delta positions from where it was
+        materialised: its K rows are re-rotated in place at every layer."""
+        slots = self.affix_slots
+        d = torch.full((self.L,), int(delta), dtype=torch.int32, device=self.device)
+        for k in self.k_pools:
+            A.acache_rerotate_k(self.model.dims, k, slots, k, slots, d, stream=stream)
+
     def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None):
         """One-shot probe (Section 3.2): forward the non-affix rows against the
         fixed shared affix cache and accumulate Eq. 5 over layers.  Returns

@@ -277,3 +277,26 @@ def test_argmax_commit(A, dtype, rows, n, ld):
     ok = (pos >= 0) & (pos < 3 * rows)
     want[pos[ok]] = ref[ok]
     np.testing.assert_array_equal(ids.cpu().numpy(), want)
+
+
+# ----------------------------------------------------------------------------- shifted reuse (Section 4)
+
+@pytest.mark.parametrize("dtype,hkv,dh,inplace", [("bf16", 4, 128, False), ("bf16", 1, 128, True),
+                                                    ("f32", 2, 64, False), ("f32", 4, 64, True)])
+def test_rerotate_k(A, dtype, hkv, dh, inplace):
+    torch = _torch()
+    n, n_slots = 300, 700
+    k = W.draw_tensor((n_slots, hkv * dh), dtype, std=1.0, seed=60 + hkv)
+    src = W.draw_permutation(n_slots, seed=61)[:n]
+    dst = src if inplace else W.draw_permutation(n_slots, seed=62)[:n]
+    delta = W.draw_ints((n,), -100000, 100000, seed=63)
+    delta[:3] = [0, 1, -1]
+    dims = A.make_dims(256, 4 * hkv, hkv, dh, 128, dtype)
+    kp = up(k, dtype)
+    out = kp if inplace else torch.zeros_like(kp)
+    A.acache_rerotate_k(dims, kp, up_i32(src), out, up_i32(dst), up_i32(delta))
+    ref = O.rerotate_keys(O.from_bits(k, dtype)[src].reshape(n, hkv, dh), delta, 10000.0)
+    assert_close(down(out)[dst].reshape(n, hkv, dh), ref, dtype, "re-rotated K")
+    if not inplace:  # untouched slots stay zero
+        rest = np.setdiff1d(np.arange(n_slots), dst)
+        assert not np.any(down(out)[rest])

@@ -265,3 +265,32 @@ def test_dropna_differs_from_keepna_below_ratio_one(setup2):
     keep = O.selective_refresh(layers, dims, req, anchors, sk, sv)
     np.testing.assert_array_equal(drop.rows, keep.rows)
     assert np.max(np.abs(drop.x - keep.x)) > 1e-3
+
+
+# ----------------------------------------------------------------------------- shifted reuse (Section 4)
+
+def test_rerotation_composes_with_rope():
+    dims = tiny_dims(nkv=2)
+    rng = np.random.default_rng(50)
+    k = rng.standard_normal((9, dims.n_kv_heads, dims.head_dim))
+    a = rng.integers(-500, 500, size=9)
+    b = rng.integers(-5000, 5000, size=9)
+    np.testing.assert_allclose(O.rerotate_keys(O.rope(k, a, dims.rope_base), b, dims.rope_base),
+                               O.rope(k, a + b, dims.rope_base), rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(O.rerotate_keys(k, np.zeros(9, dtype=int), dims.rope_base), k, rtol=0, atol=0)
+
+
+def test_shifted_donor_cache_is_the_rerotated_cache(setup2):
+    """A donor materialised delta positions later has, at every layer, the
+    same V and the K of the original donor turned by delta (attention sees
+    only relative positions)."""
+    dims, layers, req, sk, sv = setup2
+    delta = 137
+    donor = O.Request(x0=req.x0, pos=req.pos, affix=req.affix, masked=np.arange(0))
+    moved = O.Request(x0=req.x0, pos=req.pos + delta, affix=req.affix, masked=np.arange(0))
+    k0, v0 = O.materialize_affix_cache(layers, dims, donor)
+    k1, v1 = O.materialize_affix_cache(layers, dims, moved)
+    for n in range(len(layers)):
+        d = np.full(len(req.affix), delta)
+        np.testing.assert_allclose(k1[n], O.rerotate_keys(k0[n], d, dims.rope_base), rtol=1e-9, atol=1e-10)
+        np.testing.assert_allclose(v1[n], v0[n], rtol=1e-9, atol=1e-10)
