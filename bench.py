@@ -156,6 +156,9 @@ def main():
     def refresh_dropna():
         batch.refresh(anchors_fixed, K, drop_non_anchor=True)
 
+    def select_hkvd():
+        batch.select_anchors_hkvd(K)
+
     def timed(fn, n):
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -210,12 +213,13 @@ def main():
         shift_dir[0] = -shift_dir[0]
 
     if args.only_step:
-        ms_select = ms_refresh = ms_full = ms_drop = ms_shift = None
+        ms_select = ms_refresh = ms_full = ms_drop = ms_shift = ms_hkvd = None
     else:
         ms_select = timed(select, args.steps)
         ms_refresh = timed(refresh, args.steps)
         ms_full = timed(full, args.steps)
         ms_drop = timed(refresh_dropna, args.steps)
+        ms_hkvd = timed(select_hkvd, args.steps)
         ms_shift = timed(shift, 2 * max(1, args.steps // 2))
 
     peak, bound = PEAK[d.dtype]
@@ -268,7 +272,7 @@ def main():
         "phases_ms": None if ms_refresh is None else {
             "select_anchors": round(ms_select, 4), "selective_refresh": round(ms_refresh, 4),
             "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4),
-            "shift_affix": round(ms_shift, 4)},
+            "shift_affix": round(ms_shift, 4), "select_anchors_hkvd": round(ms_hkvd, 4)},
         "shift_affix_GB_per_s": None if ms_shift is None else round(
             2 * L * d.n_kv_heads * d.head_dim * (2 if d.dtype == "bf16" else 4) * d.n_layers / (ms_shift * 1e-3) / 1e9, 1),
         "refresh_speedup_vs_full": None if ms_refresh is None else round(ms_full / ms_refresh, 3),

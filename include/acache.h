@@ -236,6 +236,23 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
                                      hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_kv_deviation — the score of the CacheBlend-style selector the paper
+ * compares against (appendix, "CacheBlend-Style Anchor Selection"): each
+ * affix token's KV deviation between the shared affix-only cache and the
+ * request's full-prompt cache,
+ *   scores[b, j] = sum over the row's H_kv * d_h elements of
+ *                  (K[f] - K[s])^2 + (V[f] - V[s])^2,
+ * f = fresh_slots[b * fresh_ld + j] (the request's full-prompt K/V of affix
+ * token j at the selection layer), s = stale_slots[j] (the shared cache),
+ * accumulated in fp32 in a fixed order (scores are overwritten).  A row with
+ * a slot outside [0, n_slots) scores 0.  Pools [n_slots, pool_ld] of
+ * dims->dtype, 16-byte aligned.  The anchors are then acache_topk of the
+ * scores (Eq. 6's rule).  batch == 0 or affix_len == 0: no-op. */
+acache_status acache_kv_deviation(const acache_dims* dims, int32_t batch, int32_t affix_len, const void* k_pool,
+                                  const void* v_pool, int64_t pool_ld, int64_t n_slots, const int32_t* fresh_slots,
+                                  int64_t fresh_ld, const int32_t* stale_slots, float* scores, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * acache_rerotate_k — reuse of a cached span at shifted positions (the
  * runtime piece Section 4 and the Limitations leave to future work: the
  * cache is stored after rotation).  Rotations compose, so the K a row would

@@ -326,6 +326,25 @@ def selective_refresh(layers, dims, req: Request, anchors, stale_k, stale_v) -> 
     return run_request(layers, dims, req, selective_rows(req, anchors), stale_k, stale_v)
 
 
+def hkvd_layer(n_layers: int) -> int:
+    """Selection layer of the KV-deviation selector: the first layer whose
+    affix K/V depend on the rest of the prompt (layer 0's are row-local)."""
+    return min(1, n_layers - 1)
+
+
+def hkvd_scores(layers, dims, req: Request, stale_k, stale_v) -> np.ndarray:
+    """The CacheBlend-style selector the appendix compares against (HKVD): each affix token's
+    KV deviation between the shared (affix-only) cache and the full-prompt
+    cache, the squared difference of its K and V summed over all heads and
+    dimensions at the selection layer.  The full-prompt cache is a full
+    forward of the request through that layer.  Returns s [L]."""
+    n = hkvd_layer(len(layers))
+    full = full_refresh(layers[:n + 1], dims, req)
+    dk = full.views_k[n][req.affix] - stale_k[n]
+    dv = full.views_v[n][req.affix] - stale_v[n]
+    return (dk * dk).sum(axis=(1, 2)) + (dv * dv).sum(axis=(1, 2))
+
+
 def rerotate_keys(k: np.ndarray, delta: np.ndarray, base: float) -> np.ndarray:
     """Cached K moved by delta positions (reuse of a span at other positions;
     the cache holds K after rotation, Section 4): the half-split pairs of
@@ -335,7 +354,7 @@ def rerotate_keys(k: np.ndarray, delta: np.ndarray, base: float) -> np.ndarray:
 
 
 def drop_non_anchor_refresh(layers, dims, req: Request, anchors) -> Result:
-    """DropNA, the ablation of Section 5.4: the same anchors and request rows
+    """DropNA, the ablation of Section 5.3: the same anchors and request rows
     are recomputed, but the non-anchor affix entries are discarded, so
     attention sees only the recomputed rows (at their original positions).
     That is a full recomputation of the request restricted to those rows."""

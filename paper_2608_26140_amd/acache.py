@@ -66,6 +66,7 @@ def _load():
         "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
         "acache_argmax_commit": [I32, P, I64, I32, I32, P, P, P, I64, P],
         "acache_rerotate_k": [ctypes.POINTER(Dims), P, P, P, P, P, I32, I64, I64, P],
+        "acache_kv_deviation": [ctypes.POINTER(Dims), I32, I32, P, P, I64, I64, P, I64, P, P, P],
         "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
@@ -267,6 +268,20 @@ def acache_linear(dims: Dims, a: torch.Tensor, w: torch.Tensor, out: Optional[to
                                               int(accumulate), _ptr(ws), 0 if ws is None else ws.numel(),
                                               _stream(stream)))
     return out
+
+
+def acache_kv_deviation(dims: Dims, k_pool: torch.Tensor, v_pool: torch.Tensor, fresh_slots: torch.Tensor,
+                        stale_slots: torch.Tensor, scores: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """fresh_slots [B, L] (any row stride), stale_slots [L] -> scores [B, L]."""
+    B, L = fresh_slots.shape
+    assert fresh_slots.dtype == torch.int32 and fresh_slots.stride(1) == 1
+    _dev_i32(stale_slots, "stale_slots")
+    if scores is None:
+        scores = torch.empty((B, L), dtype=torch.float32, device=k_pool.device)
+    _check("acache_kv_deviation", lib.acache_kv_deviation(
+        ctypes.byref(dims), B, L, _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],
+        _ptr(fresh_slots), fresh_slots.stride(0), _ptr(stale_slots), _ptr(scores), _stream(stream)))
+    return scores
 
 
 def acache_rerotate_k(dims: Dims, k_src: torch.Tensor, src_slots: torch.Tensor, k_dst: torch.Tensor,

@@ -295,6 +295,23 @@ acache_status acache_rerotate_k(const acache_dims* dims, const void* k_src, cons
   return ACACHE_OK;
 }
 
+acache_status acache_kv_deviation(const acache_dims* dims, int32_t batch, int32_t affix_len, const void* k_pool,
+                                  const void* v_pool, int64_t pool_ld, int64_t n_slots, const int32_t* fresh_slots,
+                                  int64_t fresh_ld, const int32_t* stale_slots, float* scores, hipStream_t stream) {
+  acache_status st = check_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(batch >= 0 && batch <= 65535 && affix_len >= 0 && fresh_ld >= affix_len, ACACHE_ERR_SHAPE);
+  if (batch == 0 || affix_len == 0) return ACACHE_OK;
+  CHECK(k_pool && v_pool && fresh_slots && stale_slots && scores, ACACHE_ERR_NULL);
+  const int64_t width = (int64_t)dims->n_kv_heads * dims->head_dim;
+  const int64_t es = (int64_t)elem_size(dims->dtype);
+  CHECK(pool_ld >= width && (width * es) % 16 == 0, ACACHE_ERR_SHAPE);
+  CHECK(aligned16(k_pool) && aligned16(v_pool) && (pool_ld * es) % 16 == 0, ACACHE_ERR_ALIGN);
+  LAUNCH(launch_kv_deviation(dims->dtype, k_pool, v_pool, pool_ld, n_slots, fresh_slots, fresh_ld, stale_slots,
+                             batch, affix_len, (int)width, scores, stream));
+  return ACACHE_OK;
+}
+
 acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
                                    int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
                                    hipStream_t stream) {

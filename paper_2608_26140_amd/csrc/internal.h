@@ -74,6 +74,10 @@ hipError_t launch_rerotate(acache_dtype dt, const void* src, int64_t src_ld, con
                            int64_t dst_ld, const int32_t* dst_slots, const int32_t* delta, int n, int64_t n_slots,
                            int heads, int dh, float rope_base, hipStream_t s);
 
+hipError_t launch_kv_deviation(acache_dtype dt, const void* kp, const void* vp, int64_t pool_ld, int64_t n_slots,
+                              const int32_t* fresh, int64_t fresh_ld, const int32_t* stale, int batch, int L,
+                              int width, float* scores, hipStream_t s);
+
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
 // part / part_bytes: optional fp32 space for key splits (null: one split)
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,

@@ -291,6 +291,44 @@ __global__ __launch_bounds__(256) void rerotate_kernel(const T* __restrict__ src
     dr[h * dh + i + half] = from_f32<T>(x2 * cs + x1 * sn);
   }
 }
+
+// ---------------------------------------------------------------- KV deviation
+// The KV-deviation selector's score: for request b and affix token j,
+// sum over the row's K and V elements of (fresh - shared)^2, fp32, one
+// wavefront per (j, b), a fixed reduction order.
+template <typename T>
+__global__ __launch_bounds__(64) void kv_deviation_kernel(const T* __restrict__ kp, const T* __restrict__ vp,
+                                                          int64_t pool_ld, int64_t n_slots,
+                                                          const int32_t* __restrict__ fresh, int64_t fresh_ld,
+                                                          const int32_t* __restrict__ stale, int L, int width,
+                                                          float* __restrict__ scores) {
+  constexpr int PER = 16 / sizeof(T);
+  const int j = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+  const int64_t fs = fresh[(int64_t)b * fresh_ld + j], ss = stale[j];
+  const bool ok = fs >= 0 && fs < n_slots && ss >= 0 && ss < n_slots;
+  float acc = 0.f;
+  if (ok) {
+    const T* kf = kp + fs * pool_ld;
+    const T* ks = kp + ss * pool_ld;
+    const T* vf = vp + fs * pool_ld;
+    const T* vs = vp + ss * pool_ld;
+    for (int c = lane; c < width / PER; c += 64) {
+      T a[PER], e[PER], f[PER], g[PER];
+      __builtin_memcpy(a, kf + c * PER, 16);
+      __builtin_memcpy(e, ks + c * PER, 16);
+      __builtin_memcpy(f, vf + c * PER, 16);
+      __builtin_memcpy(g, vs + c * PER, 16);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const float dk = to_f32(a[i]) - to_f32(e[i]), dv = to_f32(f[i]) - to_f32(g[i]);
+        acc = fmaf(dk, dk, acc);
+        acc = fmaf(dv, dv, acc);
+      }
+    }
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) scores[(int64_t)b * L + j] = ok ? acc : 0.f;
+}
 }  // namespace
 
 hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
@@ -363,6 +401,18 @@ hipError_t launch_rerotate(acache_dtype dt, const void* src, int64_t src_ld, con
   else
     hipLaunchKernelGGL(rerotate_kernel<float>, dim3(n), dim3(256), 0, s, (const float*)src, src_ld, src_slots,
                        (float*)dst, dst_ld, dst_slots, delta, n_slots, heads, dh, l2b);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_deviation(acache_dtype dt, const void* kp, const void* vp, int64_t pool_ld, int64_t n_slots,
+                              const int32_t* fresh, int64_t fresh_ld, const int32_t* stale, int batch, int L,
+                              int width, float* scores, hipStream_t s) {
+  if (dt == ACACHE_BF16)
+    hipLaunchKernelGGL(kv_deviation_kernel<bf16>, dim3(L, batch), dim3(64), 0, s, (const bf16*)kp, (const bf16*)vp,
+                       pool_ld, n_slots, fresh, fresh_ld, stale, L, width, scores);
+  else
+    hipLaunchKernelGGL(kv_deviation_kernel<float>, dim3(L, batch), dim3(64), 0, s, (const float*)kp,
+                       (const float*)vp, pool_ld, n_slots, fresh, fresh_ld, stale, L, width, scores);
   return hipGetLastError();
 }
 

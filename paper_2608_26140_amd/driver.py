@@ -93,16 +93,16 @@ class AffixBatch:
         return [(b0, min(self.B, b0 + per)) for b0 in range(0, self.B, per)]
 
     def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None,
-                   drop_non_anchor: bool = False, stream=None):
+                   drop_non_anchor: bool = False, upto: Optional[int] = None, stream=None):
         """drop_non_anchor: attention reads only the recomputed rows (DropNA,
-        Section 5.4): their write slots serve as the read slots, R keys per
+        Section 5.3): their write slots serve as the read slots, R keys per
         request, and the non-anchor affix entries are never read."""
         R = self.rows_per_request(k)
         groups = self.request_groups(R)
         read, nk = (m["write_slots"], R) if drop_non_anchor else (m["read_slots"], self.S)
         if score is not None and len(groups) > 1:
             raise ValueError("probe batch too large for one call")
-        for n in range(self.model.n_layers):
+        for n in range(self.model.n_layers if upto is None else min(upto, self.model.n_layers)):
             for b0, b1 in groups:
                 nb = b1 - b0
                 cu_rows = [b * R for b in range(nb + 1)]
@@ -155,10 +155,28 @@ class AffixBatch:
             return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
         return A.acache_topk(scores, k, stream=stream), scores
 
+    def select_anchors_hkvd(self, k: int, stream=None):
+        """The CacheBlend-style selector (KV deviation) in place of Eq. 4-5:
+        a full-prompt forward of every request through the selection layer
+        (the first whose affix K/V depend on context), then each affix
+        token's squared K/V deviation from the shared cache, then Eq. 6's
+        top-K.  Returns (anchors [B, k], scores [B, L])."""
+        n = min(1, self.model.n_layers - 1)
+        every = torch.arange(self.L, dtype=torch.int32, device=self.device).repeat(self.B, 1).contiguous()
+        m = self.maps(every, self.L, stream)
+        x = self.gather_inputs(m, stream)
+        self.run_layers(x, m, self.L, upto=n + 1, stream=stream)
+        fresh = m["write_slots"].view(self.B, self.S)[:, self.ab:self.ab + self.L]
+        scores = A.acache_kv_deviation(self.model.dims, self.k_pools[n], self.v_pools[n], fresh, self.affix_slots,
+                                       stream=stream)
+        if k == 0:
+            return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
+        return A.acache_topk(scores, k, stream=stream), scores
+
     def refresh(self, anchors: Optional[torch.Tensor], k: int, drop_non_anchor: bool = False, stream=None):
         """Selective recomputation (Section 3.3): anchors plus every
         request-specific row through all layers; with drop_non_anchor the
-        DropNA ablation (Section 5.4).  Returns (x rows [B*R, d], maps)."""
+        DropNA ablation (Section 5.3).  Returns (x rows [B*R, d], maps)."""
         m = self.maps(anchors, k, stream)
         x = self.gather_inputs(m, stream)
         self.run_layers(x, m, k, drop_non_anchor=drop_non_anchor, stream=stream)

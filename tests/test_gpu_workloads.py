@@ -215,7 +215,7 @@ def test_ratio_zero_equals_direct_reuse(case):
 
 
 def test_dropna_against_oracle_and_never_reads_non_anchors(case):
-    """DropNA (Section 5.4): the same anchors, attention over the recomputed
+    """DropNA (Section 5.3): the same anchors, attention over the recomputed
     rows only.  The shared affix region is poisoned with NaN: no non-anchor
     entry may be read."""
     w, s, layers, sk, sv, oc = case
@@ -248,6 +248,23 @@ def test_keepna_equals_dropna_at_ratio_one(case):
     keep = down_bits(keep).copy()
     drop, _ = s.batch.refresh(every, L, drop_non_anchor=True)
     np.testing.assert_array_equal(down_bits(drop), keep)
+
+
+def test_hkvd_selector_against_oracle(case):
+    """The CacheBlend-style selector (KV deviation between the shared cache
+    and the full-prompt cache at the selection layer) and its top-K."""
+    w, s, layers, sk, sv, oc = case
+    dims = oracle_dims(w)
+    dt = w.dims.dtype
+    K = w.n_anchors
+    anchors, scores = s.batch.select_anchors_hkvd(K)
+    g_scores, g_anchors = down(scores), anchors.cpu().numpy()
+    for b in range(w.batch):
+        ref = O.hkvd_scores(layers, dims, oc.req(b), sk, sv)
+        assert_close(g_scores[b], ref, dt, f"KV deviation request {b}")
+        ov = anchors_agree(g_anchors[b], O.topk_anchors(ref, K), ref, K, TOL[dt])
+        assert_overlap(ov, ref, K, TOL[dt], f"HKVD request {b}")
+        np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], K))
 
 
 def test_anchor_stale_poison_and_determinism(case):

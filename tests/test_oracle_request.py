@@ -233,7 +233,7 @@ def test_maps_properties(layout, k):
         assert np.all((q_rows[b * G:(b + 1) * G] >= b * R) & (q_rows[b * G:(b + 1) * G] < (b + 1) * R))
 
 
-# ----------------------------------------------------------------------------- DropNA (Section 5.4)
+# ----------------------------------------------------------------------------- DropNA (Section 5.3)
 
 def test_dropna_equals_keepna_and_full_at_ratio_one(setup2):
     dims, layers, req, sk, sv = setup2
@@ -294,3 +294,36 @@ def test_shifted_donor_cache_is_the_rerotated_cache(setup2):
         d = np.full(len(req.affix), delta)
         np.testing.assert_allclose(k1[n], O.rerotate_keys(k0[n], d, dims.rope_base), rtol=1e-9, atol=1e-10)
         np.testing.assert_allclose(v1[n], v0[n], rtol=1e-9, atol=1e-10)
+
+
+# ----------------------------------------------------------------------------- HKVD selector (appendix, CacheBlend-style selection)
+
+def test_hkvd_scores_brute_force_and_zero_deviation(setup2):
+    dims, layers, req, sk, sv = setup2
+    s = O.hkvd_scores(layers, dims, req, sk, sv)
+    n = O.hkvd_layer(len(layers))
+    assert n == 1
+    full = O.full_refresh(layers, dims, req)
+    for j, row in enumerate(req.affix[:5]):
+        want = 0.0
+        for h in range(dims.n_kv_heads):
+            for e in range(dims.head_dim):
+                want += (full.views_k[n][row, h, e] - sk[n][j, h, e]) ** 2
+                want += (full.views_v[n][row, h, e] - sv[n][j, h, e]) ** 2
+        assert s[j] == pytest.approx(want, rel=1e-12)
+    # a shared cache equal to the full-prompt cache deviates nowhere
+    fk = [v[req.affix] for v in full.views_k]
+    fv = [v[req.affix] for v in full.views_v]
+    np.testing.assert_allclose(O.hkvd_scores(layers, dims, req, fk, fv), 0.0, atol=1e-20)
+
+
+def test_hkvd_one_layer_uses_layer_zero():
+    dims = tiny_dims(nkv=2)
+    layers = tiny_layers(dims, 1, seed=70)
+    req = tiny_request(dims, seed=71)
+    sk, sv = tiny_stale(layers, dims, req, seed=72)
+    assert O.hkvd_layer(1) == 0
+    s = O.hkvd_scores(layers, dims, req, sk, sv)
+    k0, v0 = O.layer_kv(layers[0], dims, req.x0[req.affix], req.pos[req.affix])
+    np.testing.assert_allclose(s, ((k0 - sk[0]) ** 2).sum(axis=(1, 2)) + ((v0 - sv[0]) ** 2).sum(axis=(1, 2)),
+                               rtol=1e-12)
