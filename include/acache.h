@@ -273,13 +273,31 @@ acache_status acache_rerotate_k(const acache_dims* dims, const void* k_src, cons
  * (Section 3.1; the online loop of Section 4.3), in its greedy form: for
  * every row i < rows, out[i] = the index of the largest of x[i, 0 .. n),
  * comparing values as numbers with -0 == +0 and NaN below everything, the
- * lowest index among equal values.  With commit_pos (nullable) the index is
- * also written to ids[commit_pos[i]]; positions outside [0, ids_len) are
- * skipped.  x [rows, ld] of `dtype` (logits).  rows == 0: no-op; n == 0
- * with rows > 0: ACACHE_ERR_SHAPE. */
+ * lowest index among equal values.  conf (nullable, fp32 [rows]) receives
+ * the row's confidence, the softmax probability of its largest value,
+ * 1 / sum_j exp(x_j - max) over the values that are not NaN or -inf (equal
+ * maxima, +inf included, share the mass equally; 0 for a row with none).  With commit_pos (nullable) the index is also written to
+ * ids[commit_pos[i]]; positions outside [0, ids_len) are skipped.
+ * x [rows, ld] of `dtype` (logits).  rows == 0: no-op; n == 0 with
+ * rows > 0: ACACHE_ERR_SHAPE. */
 acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
-                                   int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
-                                   hipStream_t stream);
+                                   int32_t* out, float* conf, const int32_t* commit_pos, int32_t* ids,
+                                   int64_t ids_len, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * acache_threshold_commit — one decode step's commit in the block-wise loop
+ * (Section 3.1; Section 4.3: during block decoding queries are formed for
+ * the current block only; Section 5 commits by a confidence threshold).  For
+ * each request b, over its rows r = b * block .. b * block + block - 1 (pick
+ * and conf from acache_argmax_commit of the block's logits): every row with
+ * committed[r] == 0 and conf[r] >= tau is committed; if none is, the single
+ * uncommitted row with the highest conf (the lowest r among equals; NaN
+ * lowest).  Committing sets committed[r] = 1 and ids[commit_pos[r]] =
+ * pick[r] (skipped outside [0, ids_len)).  count[b] = rows committed by this
+ * call (0 once the block is done).  batch == 0: no-op. */
+acache_status acache_threshold_commit(int32_t batch, int32_t block, const int32_t* pick, const float* conf, float tau,
+                                      int32_t* committed, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                      int32_t* count, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Building blocks of acache_layer_recompute, exported so each can be checked

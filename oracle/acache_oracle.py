@@ -248,6 +248,50 @@ def greedy_commit(logits: np.ndarray) -> np.ndarray:
     return out
 
 
+def confidence(logits: np.ndarray) -> np.ndarray:
+    """A row's confidence in the predict-then-commit loop (Section 3.1): the
+    softmax probability of its largest finite logit, 1 / sum_j exp(x_j - max)
+    over the finite values (0 for a row with none)."""
+    x = np.asarray(logits, dtype=np.float64)
+    out = np.zeros(x.shape[0])
+    for i, row in enumerate(x):
+        fin = row[np.isfinite(row) | (row == np.inf)]
+        fin = fin[fin > -np.inf]
+        if fin.size == 0:
+            continue
+        m = fin.max()
+        top = fin == m  # equal maxima, +inf included, count exactly once each
+        out[i] = 1.0 / np.sum(np.where(top, 1.0, np.exp(np.where(top, 0.0, fin - m))))
+    return out
+
+
+def threshold_commit(conf: np.ndarray, committed: np.ndarray, tau: float) -> np.ndarray:
+    """One decode step's commit over a block (Sections 3.1, 5): the
+    uncommitted rows with confidence >= tau, or, if there is none, the single
+    most confident uncommitted row (the lowest row among equals).  Returns the
+    boolean mask of rows committed by this step."""
+    conf = np.asarray(conf, dtype=np.float64)
+    free = ~np.asarray(committed, dtype=bool)
+    take = free & (conf >= tau)
+    if not take.any() and free.any():
+        key = np.where(free, np.where(np.isnan(conf), -0.5, conf), -np.inf)
+        take = np.zeros_like(free)
+        take[int(np.argmax(key))] = True
+    return take
+
+
+def decode_step(layers: Sequence["Layer"], dims: "Dims", views_k, views_v, x_block: np.ndarray,
+                block_pos: np.ndarray):
+    """A block decoding step (Section 4.3): queries only for the block's rows,
+    whose fresh K/V are written into the request's logical view before
+    attention reads the whole view through every layer.  views_k/views_v:
+    per layer [S, H_kv, d_h], updated in place.  Returns the block's outputs."""
+    x = np.asarray(x_block, dtype=np.float64).copy()
+    for n, w in enumerate(layers):
+        x, _, _ = layer_forward(w, dims, x, block_pos, block_pos, views_k[n], views_v[n])
+    return x
+
+
 # ----------------------------------------------------------------------------
 # requests: probe, selective refresh, full refresh, direct reuse
 # ----------------------------------------------------------------------------

@@ -64,7 +64,8 @@ def _load():
         "acache_topk": [P, I32, I32, I32, P, P],
         "acache_gather_rows": [P, I64, I64, P, P, I64, I32, I32, P, I64, P],
         "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
-        "acache_argmax_commit": [I32, P, I64, I32, I32, P, P, P, I64, P],
+        "acache_argmax_commit": [I32, P, I64, I32, I32, P, P, P, P, I64, P],
+        "acache_threshold_commit": [I32, I32, P, P, ctypes.c_float, P, P, P, I64, P, P],
         "acache_rerotate_k": [ctypes.POINTER(Dims), P, P, P, P, P, I32, I64, I64, P],
         "acache_kv_deviation": [ctypes.POINTER(Dims), I32, I32, P, P, I64, I64, P, I64, P, P, P],
         "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
@@ -297,20 +298,39 @@ def acache_rerotate_k(dims: Dims, k_src: torch.Tensor, src_slots: torch.Tensor, 
 
 def acache_argmax_commit(x: torch.Tensor, out: Optional[torch.Tensor] = None,
                          commit_pos: Optional[torch.Tensor] = None, ids: Optional[torch.Tensor] = None,
-                         stream=None) -> torch.Tensor:
+                         conf: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """Row argmax of x [rows, n] (lowest index on ties, NaN lowest); with
-    commit_pos, also ids[commit_pos[i]] = argmax of row i."""
+    commit_pos, also ids[commit_pos[i]] = argmax of row i; conf (fp32 [rows],
+    optional) receives each row's largest softmax probability."""
     rows, n = x.shape
     if out is None:
         out = torch.empty(rows, dtype=torch.int32, device=x.device)
     if commit_pos is not None:
         _dev_i32(commit_pos, "commit_pos")
         _dev_i32(ids, "ids")
+    if conf is not None and (conf.dtype != torch.float32 or not conf.is_contiguous() or conf.numel() < rows):
+        raise ValueError("conf must be a contiguous float32 tensor of at least `rows` values")
     dt = ACACHE_BF16 if x.dtype == torch.bfloat16 else ACACHE_F32
     _check("acache_argmax_commit", lib.acache_argmax_commit(
-        dt, _ptr(x), x.stride(0), rows, n, _ptr(out), _ptr(commit_pos), _ptr(ids),
+        dt, _ptr(x), x.stride(0), rows, n, _ptr(out), _ptr(conf), _ptr(commit_pos), _ptr(ids),
         0 if ids is None else ids.numel(), _stream(stream)))
     return out
+
+
+def acache_threshold_commit(block: int, pick: torch.Tensor, conf: torch.Tensor, tau: float, committed: torch.Tensor,
+                            commit_pos: torch.Tensor, ids: torch.Tensor, count: torch.Tensor, stream=None):
+    """One decode step's commit over B requests x `block` rows (see the header)."""
+    for t, n in ((pick, "pick"), (committed, "committed"), (commit_pos, "commit_pos"), (ids, "ids"),
+                 (count, "count")):
+        _dev_i32(t, n)
+    if conf.dtype != torch.float32 or not conf.is_contiguous() or conf.numel() != pick.numel():
+        raise ValueError("conf must be a contiguous float32 tensor shaped like pick")
+    if block <= 0 or pick.numel() % block or committed.numel() != pick.numel() or commit_pos.numel() != pick.numel():
+        raise ValueError("pick, committed and commit_pos hold batch * block values")
+    batch = pick.numel() // block
+    _check("acache_threshold_commit", lib.acache_threshold_commit(
+        batch, block, _ptr(pick), _ptr(conf), float(tau), _ptr(committed), _ptr(commit_pos), _ptr(ids),
+        ids.numel(), _ptr(count), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------- measurement hook

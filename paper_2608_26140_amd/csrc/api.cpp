@@ -313,14 +313,24 @@ acache_status acache_kv_deviation(const acache_dims* dims, int32_t batch, int32_
 }
 
 acache_status acache_argmax_commit(acache_dtype dtype, const void* x, int64_t ld, int32_t rows, int32_t n,
-                                   int32_t* out, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
-                                   hipStream_t stream) {
+                                   int32_t* out, float* conf, const int32_t* commit_pos, int32_t* ids,
+                                   int64_t ids_len, hipStream_t stream) {
   CHECK(dtype == ACACHE_BF16 || dtype == ACACHE_F32, ACACHE_ERR_UNSUPPORTED);
   CHECK(rows >= 0 && n >= 0 && ld >= n && ids_len >= 0, ACACHE_ERR_SHAPE);
   if (rows == 0) return ACACHE_OK;
   CHECK(n > 0, ACACHE_ERR_SHAPE);
   CHECK(x && out && (!commit_pos || ids), ACACHE_ERR_NULL);
-  LAUNCH_T(ACACHE_K_ARGMAX, stream, launch_argmax_commit(dtype, x, ld, rows, n, out, commit_pos, ids, ids_len, stream));
+  LAUNCH_T(ACACHE_K_ARGMAX, stream, launch_argmax_commit(dtype, x, ld, rows, n, out, conf, commit_pos, ids, ids_len, stream));
+  return ACACHE_OK;
+}
+
+acache_status acache_threshold_commit(int32_t batch, int32_t block, const int32_t* pick, const float* conf, float tau,
+                                      int32_t* committed, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                      int32_t* count, hipStream_t stream) {
+  CHECK(batch >= 0 && block >= 0 && ids_len >= 0, ACACHE_ERR_SHAPE);
+  if (batch == 0) return ACACHE_OK;
+  CHECK(pick && conf && committed && commit_pos && ids && count, ACACHE_ERR_NULL);
+  LAUNCH(launch_threshold_commit(batch, block, pick, conf, tau, committed, commit_pos, ids, ids_len, count, stream));
   return ACACHE_OK;
 }
 

@@ -68,7 +68,10 @@ int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL
 size_t gemm_bf16_sk_ws_bytes();             // stream-K workspace (any shape)
 
 hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int rows, int n, int32_t* out,
-                               const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s);
+                               float* conf, const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s);
+hipError_t launch_threshold_commit(int batch, int block, const int32_t* pick, const float* conf, float tau,
+                                  int32_t* committed, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                  int32_t* count, hipStream_t s);
 
 hipError_t launch_rerotate(acache_dtype dt, const void* src, int64_t src_ld, const int32_t* src_slots, void* dst,
                            int64_t dst_ld, const int32_t* dst_slots, const int32_t* delta, int n, int64_t n_slots,

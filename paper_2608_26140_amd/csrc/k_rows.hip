@@ -214,9 +214,36 @@ __device__ __forceinline__ void argmax_take(uint32_t key, int idx, uint32_t& bk,
 __device__ __forceinline__ uint32_t elem_bits(bf16 v) { return (uint32_t)__builtin_bit_cast(uint16_t, v) << 16; }
 __device__ __forceinline__ uint32_t elem_bits(float v) { return __builtin_bit_cast(uint32_t, v); }
 
+// Online softmax sum: (m, s) with s = sum exp(x - m) over the finite values
+// seen (NaN and -inf add nothing); combining rescales the smaller maximum.
+__device__ __forceinline__ void softmax_add(float x, float& m, float& s) {
+  if (!(x > -INFINITY)) return;  // NaN or -inf
+  if (x > m) {
+    s = s * __expf(m - x) + 1.f;
+    m = x;
+  } else if (x == m) {
+    s += 1.f;  // exact, also for an infinite maximum
+  } else {
+    s += __expf(x - m);
+  }
+}
+__device__ __forceinline__ void softmax_merge(float m2, float s2, float& m, float& s) {
+  if (s2 == 0.f) return;
+  if (s != 0.f && m2 == m) {
+    s += s2;
+    return;
+  }
+  if (s == 0.f || m2 > m) {
+    s = s2 + (s == 0.f ? 0.f : s * __expf(m - m2));
+    m = m2;
+  } else {
+    s += s2 * __expf(m2 - m);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void argmax_commit_kernel(const T* __restrict__ x, int64_t ld, int n, int vec,
-                                                            int32_t* __restrict__ out,
+                                                            int32_t* __restrict__ out, float* __restrict__ conf,
                                                             const int32_t* __restrict__ commit_pos,
                                                             int32_t* __restrict__ ids, int64_t ids_len) {
   constexpr int PER = 16 / sizeof(T);
@@ -224,6 +251,7 @@ __global__ __launch_bounds__(256) void argmax_commit_kernel(const T* __restrict_
   const T* xr = x + row * ld;
   uint32_t bk = 0u;
   int bi = 0x7FFFFFFF;
+  float sm = -INFINITY, ss = 0.f;
   int start = 0;
   if (vec) {
     const int chunks = n / PER;
@@ -232,29 +260,45 @@ __global__ __launch_bounds__(256) void argmax_commit_kernel(const T* __restrict_
       T v[PER];
       __builtin_memcpy(v, &raw, 16);
 #pragma unroll
-      for (int j = 0; j < PER; ++j) argmax_take(order_key(elem_bits(v[j])), c * PER + j, bk, bi);
+      for (int j = 0; j < PER; ++j) {
+        argmax_take(order_key(elem_bits(v[j])), c * PER + j, bk, bi);
+        if (conf) softmax_add(to_f32(v[j]), sm, ss);
+      }
     }
     start = chunks * PER;
   }
-  for (int i = start + threadIdx.x; i < n; i += 256) argmax_take(order_key(elem_bits(xr[i])), i, bk, bi);
+  for (int i = start + threadIdx.x; i < n; i += 256) {
+    argmax_take(order_key(elem_bits(xr[i])), i, bk, bi);
+    if (conf) softmax_add(to_f32(xr[i]), sm, ss);
+  }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const uint32_t ok = __shfl_xor(bk, o);
     const int oi = __shfl_xor(bi, o);
     argmax_take(ok, oi, bk, bi);
+    const float om = __shfl_xor(sm, o), os = __shfl_xor(ss, o);
+    softmax_merge(om, os, sm, ss);
   }
   __shared__ uint32_t sk[4];
   __shared__ int si[4];
+  __shared__ float smm[4], sss[4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   if (lane == 0) {
     sk[wave] = bk;
     si[wave] = bi;
+    smm[wave] = sm;
+    sss[wave] = ss;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
 #pragma unroll
-    for (int w = 1; w < 4; ++w) argmax_take(sk[w], si[w], bk, bi);
+    for (int w = 1; w < 4; ++w) {
+      argmax_take(sk[w], si[w], bk, bi);
+      softmax_merge(smm[w], sss[w], sm, ss);
+    }
     out[row] = bi;
+    // probability of the largest finite logit (the argmax unless the row has +inf or only NaN)
+    if (conf) conf[row] = ss > 0.f ? 1.f / ss : 0.f;
     if (commit_pos) {
       const int64_t p = commit_pos[row];
       if (p >= 0 && p < ids_len) ids[p] = bi;
@@ -329,6 +373,70 @@ __global__ __launch_bounds__(64) void kv_deviation_kernel(const T* __restrict__ 
   acc = wave_sum(acc);
   if (lane == 0) scores[(int64_t)b * L + j] = ok ? acc : 0.f;
 }
+
+// ---------------------------------------------------------------- threshold commit
+// One wavefront per request, over its block of `block` rows: every
+// uncommitted row whose confidence reaches tau is committed; if none does,
+// the single most confident uncommitted row (lowest row on equal
+// confidence).  Committing writes the row's pick to ids[commit_pos[row]]
+// and sets its flag; count[b] receives the number committed in this call.
+__global__ __launch_bounds__(64) void threshold_commit_kernel(int block, const int32_t* __restrict__ pick,
+                                                              const float* __restrict__ conf, float tau,
+                                                              int32_t* __restrict__ committed,
+                                                              const int32_t* __restrict__ commit_pos,
+                                                              int32_t* __restrict__ ids, int64_t ids_len,
+                                                              int32_t* __restrict__ count) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  int n_new = 0;
+  // pass 1: threshold
+  for (int r0 = 0; r0 < block; r0 += 64) {
+    const int r = r0 + lane;
+    const int64_t row = (int64_t)b * block + r;
+    bool take = false;
+    if (r < block && !committed[row]) take = conf[row] >= tau;
+    if (take) {
+      const int64_t p = commit_pos[row];
+      if (p >= 0 && p < ids_len) ids[p] = pick[row];
+      committed[row] = 1;
+    }
+    n_new += __popcll(__builtin_amdgcn_ballot_w64(take));
+  }
+  if (n_new == 0) {
+    // pass 2: the most confident uncommitted row
+    float best = -1.f;
+    int best_r = 0x7FFFFFFF;
+    for (int r0 = 0; r0 < block; r0 += 64) {
+      const int r = r0 + lane;
+      if (r < block && !committed[(int64_t)b * block + r]) {
+        const float c = conf[(int64_t)b * block + r];
+        const float ck = c == c ? c : -0.5f;  // NaN ranks below every confidence
+        if (ck > best || (ck == best && r < best_r)) {
+          best = ck;
+          best_r = r;
+        }
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ob = __shfl_xor(best, o);
+      const int orr = __shfl_xor(best_r, o);
+      if (ob > best || (ob == best && orr < best_r)) {
+        best = ob;
+        best_r = orr;
+      }
+    }
+    if (best_r < block) {
+      if (lane == 0) {
+        const int64_t row = (int64_t)b * block + best_r;
+        const int64_t p = commit_pos[row];
+        if (p >= 0 && p < ids_len) ids[p] = pick[row];
+        committed[row] = 1;
+      }
+      n_new = 1;
+    }
+  }
+  if (lane == 0) count[b] = n_new;
+}
 }  // namespace
 
 hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows, const int32_t* idx,
@@ -379,15 +487,15 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
 }
 
 hipError_t launch_argmax_commit(acache_dtype dt, const void* x, int64_t ld, int rows, int n, int32_t* out,
-                               const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s) {
+                               float* conf, const int32_t* commit_pos, int32_t* ids, int64_t ids_len, hipStream_t s) {
   const int es = dt == ACACHE_BF16 ? 2 : 4;
   const int vec = ((uintptr_t)x % 16 == 0 && (ld * es) % 16 == 0) ? 1 : 0;
   if (dt == ACACHE_BF16)
     hipLaunchKernelGGL(argmax_commit_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x, ld, n, vec, out,
-                       commit_pos, ids, ids_len);
+                       conf, commit_pos, ids, ids_len);
   else
     hipLaunchKernelGGL(argmax_commit_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x, ld, n, vec, out,
-                       commit_pos, ids, ids_len);
+                       conf, commit_pos, ids, ids_len);
   return hipGetLastError();
 }
 
@@ -413,6 +521,14 @@ hipError_t launch_kv_deviation(acache_dtype dt, const void* kp, const void* vp, 
   else
     hipLaunchKernelGGL(kv_deviation_kernel<float>, dim3(L, batch), dim3(64), 0, s, (const float*)kp,
                        (const float*)vp, pool_ld, n_slots, fresh, fresh_ld, stale, L, width, scores);
+  return hipGetLastError();
+}
+
+hipError_t launch_threshold_commit(int batch, int block, const int32_t* pick, const float* conf, float tau,
+                                  int32_t* committed, const int32_t* commit_pos, int32_t* ids, int64_t ids_len,
+                                  int32_t* count, hipStream_t s) {
+  hipLaunchKernelGGL(threshold_commit_kernel, dim3(batch), dim3(64), 0, s, block, pick, conf, tau, committed,
+                     commit_pos, ids, ids_len, count);
   return hipGetLastError();
 }
 

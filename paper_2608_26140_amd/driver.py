@@ -14,6 +14,7 @@ on one stream, without synchronising.
 
 from __future__ import annotations
 
+import contextlib
 from typing import List, Optional
 
 import torch
@@ -225,12 +226,19 @@ class DecodePlan:
         self.k = batch.L if full else k
         self.anchors = (torch.arange(batch.L, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
                         if full else None)
-        self.rows, self.pos = [], []
+        self.rows, self.pos, self.row_pos, self.write_slots = [], [], [], []
+        nonaffix = np.concatenate([np.arange(0, batch.ab), np.arange(batch.ab + batch.L, S)])
+        i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
         for blk in range(n_blocks):
             p0 = batch.mb + blk * block_len
             self.rows.append(block_row_index(batch, self.k, p0, block_len))
-            pos = (np.arange(B)[:, None] * S + np.arange(p0, p0 + block_len)[None, :]).reshape(-1)
-            self.pos.append(torch.from_numpy(pos.astype(np.int32)).to(dev))
+            p = np.arange(p0, p0 + block_len)
+            self.pos.append(i32((np.arange(B)[:, None] * S + p[None, :]).reshape(-1)))
+            self.row_pos.append(i32(np.tile(p, B)))
+            # a request's refresh row i writes private slot L + b * stride + i
+            # (Section 4.1); the block's rows keep those slots while it decodes
+            local = self.k + np.searchsorted(nonaffix, p)
+            self.write_slots.append(i32((batch.L + np.arange(B)[:, None] * batch.stride + local[None, :]).reshape(-1)))
 
 
 def decode_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, logits: torch.Tensor,
@@ -254,3 +262,92 @@ def decode_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, log
         A.acache_argmax_commit(logits, out=committed[blk], commit_pos=plan.pos[blk], ids=batch.remap,
                                stream=stream)
     return committed
+
+
+def _on(stream):
+    """torch's own copies and fills go to the stream the library calls use."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+
+
+def decode_step(batch: AffixBatch, plan: DecodePlan, blk: int, read_slots: torch.Tensor, stream=None):
+    """One decoding step of block ``blk`` (Section 4.3, Appendix C.1): the
+    block's rows, embedded from the current token ids, go through every
+    layer with queries for those rows only; each layer writes their fresh
+    K/V to the rows' private slots, then attention reads each request's
+    whole logical context through ``read_slots`` (the refresh's read-slot
+    map).  Returns the block's last-layer rows [B * block_len, d]."""
+    B, blen = batch.B, plan.block_len
+    cu_rows = [b * blen for b in range(B + 1)]
+    cu_keys = [b * batch.S for b in range(B + 1)]
+    h = A.acache_gather_rows(batch.x_src, plan.pos[blk], batch.remap, stream=stream)
+    for i in range(batch.model.n_layers):
+        A.acache_layer_recompute(batch.model.dims, batch.model.lw[i], cu_rows, cu_keys, h, plan.row_pos[blk],
+                                 plan.write_slots[blk], read_slots, batch.k_pools[i], batch.v_pools[i],
+                                 batch.ws, stream=stream)
+    return h
+
+
+def decode_threshold_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, tau: float,
+                              anchors: Optional[torch.Tensor] = None, trace: Optional[list] = None,
+                              max_steps: Optional[int] = None, stream=None):
+    """Block-wise decoding with confidence-threshold commits (Sections 3.1,
+    4.3, 5).  Per block: a refresh (selective, or full recomputation) whose
+    block rows give the first predictions; then, until every position of the
+    block is committed, decode steps that form queries for the block's rows
+    only, write their fresh K/V to the rows' private slots and attend over the
+    refresh's read-slot view, each followed by the final norm, the LM head
+    and a commit of every uncommitted position with confidence >= tau (or
+    the single most confident one).  Commits land in the token ids
+    (``batch.remap``) that the next step and the next refresh embed; that is
+    where the caller reads the generated tokens.
+
+    The batch steps together: a request whose block is done commits nothing
+    until the rest are.  The host reads the per-request commit counts after
+    each step (one synchronisation) to know when the block is done.
+    trace: if a list, receives per step a dict of host copies (block,
+    logits, pick, conf, committed flags).  Returns the number of steps
+    (commits) each block took; every step commits at least one position of
+    each request whose block is not done, so a block takes at most
+    block_len steps.  max_steps ends a block early (for measurement): its
+    positions not yet committed keep the mask id."""
+    if batch.remap is None:
+        raise ValueError("decode steps embed token ids: the batch needs remap")
+    B, blen, dev = batch.B, plan.block_len, batch.device
+    dims = batch.model.dims
+    if plan.full:
+        anchors = plan.anchors
+    elif anchors is None:
+        anchors, _ = batch.select_anchors(k, stream=stream)
+    n = B * blen
+    logits = torch.empty((n, head.w.shape[0]), dtype=batch.model.dtype, device=dev)
+    pick = torch.empty(n, dtype=torch.int32, device=dev)
+    conf = torch.empty(n, dtype=torch.float32, device=dev)
+    flags = torch.empty(n, dtype=torch.int32, device=dev)
+    count = torch.empty(B, dtype=torch.int32, device=dev)
+    count_host = torch.empty(B, dtype=torch.int32, pin_memory=True)
+    steps = []
+    for blk in range(plan.n_blocks):
+        x, m = batch.refresh(anchors, plan.k, stream=stream)
+        h = A.acache_gather_rows(x, plan.rows[blk], stream=stream)
+        with _on(stream):
+            flags.zero_()
+        done, step = 0, 0
+        while True:
+            y = A.acache_rmsnorm(dims, h, head.norm_g, stream=stream)
+            A.acache_linear(dims, y, head.w, out=logits, ws=batch.ws, stream=stream)
+            A.acache_argmax_commit(logits, out=pick, conf=conf, stream=stream)
+            A.acache_threshold_commit(blen, pick, conf, tau, flags, plan.pos[blk], batch.remap, count,
+                                      stream=stream)
+            with _on(stream):
+                count_host.copy_(count, non_blocking=True)
+            (stream if stream is not None else torch.cuda.current_stream()).synchronize()
+            if trace is not None:
+                trace.append(dict(block=blk, logits=logits.float().cpu().numpy(), pick=pick.cpu().numpy(),
+                                  conf=conf.cpu().numpy(), committed=flags.cpu().numpy()))
+            done += int(count_host.sum())
+            step += 1
+            if done >= n or (max_steps is not None and step >= max_steps):
+                break
+            h = decode_step(batch, plan, blk, m["read_slots"], stream=stream)
+        steps.append(step)
+    return steps

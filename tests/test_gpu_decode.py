@@ -1,0 +1,262 @@
+"""Block decoding over the read-slot view (Section 4.3, Appendix C.1) and the
+confidence-threshold commit (Sections 3.1, 5).
+
+* The commit kernel against the oracle's rule on seeded confidences (ties,
+  NaN, committed rows, blocks over one wavefront).
+* Decode steps against the oracle: after a selective refresh (oracle anchors,
+  oracle stale cache rounded to storage, both sides), the block's token ids
+  are set to a seeded mix of committed tokens and the mask id, identical on
+  both sides, and one decode step runs on each; then a second pattern and a
+  second step over the views the first one left.  Compared: the block's
+  output rows, the fresh K/V in the rows' private slots, the untouched rest
+  of the pools, the LM-head logits and confidences.
+* The schedule: every step's commits obey the rule for the confidences the
+  step computed, the committed ids are the step's picks, a block ends within
+  block_len steps, tau = 0 reproduces the one-step greedy schedule and
+  tau > 1 commits one position per request per step.
+
+The schedule is not followed against the oracle's own trajectory: in a
+random-init model the masked rows of a block carry nearly equal confidences,
+so a fallback commit (the most confident row) is decided by gaps below the
+logits' bf16 rounding, and either choice is then correct.
+"""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import acache_oracle as O
+from tests.gpu_util import TOL, assert_close, down, down_bits, up, up_i32
+from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
+
+pytestmark = pytest.mark.gpu
+
+
+# ----------------------------------------------------------------------------- the commit kernel
+
+@pytest.mark.parametrize("batch,block,tau", [(3, 8, 0.5), (2, 64, 0.7), (4, 100, 0.3), (1, 1, 0.9),
+                                             (5, 32, 2.0), (2, 7, -1.0)])
+def test_threshold_commit_kernel(batch, block, tau):
+    import torch
+    from paper_2608_26140_amd import acache as A
+    n = batch * block
+    rng = np.random.default_rng(block * 7 + batch)
+    conf = rng.integers(0, 8, size=n).astype(np.float32) / 8     # many ties, values at tau
+    conf[rng.random(n) < 0.1] = np.nan
+    flags = (rng.random(n) < 0.3).astype(np.int32)
+    if batch > 1:
+        flags[block:2 * block] = 1                                 # a request already done
+    pick = rng.integers(0, 1000, size=n).astype(np.int32)
+    ids_len = 3 * n
+    pos = rng.permutation(ids_len)[:n].astype(np.int32)
+    pos[0] = -1                                                    # skipped
+    ids = torch.full((ids_len,), -3, dtype=torch.int32, device="cuda")
+    fl = up_i32(flags)
+    count = torch.full((batch,), -9, dtype=torch.int32, device="cuda")
+    A.acache_threshold_commit(block, up_i32(pick), torch.from_numpy(conf).cuda(), tau, fl, up_i32(pos), ids, count)
+    want_ids = np.full(ids_len, -3)
+    want_flags = flags.copy()
+    want_count = np.zeros(batch, dtype=np.int64)
+    t32 = float(np.float32(tau))
+    for b in range(batch):
+        sl = slice(b * block, (b + 1) * block)
+        take = O.threshold_commit(conf[sl].astype(np.float64), flags[sl].astype(bool), t32)
+        want_flags[sl][take] = 1
+        want_count[b] = take.sum()
+        for r in np.flatnonzero(take):
+            p = pos[b * block + r]
+            if 0 <= p < ids_len:
+                want_ids[p] = pick[b * block + r]
+    np.testing.assert_array_equal(fl.cpu().numpy(), want_flags)
+    np.testing.assert_array_equal(count.cpu().numpy(), want_count)
+    np.testing.assert_array_equal(ids.cpu().numpy(), want_ids)
+
+
+def test_argmax_confidence():
+    import torch
+    from paper_2608_26140_amd import acache as A
+    rng = np.random.default_rng(3)
+    for dtype, rows, n in (("bf16", 40, 1024), ("bf16", 6, 300), ("f32", 9, 5000)):
+        vals = (rng.standard_normal((rows, n)) * 4).astype(np.float32)
+        vals[0, :] = -np.inf
+        vals[1, 3] = np.inf
+        vals[2, ::3] = np.nan
+        vals[3, :] = 1.5                                           # all equal: 1/n
+        vals[4, : n // 2] = -np.inf
+        bits = W.bf16_bits_from_f32(vals) if dtype == "bf16" else vals
+        conf = torch.full((rows,), -1.0, dtype=torch.float32, device="cuda")
+        out = A.acache_argmax_commit(up(bits, dtype), conf=conf)
+        x = O.from_bits(bits, dtype)
+        np.testing.assert_array_equal(out.cpu().numpy(), O.greedy_commit(x))
+        np.testing.assert_allclose(conf.cpu().numpy(), O.confidence(x), rtol=2e-5, atol=1e-30)
+
+
+# ----------------------------------------------------------------------------- decode steps vs the oracle
+
+@pytest.fixture(scope="module")
+def serve():
+    import torch
+    from paper_2608_26140_amd import workload as WL
+    w = W.get_config("mini-serve")
+    s = WL.build(w)
+    dt, lay = w.dims.dtype, w.layout
+    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    layers = oracle_layers(w, s.host)
+    dims = oracle_dims(w)
+    sk64, sv64 = oracle_stale(w, s.host, layers)
+    sk, sv = [], []
+    for n in range(len(layers)):
+        kb = W.bf16_bits_from_f32(sk64[n].astype(np.float32))
+        vb = W.bf16_bits_from_f32(sv64[n].astype(np.float32))
+        s.batch.k_pools[n][:L] = up(kb.reshape(L, -1), dt)
+        s.batch.v_pools[n][:L] = up(vb.reshape(L, -1), dt)
+        sk.append(O.from_bits(kb, dt))
+        sv.append(O.from_bits(vb, dt))
+    anchors = np.stack([O.topk_anchors(O.probe(layers, dims, oracle_request(w, s.host, b), sk, sv).scores, K)
+                        for b in range(B)])
+    torch.cuda.synchronize()
+    return w, s, layers, dims, sk, sv, anchors
+
+
+def _block_ids(w, base_ids, blk, seed):
+    """A seeded state of block ``blk``: each position holds a drawn token id
+    (committed) or keeps the mask id (not yet committed)."""
+    lay = w.layout
+    ids = base_ids.copy()
+    p0 = lay.mask_begin + blk * w.decode_block
+    B = ids.shape[0]
+    tok = W.draw_ints((B, w.decode_block), 0, w.dims.vocab - 1, seed=seed)
+    keep = W.draw_ints((B, w.decode_block), 0, 2, seed=seed, tag=1) == 0
+    ids[:, p0:p0 + w.decode_block] = np.where(keep, ids[:, p0:p0 + w.decode_block], tok)
+    return ids
+
+
+def test_decode_steps_against_oracle(serve):
+    import torch
+    from paper_2608_26140_amd import driver as D
+    w, s, layers, dims, sk, sv, anchors = serve
+    dt, lay = w.dims.dtype, w.layout
+    B, K, blen, S = w.batch, w.n_anchors, w.decode_block, lay.seq_len
+    blk = 1
+    p0 = lay.mask_begin + blk * blen
+    positions = np.arange(p0, p0 + blen)
+    emb = O.from_bits(s.host["embedding"], dt)
+    g_bits, head_bits = W.draw_lm_head(w)
+    head = D.Head(up(g_bits, dt), up(head_bits, dt))
+    g64, head64 = O.from_bits(g_bits, dt), O.from_bits(head_bits, dt)
+    plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=False)
+
+    # the refresh at the block's start, from the block-0-committed state
+    ids = _block_ids(w, s.host["ids"].reshape(B, S), 0, seed=71)
+    s.batch.remap.copy_(up_i32(ids.reshape(-1)))
+    x, m = s.batch.refresh(up_i32(anchors), K)
+    # the plan's write slots are the refresh's slots of the block's rows
+    np.testing.assert_array_equal(plan.write_slots[blk].cpu().numpy(),
+                                  m["write_slots"][plan.rows[blk].long()].cpu().numpy())
+    refs = []
+    for b in range(B):
+        base = oracle_request(w, s.host, b)
+        req = O.Request(x0=emb[ids[b]], pos=base.pos, affix=base.affix, masked=base.masked)
+        refs.append(O.selective_refresh(layers, dims, req, anchors[b], sk, sv))
+
+    wslots = plan.write_slots[blk].long()
+    kv = (w.dims.n_kv_heads, w.dims.head_dim)
+    for step, seed in enumerate((72, 73)):
+        ids = _block_ids(w, ids, blk, seed)
+        s.batch.remap.copy_(up_i32(ids.reshape(-1)))
+        keep = np.ones(s.batch.n_slots, dtype=bool)
+        keep[wslots.cpu().numpy()] = False
+        before = [down_bits(p[torch.from_numpy(np.flatnonzero(keep)).cuda()]) for p in s.batch.k_pools]
+        h = D.decode_step(s.batch, plan, blk, m["read_slots"])
+        y = D.A.acache_rmsnorm(s.batch.model.dims, h, head.norm_g)
+        logits = D.A.acache_linear(s.batch.model.dims, y, head.w)
+        conf = torch.empty(B * blen, dtype=torch.float32, device="cuda")
+        D.A.acache_argmax_commit(logits, conf=conf)
+        got_h = down(h).reshape(B, blen, -1)
+        got_lg = down(logits).reshape(B, blen, -1)
+        for b in range(B):
+            ref = refs[b]
+            xb = O.decode_step(layers, dims, ref.views_k, ref.views_v, emb[ids[b, positions]], positions)
+            what = f"step {step} request {b}"
+            assert_close(got_h[b], xb, dt, f"{what}: block rows")
+            lg = O.rms_norm(xb, g64, dims.rms_eps) @ head64.T
+            assert_close(got_lg[b], lg, dt, f"{what}: logits")
+            ws_b = wslots[b * blen:(b + 1) * blen]
+            for n in range(len(layers)):
+                assert_close(down(s.batch.k_pools[n][ws_b]).reshape(blen, *kv), ref.views_k[n][positions], dt,
+                             f"{what}: fresh K layer {n}")
+                assert_close(down(s.batch.v_pools[n][ws_b]).reshape(blen, *kv), ref.views_v[n][positions], dt,
+                             f"{what}: fresh V layer {n}")
+        # confidences: the kernel's softmax of its own logits
+        np.testing.assert_allclose(conf.cpu().numpy(), O.confidence(got_lg.reshape(B * blen, -1)), rtol=2e-5)
+        # a decode step writes only the block's slots
+        after = [down_bits(p[torch.from_numpy(np.flatnonzero(keep)).cuda()]) for p in s.batch.k_pools]
+        for a0, a1 in zip(before, after):
+            np.testing.assert_array_equal(a0, a1)
+
+
+# ----------------------------------------------------------------------------- the schedule
+
+def _fresh_ids(s, w):
+    s.batch.remap.copy_(up_i32(s.host["ids"].reshape(-1)))
+
+
+def _check_trace(trace, tau, blen, B, n_blocks, steps, ids_final, mask_begin, S):
+    by_block = [[t for t in trace if t["block"] == k] for k in range(n_blocks)]
+    assert [len(t) for t in by_block] == list(steps)
+    t32 = np.float32(tau)
+    for k, tr in enumerate(by_block):
+        assert 1 <= len(tr) <= blen
+        prev = np.zeros(B * blen, dtype=np.int32)
+        for t in tr:
+            new = (t["committed"] == 1) & (prev == 0)
+            assert np.all(t["committed"][prev == 1] == 1), "a commit was undone"
+            for b in range(B):
+                sl = slice(b * blen, (b + 1) * blen)
+                free = prev[sl] == 0
+                c = t["conf"][sl]
+                above = free & (c >= t32)
+                if above.any():
+                    assert np.array_equal(new[sl], above), f"block {k} request {b}: threshold commits"
+                elif free.any():
+                    assert new[sl].sum() == 1, f"block {k} request {b}: one fallback commit"
+                    r = int(np.flatnonzero(new[sl])[0])
+                    key = np.where(np.isnan(c), -0.5, c)
+                    assert key[r] == key[free].max() and r == np.flatnonzero(free & (key == key[r]))[0]
+                else:
+                    assert not new[sl].any()
+            # the committed ids are the step's picks
+            for i in np.flatnonzero(new):
+                b, r = divmod(int(i), blen)
+                assert ids_final[b * S + mask_begin + k * blen + r] == t["pick"][i]
+            prev = t["committed"].copy()
+        assert np.all(prev == 1), f"block {k} not fully committed"
+
+
+@pytest.mark.parametrize("tau", [0.9, 0.0, 2.0])
+def test_threshold_schedule(serve, tau):
+    import torch
+    from paper_2608_26140_amd import driver as D
+    w, s, layers, dims, sk, sv, anchors = serve
+    dt, lay = w.dims.dtype, w.layout
+    B, K, blen = w.batch, w.n_anchors, w.decode_block
+    n_blocks = lay.mask_len // blen
+    g_bits, head_bits = W.draw_lm_head(w)
+    head = D.Head(up(g_bits, dt), up(head_bits, dt))
+    plan = D.DecodePlan(s.batch, K, blen, n_blocks, full=False)
+    a = up_i32(anchors)
+    _fresh_ids(s, w)
+    trace = []
+    steps = D.decode_threshold_schedule(s.batch, head, plan, K, tau, anchors=a, trace=trace)
+    ids_final = s.batch.remap.cpu().numpy()
+    _check_trace(trace, tau, blen, B, n_blocks, steps, ids_final, lay.mask_begin, lay.seq_len)
+    if tau == 0.0:
+        # every row passes at once: the one-step greedy schedule
+        assert steps == [1] * n_blocks
+        _fresh_ids(s, w)
+        logits = torch.empty((B * blen, w.dims.vocab), dtype=torch.bfloat16, device="cuda")
+        committed = torch.empty((n_blocks, B * blen), dtype=torch.int32, device="cuda")
+        D.decode_schedule(s.batch, head, plan, K, logits, committed, anchors=a)
+        np.testing.assert_array_equal(s.batch.remap.cpu().numpy(), ids_final)
+    if tau > 1.0:
+        assert steps == [blen] * n_blocks

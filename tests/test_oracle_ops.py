@@ -329,3 +329,30 @@ def test_greedy_commit_brute_force_and_numpy():
                 best = j
         assert got[i] == best
     np.testing.assert_array_equal(got, np.argmax(x, axis=1))  # first maximum, as numpy defines it
+
+
+def test_confidence_and_threshold_commit():
+    x = np.array([[0.0, np.log(3.0), -np.inf, np.nan],   # probs 1/4, 3/4 -> 0.75
+                  [1.0, 1.0, 1.0, 1.0],                    # 0.25
+                  [np.nan, -np.inf, np.nan, -np.inf]])     # no finite value -> 0
+    np.testing.assert_allclose(O.confidence(x), [0.75, 0.25, 0.0], rtol=1e-12)
+    conf = np.array([0.3, 0.95, 0.2, 0.97, np.nan])
+    np.testing.assert_array_equal(O.threshold_commit(conf, np.zeros(5, bool), 0.9), [0, 1, 0, 1, 0])
+    # none above tau: the single most confident free row, lowest row on ties
+    np.testing.assert_array_equal(O.threshold_commit(np.array([0.3, 0.5, 0.5, 0.1]), np.array([0, 0, 0, 0], bool), 0.9),
+                                  [0, 1, 0, 0])
+    np.testing.assert_array_equal(O.threshold_commit(np.array([0.3, 0.5, 0.5, 0.1]), np.array([0, 1, 0, 0], bool), 0.9),
+                                  [0, 0, 1, 0])
+    # nothing left to commit
+    assert not O.threshold_commit(np.array([0.9]), np.array([True]), 0.5).any()
+    # brute force: random confidences
+    rng = np.random.default_rng(5)
+    for _ in range(50):
+        c = rng.random(8)
+        done = rng.random(8) < 0.3
+        t = O.threshold_commit(c, done, 0.7)
+        want = (~done) & (c >= 0.7)
+        if not want.any() and (~done).any():
+            want = np.zeros(8, bool)
+            want[min(np.flatnonzero(~done), key=lambda i: (-c[i], i))] = True
+        np.testing.assert_array_equal(t, want)
