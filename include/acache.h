@@ -59,7 +59,8 @@ typedef enum {
   ACACHE_ERR_ALIGN = 3,       /* a pointer or leading dimension is not 16-byte aligned */
   ACACHE_ERR_UNSUPPORTED = 4, /* valid, but outside the shapes the kernels implement */
   ACACHE_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than acache_workspace_size() */
-  ACACHE_ERR_DEVICE = 6       /* a HIP launch or call failed */
+  ACACHE_ERR_DEVICE = 6,      /* a HIP launch or call failed */
+  ACACHE_ERR_SPACE = 7        /* a block pool has fewer free blocks than asked for */
 } acache_status;
 
 typedef enum { ACACHE_F32 = 0, ACACHE_BF16 = 1 } acache_dtype;
@@ -193,6 +194,53 @@ acache_status acache_build_maps(const acache_layout* layout, int32_t batch,
                                 const int32_t* anchors, int32_t k, int32_t* row_pos,
                                 int32_t* row_src, int32_t* write_slots, int32_t* read_slots,
                                 int32_t* q_rows, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Block-granular KV slots (Section 4.1: the shared prefix cache sits in
+ * reserved shared blocks, and each request's anchors and request-specific
+ * positions in private blocks; peak KV use is then counted in whole blocks,
+ * the granularity behind the batch-1 overhead discussed with Table 4).
+ *
+ * A paged slot plan: slots come in blocks of block_size consecutive slots,
+ * block id i covering slots i*block_size .. i*block_size + block_size-1.
+ *   affix-local index j      -> shared_blocks[j / bs] * bs + j % bs
+ *   request b's rank-i row   -> private_blocks[b * blocks_per_request + i / bs] * bs + i % bs
+ * (bs = block_size).  shared_blocks [ceil(L / bs)] and private_blocks
+ * [batch * blocks_per_request] are DEVICE arrays of block ids >= 0; a slot
+ * that would not fit in int32 is written as -1, which every consumer skips.
+ */
+typedef struct {
+  int32_t block_size;
+  int32_t blocks_per_request;
+  const int32_t* shared_blocks;
+  const int32_t* private_blocks;
+} acache_paging;
+
+/* acache_build_maps_paged — acache_build_maps with the slots of a paged
+ * plan in place of shared_base / private_base / private_stride (which it
+ * ignores): the same rows, positions and order.  Requires block_size >= 1
+ * and blocks_per_request * block_size >= R. */
+acache_status acache_build_maps_paged(const acache_layout* layout, const acache_paging* paging,
+                                      int32_t batch, const int32_t* anchors, int32_t k, int32_t* row_pos,
+                                      int32_t* row_src, int32_t* write_slots, int32_t* read_slots,
+                                      int32_t* q_rows, hipStream_t stream);
+
+/* acache_block_pool — a host-side allocator of block ids 0 .. capacity-1
+ * (no device memory: the caller sizes the KV pools to capacity blocks).
+ * alloc writes n ids to ids [host] — the lowest free ones, ascending — or
+ * returns ACACHE_ERR_SPACE and allocates nothing; free returns n allocated
+ * ids (ACACHE_ERR_SHAPE, and nothing freed, for an id out of range, not
+ * allocated, or listed twice).  stats reports capacity, blocks in use and
+ * the peak in use since creation or reset_peak (any output may be NULL).
+ * A pool is not thread-safe. */
+typedef struct acache_block_pool acache_block_pool;
+acache_status acache_block_pool_create(int32_t capacity, acache_block_pool** pool);
+acache_status acache_block_pool_destroy(acache_block_pool* pool);
+acache_status acache_block_pool_alloc(acache_block_pool* pool, int32_t n, int32_t* ids);
+acache_status acache_block_pool_free(acache_block_pool* pool, int32_t n, const int32_t* ids);
+acache_status acache_block_pool_stats(const acache_block_pool* pool, int32_t* capacity, int32_t* in_use,
+                                      int32_t* peak);
+acache_status acache_block_pool_reset_peak(acache_block_pool* pool);
 
 /* ---------------------------------------------------------------------------
  * acache_attention — read-slot attention (Appendix C.1): for request b,

@@ -261,7 +261,9 @@ def confidence(logits: np.ndarray) -> np.ndarray:
             continue
         m = fin.max()
         top = fin == m  # equal maxima, +inf included, count exactly once each
-        out[i] = 1.0 / np.sum(np.where(top, 1.0, np.exp(np.where(top, 0.0, fin - m))))
+        with np.errstate(invalid="ignore"):  # inf - inf where top; replaced by 0
+            d = np.where(top, 0.0, fin - m)
+        out[i] = 1.0 / np.sum(np.where(top, 1.0, np.exp(d)))
     return out
 
 
@@ -448,6 +450,25 @@ def build_maps(seq_len: int, affix_begin: int, affix_len: int, mask_begin: int, 
     affix_begin).  Returns row_pos, row_src (b * seq_len + p), write_slots,
     read_slots [B * seq_len], q_rows (batch row index of each masked
     position)."""
+    return _maps(seq_len, affix_begin, affix_len, mask_begin, mask_len, anchors,
+                 lambda j: shared_base + j, lambda b, i: private_base + b * private_stride + i)
+
+
+def build_maps_paged(seq_len: int, affix_begin: int, affix_len: int, mask_begin: int, mask_len: int,
+                     anchors: np.ndarray, block_size: int, shared_blocks, private_blocks,
+                     blocks_per_request: int):
+    """The same maps over block-granular slots (Section 4.1: shared blocks
+    for the affix cache, private blocks per request): affix-local index j
+    lives in slot shared_blocks[j // bs] * bs + j % bs, request b's i-th
+    recomputed position in private_blocks[b * blocks_per_request + i // bs]
+    * bs + i % bs."""
+    bs = block_size
+    return _maps(seq_len, affix_begin, affix_len, mask_begin, mask_len, anchors,
+                 lambda j: int(shared_blocks[j // bs]) * bs + j % bs,
+                 lambda b, i: int(private_blocks[b * blocks_per_request + i // bs]) * bs + i % bs)
+
+
+def _maps(seq_len, affix_begin, affix_len, mask_begin, mask_len, anchors, shared_slot, private_slot):
     anchors = np.asarray(anchors, dtype=np.int64).reshape(len(anchors), -1)
     n_req = anchors.shape[0]
     row_pos, row_src, write_slots, q_rows = [], [], [], []
@@ -459,13 +480,13 @@ def build_maps(seq_len: int, affix_begin: int, affix_len: int, mask_begin: int, 
                       if not (affix_begin <= p < affix_begin + affix_len) or p in anchor_pos]
         slot_of = {}
         for i, p in enumerate(recomputed):
-            slot = private_base + b * private_stride + i
+            slot = private_slot(b, i)
             slot_of[p] = slot
             row_pos.append(p)
             row_src.append(b * seq_len + p)
             write_slots.append(slot)
         for p in range(seq_len):
-            read_slots[b * seq_len + p] = slot_of[p] if p in slot_of else shared_base + (p - affix_begin)
+            read_slots[b * seq_len + p] = slot_of[p] if p in slot_of else shared_slot(p - affix_begin)
         index_of = {p: i for i, p in enumerate(recomputed)}
         for p in range(mask_begin, mask_begin + mask_len):
             q_rows.append(base_row + index_of[p])

@@ -53,6 +53,11 @@ class Layout(ctypes.Structure):
                                               "shared_base", "private_base", "private_stride")]
 
 
+class Paging(ctypes.Structure):
+    _fields_ = [("block_size", ctypes.c_int32), ("blocks_per_request", ctypes.c_int32),
+                ("shared_blocks", ctypes.c_void_p), ("private_blocks", ctypes.c_void_p)]
+
+
 def _load():
     if not os.path.exists(_LIB_PATH):
         raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2608_26140_amd.build`")
@@ -69,6 +74,13 @@ def _load():
         "acache_rerotate_k": [ctypes.POINTER(Dims), P, P, P, P, P, I32, I64, I64, P],
         "acache_kv_deviation": [ctypes.POINTER(Dims), I32, I32, P, P, I64, I64, P, I64, P, P, P],
         "acache_build_maps": [ctypes.POINTER(Layout), I32, P, I32, P, P, P, P, P, P],
+        "acache_build_maps_paged": [ctypes.POINTER(Layout), ctypes.POINTER(Paging), I32, P, I32, P, P, P, P, P, P],
+        "acache_block_pool_create": [I32, ctypes.POINTER(P)],
+        "acache_block_pool_destroy": [P],
+        "acache_block_pool_alloc": [P, I32, PI],
+        "acache_block_pool_free": [P, I32, PI],
+        "acache_block_pool_stats": [P, PI, PI, PI],
+        "acache_block_pool_reset_peak": [P],
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
                                    P, P, P, P, P, P, I64, I64, ctypes.POINTER(ScoreArgs), P, SZ, P],
@@ -185,6 +197,66 @@ def acache_build_maps(layout: Layout, batch: int, anchors: Optional[torch.Tensor
         _ptr(out["row_src"]), _ptr(out["write_slots"]), _ptr(out["read_slots"]), _ptr(out["q_rows"]),
         _stream(stream)))
     return out
+
+
+def acache_build_maps_paged(layout: Layout, batch: int, anchors: Optional[torch.Tensor], k: int, block_size: int,
+                            shared_blocks: Optional[torch.Tensor], private_blocks: torch.Tensor,
+                            blocks_per_request: int, device="cuda", stream=None) -> dict:
+    """acache_build_maps with slots from block tables (device int32)."""
+    if anchors is not None:
+        _dev_i32(anchors, "anchors")
+    for t, n in ((shared_blocks, "shared_blocks"), (private_blocks, "private_blocks")):
+        if t is not None:
+            _dev_i32(t, n)
+    R = k + layout.seq_len - layout.affix_len
+    t = lambda n: torch.empty(n, dtype=torch.int32, device=device)
+    out = dict(row_pos=t(batch * R), row_src=t(batch * R), write_slots=t(batch * R),
+               read_slots=t(batch * layout.seq_len), q_rows=t(batch * layout.mask_len))
+    pg = Paging(block_size, blocks_per_request, None if shared_blocks is None else shared_blocks.data_ptr(),
+                None if private_blocks is None else private_blocks.data_ptr())
+    _check("acache_build_maps_paged", lib.acache_build_maps_paged(
+        ctypes.byref(layout), ctypes.byref(pg), batch, _ptr(anchors) if k > 0 else None, k, _ptr(out["row_pos"]),
+        _ptr(out["row_src"]), _ptr(out["write_slots"]), _ptr(out["read_slots"]), _ptr(out["q_rows"]),
+        _stream(stream)))
+    return out
+
+
+class BlockPool:
+    """The library's host-side KV block allocator (acache_block_pool)."""
+
+    def __init__(self, capacity: int):
+        h = ctypes.c_void_p()
+        _check("acache_block_pool_create", lib.acache_block_pool_create(int(capacity), ctypes.byref(h)))
+        self._h = h
+
+    def alloc(self, n: int) -> list:
+        ids = (ctypes.c_int32 * max(n, 1))()
+        _check("acache_block_pool_alloc", lib.acache_block_pool_alloc(self._h, int(n), ids))
+        return list(ids[:n])
+
+    def free(self, ids: Sequence[int]):
+        arr = _i32(list(ids)) if len(ids) else (ctypes.c_int32 * 1)()
+        _check("acache_block_pool_free", lib.acache_block_pool_free(self._h, len(ids), arr))
+
+    def stats(self) -> dict:
+        c, u, p = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check("acache_block_pool_stats", lib.acache_block_pool_stats(self._h, ctypes.byref(c), ctypes.byref(u),
+                                                                      ctypes.byref(p)))
+        return dict(capacity=c.value, in_use=u.value, peak=p.value)
+
+    def reset_peak(self):
+        _check("acache_block_pool_reset_peak", lib.acache_block_pool_reset_peak(self._h))
+
+    def close(self):
+        if self._h:
+            lib.acache_block_pool_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def _ragged(cu_rows: Sequence[int], cu_keys: Sequence[int]):

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libacache.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "k_rows.hip", "k_topk.hip", "k_gemm.hip", "k_attention.hip", "k_score.hip", "k_f32.hip"]
+SOURCES = ["api.cpp", "k_rows.hip", "k_topk.hip", "k_gemm.hip", "k_attention.hip", "k_score.hip", "k_f32.hip", "pages.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

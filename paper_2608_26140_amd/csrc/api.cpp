@@ -210,6 +210,7 @@ const char* acache_status_string(acache_status st) {
     case ACACHE_ERR_UNSUPPORTED: return "shape or type outside what the kernels implement";
     case ACACHE_ERR_WORKSPACE: return "workspace missing or too small";
     case ACACHE_ERR_DEVICE: return "a HIP launch or call failed";
+    case ACACHE_ERR_SPACE: return "not enough free blocks in the pool";
   }
   return "unknown status";
 }
@@ -334,6 +335,39 @@ acache_status acache_threshold_commit(int32_t batch, int32_t block, const int32_
   return ACACHE_OK;
 }
 
+static acache_status check_layout(const acache_layout* lay, int32_t batch, int32_t k) {
+  CHECK(lay, ACACHE_ERR_NULL);
+  const int S = lay->seq_len, ab = lay->affix_begin, L = lay->affix_len;
+  CHECK(batch >= 0 && S >= 0 && L >= 0 && ab >= 0 && ab + L <= S, ACACHE_ERR_SHAPE);
+  CHECK(k >= 0 && k <= L, ACACHE_ERR_SHAPE);
+  CHECK(lay->mask_len >= 0 && lay->mask_begin >= 0 && lay->mask_begin + lay->mask_len <= S,
+        ACACHE_ERR_SHAPE);
+  CHECK(lay->mask_len == 0 || lay->mask_begin + lay->mask_len <= ab || lay->mask_begin >= ab + L,
+        ACACHE_ERR_SHAPE);  // the masked span is not part of the affix
+  CHECK((int64_t)batch * S < (int64_t)1 << 31, ACACHE_ERR_SHAPE);
+  return ACACHE_OK;
+}
+
+acache_status acache_build_maps_paged(const acache_layout* lay, const acache_paging* paging, int32_t batch,
+                                      const int32_t* anchors, int32_t k, int32_t* row_pos, int32_t* row_src,
+                                      int32_t* write_slots, int32_t* read_slots, int32_t* q_rows,
+                                      hipStream_t stream) {
+  acache_status st = check_layout(lay, batch, k);
+  if (st != ACACHE_OK) return st;
+  CHECK(paging, ACACHE_ERR_NULL);
+  const int R = k + lay->seq_len - lay->affix_len;
+  CHECK(paging->block_size >= 1 && paging->blocks_per_request >= 0, ACACHE_ERR_SHAPE);
+  CHECK((int64_t)paging->blocks_per_request * paging->block_size >= R, ACACHE_ERR_SHAPE);
+  if (batch == 0 || lay->seq_len == 0) return ACACHE_OK;
+  CHECK(row_pos && row_src && write_slots && read_slots, ACACHE_ERR_NULL);
+  CHECK(k == 0 || anchors, ACACHE_ERR_NULL);
+  CHECK(lay->affix_len == k || paging->shared_blocks, ACACHE_ERR_NULL);  // some affix position reads shared
+  CHECK(R == 0 || paging->private_blocks, ACACHE_ERR_NULL);
+  LAUNCH_T(ACACHE_K_MAPS, stream, launch_build_maps(*lay, paging, batch, anchors, k, row_pos, row_src, write_slots,
+                                                    read_slots, q_rows, stream));
+  return ACACHE_OK;
+}
+
 acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const int32_t* anchors,
                                 int32_t k, int32_t* row_pos, int32_t* row_src,
                                 int32_t* write_slots, int32_t* read_slots, int32_t* q_rows,
@@ -353,8 +387,8 @@ acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const i
   if (batch == 0 || S == 0) return ACACHE_OK;
   CHECK(row_pos && row_src && write_slots && read_slots, ACACHE_ERR_NULL);
   CHECK(k == 0 || anchors, ACACHE_ERR_NULL);
-  LAUNCH_T(ACACHE_K_MAPS, stream, launch_build_maps(*lay, batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows,
-                           stream));
+  LAUNCH_T(ACACHE_K_MAPS, stream, launch_build_maps(*lay, nullptr, batch, anchors, k, row_pos, row_src, write_slots,
+                                                    read_slots, q_rows, stream));
   return ACACHE_OK;
 }
 

@@ -27,9 +27,10 @@ hipError_t launch_gather_rows(const void* src, int64_t src_ld, int64_t src_rows,
 hipError_t launch_kv_scatter(const void* k_src, const void* v_src, int64_t src_ld_bytes, int n,
                              const int32_t* slots, void* k_pool, void* v_pool,
                              int64_t pool_ld_bytes, int64_t n_slots, int row_bytes, hipStream_t s);
-hipError_t launch_build_maps(const acache_layout& lay, int batch, const int32_t* anchors, int k,
-                             int32_t* row_pos, int32_t* row_src, int32_t* write_slots,
-                             int32_t* read_slots, int32_t* q_rows, hipStream_t s);
+// paging NULL: the layout's flat slot plan
+hipError_t launch_build_maps(const acache_layout& lay, const acache_paging* paging, int batch,
+                             const int32_t* anchors, int k, int32_t* row_pos, int32_t* row_src,
+                             int32_t* write_slots, int32_t* read_slots, int32_t* q_rows, hipStream_t s);
 hipError_t launch_topk(const float* scores, int batch, int L, int k, int32_t* out, hipStream_t s);
 hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y, int rows, int d,
                           float eps, hipStream_t s);

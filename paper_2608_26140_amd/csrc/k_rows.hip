@@ -56,7 +56,16 @@ __global__ __launch_bounds__(256) void kv_scatter_kernel(const char* __restrict_
 }
 
 // ---------------------------------------------------------------- maps (Section 4.1)
-__global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, int batch,
+// Slot of index i in a block table (block_size consecutive slots per block);
+// -1 where the slot does not fit in int32.
+__device__ __forceinline__ int32_t paged_slot(const int32_t* __restrict__ table, int bs, int i) {
+  const int64_t s = (int64_t)table[i / bs] * bs + (i % bs);
+  return (s >= 0 && s <= INT32_MAX) ? (int32_t)s : -1;
+}
+
+// With pg.block_size > 0 the slots come from the paging plan's block tables;
+// otherwise from the layout's shared_base / private_base / private_stride.
+__global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, acache_paging pg, int batch,
                                                          const int32_t* __restrict__ anchors, int k,
                                                          int32_t* __restrict__ row_pos,
                                                          int32_t* __restrict__ row_src,
@@ -90,7 +99,9 @@ __global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, int 
   }
   int32_t slot;
   if (rec) {
-    slot = lay.private_base + b * lay.private_stride + rank;
+    slot = pg.block_size > 0
+               ? paged_slot(pg.private_blocks + (int64_t)b * pg.blocks_per_request, pg.block_size, rank)
+               : lay.private_base + b * lay.private_stride + rank;
     const int64_t row = (int64_t)b * R + rank;
     row_pos[row] = p;
     row_src[row] = b * S + p;
@@ -98,7 +109,7 @@ __global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, int 
     if (q_rows && p >= lay.mask_begin && p < lay.mask_begin + lay.mask_len)
       q_rows[(int64_t)b * lay.mask_len + (p - lay.mask_begin)] = (int32_t)row;
   } else {
-    slot = lay.shared_base + (p - ab);
+    slot = pg.block_size > 0 ? paged_slot(pg.shared_blocks, pg.block_size, p - ab) : lay.shared_base + (p - ab);
   }
   rslots[t] = slot;
 }
@@ -459,11 +470,13 @@ hipError_t launch_kv_scatter(const void* k_src, const void* v_src, int64_t src_l
   return hipGetLastError();
 }
 
-hipError_t launch_build_maps(const acache_layout& lay, int batch, const int32_t* anchors, int k,
-                             int32_t* row_pos, int32_t* row_src, int32_t* write_slots,
-                             int32_t* read_slots, int32_t* q_rows, hipStream_t s) {
+hipError_t launch_build_maps(const acache_layout& lay, const acache_paging* paging, int batch,
+                             const int32_t* anchors, int k, int32_t* row_pos, int32_t* row_src,
+                             int32_t* write_slots, int32_t* read_slots, int32_t* q_rows, hipStream_t s) {
   const int64_t work = (int64_t)batch * lay.seq_len;
-  hipLaunchKernelGGL(build_maps_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, lay,
+  acache_paging pg{};
+  if (paging) pg = *paging;
+  hipLaunchKernelGGL(build_maps_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, lay, pg,
                      batch, anchors, k, row_pos, row_src, write_slots, read_slots, q_rows);
   return hipGetLastError();
 }

@@ -17,6 +17,7 @@ from __future__ import annotations
 import contextlib
 from typing import List, Optional
 
+import numpy as np
 import torch
 
 from . import acache as A
@@ -51,13 +52,21 @@ class AffixBatch:
     either indexed by b * S + position (hidden rows) or through ``remap``
     (token ids, x_src = embedding table).
 
-    KV pools: one K and one V pool per layer, [L + B * private_stride,
-    H_kv * d_h].  Slots [0, L) are the shared affix region; request b's
-    recomputed rows use [L + b * private_stride, ...) (Section 4.1)."""
+    KV pools: one K and one V pool per layer, [n_slots, H_kv * d_h]
+    (Section 4.1).  Flat plan (block_size None): slots [0, L) are the shared
+    affix region and request b's recomputed rows use [L + b *
+    private_stride, ...).  Paged plan: slots come in blocks of block_size
+    from the library's block pool; the shared affix takes ceil(L / bs)
+    blocks at creation (the first ones: slots [0, L) again), and each
+    request a private block table of ceil(R / bs) blocks, grown when a call
+    needs more rows and given back by release_private().  The pools hold
+    enough blocks for the largest R the batch is built for (max_rows, else
+    S: full recomputation)."""
 
     def __init__(self, model: Model, seq_len: int, affix_begin: int, affix_len: int, mask_begin: int,
                  mask_len: int, batch: int, x_src: torch.Tensor, remap: Optional[torch.Tensor] = None,
-                 private_stride: Optional[int] = None, max_rows: Optional[int] = None, device="cuda"):
+                 private_stride: Optional[int] = None, max_rows: Optional[int] = None, device="cuda",
+                 block_size: Optional[int] = None):
         self.model = model
         self.S, self.ab, self.L = seq_len, affix_begin, affix_len
         self.mb, self.G, self.B = mask_begin, mask_len, batch
@@ -65,21 +74,74 @@ class AffixBatch:
         self.x_src = x_src
         self.remap = remap
         self.device = device
-        self.n_slots = affix_len + batch * self.stride
+        self.bs = block_size
+        self.table_version = 0
+        r_max = seq_len if max_rows is None else max_rows
+        if block_size:
+            n_shared = -(-affix_len // block_size)
+            self.pages = A.BlockPool(n_shared + batch * -(-r_max // block_size))
+            self.shared_host = self.pages.alloc(n_shared)
+            self.shared_blocks = self._i32(self.shared_host)
+            self._table_host, self._table, self._table_nb = [], None, 0
+            self.n_slots = self.pages.stats()["capacity"] * block_size
+            j = np.arange(affix_len)
+            self.affix_slots = self._i32(np.asarray(self.shared_host, dtype=np.int64)[j // block_size] * block_size
+                                         + j % block_size)
+        else:
+            self.pages = None
+            self.n_slots = affix_len + batch * self.stride
+            self.affix_slots = torch.arange(affix_len, dtype=torch.int32, device=device)
         shape = (self.n_slots, model.kv_width)
         self.k_pools = [torch.zeros(shape, dtype=model.dtype, device=device) for _ in range(model.n_layers)]
         self.v_pools = [torch.zeros(shape, dtype=model.dtype, device=device) for _ in range(model.n_layers)]
-        self.affix_slots = torch.arange(affix_len, dtype=torch.int32, device=device)
-        rows = batch * (seq_len if max_rows is None else max_rows)
-        self.ws = A.workspace(model.dims, rows, batch, affix_len, device)
+        self.ws = A.workspace(model.dims, batch * r_max, batch, affix_len, device)
         self.layout = A.Layout(seq_len, affix_begin, affix_len, mask_begin, mask_len, 0, affix_len, self.stride)
+
+    def _i32(self, a) -> torch.Tensor:
+        return torch.from_numpy(np.ascontiguousarray(np.asarray(a), dtype=np.int32)).to(self.device)
+
+    # ------------------------------------------------------------------ paging
+    def private_table(self, R: int):
+        """The private block table ([B * nb] device ids, nb) covering R rows
+        per request; grows (new blocks, old ones returned) when R needs more."""
+        nb = -(-R // self.bs)
+        if nb > self._table_nb:
+            self.release_private()
+            self._table_host = self.pages.alloc(self.B * nb)
+            self._table, self._table_nb = self._i32(self._table_host), nb
+            self.table_version += 1
+        return self._table, self._table_nb
+
+    def release_private(self):
+        """Give every request's private blocks back to the pool."""
+        if self.pages is not None and self._table_host:
+            self.pages.free(self._table_host)
+            self._table_host, self._table, self._table_nb = [], None, 0
+            self.table_version += 1
+
+    def private_slots(self, R: int) -> np.ndarray:
+        """[B, R] slot of request b's rank-i recomputed row (host copy)."""
+        i = np.arange(R)
+        if self.pages is None:
+            return self.L + np.arange(self.B)[:, None] * self.stride + i[None, :]
+        _, nb = self.private_table(R)
+        tbl = np.asarray(self._table_host, dtype=np.int64).reshape(self.B, nb)
+        return tbl[:, i // self.bs] * self.bs + i % self.bs
+
+    def kv_bytes(self, blocks: int) -> int:
+        """Bytes of K and V over every layer held by `blocks` blocks."""
+        return blocks * self.bs * self.model.kv_width * 2 * self.model.n_layers * self.k_pools[0].element_size()
 
     # ------------------------------------------------------------------ pieces
     def rows_per_request(self, k: int) -> int:
         return k + self.S - self.L
 
     def maps(self, anchors: Optional[torch.Tensor], k: int, stream=None) -> dict:
-        return A.acache_build_maps(self.layout, self.B, anchors, k, self.device, stream)
+        if self.pages is None:
+            return A.acache_build_maps(self.layout, self.B, anchors, k, self.device, stream)
+        tbl, nb = self.private_table(self.rows_per_request(k))
+        return A.acache_build_maps_paged(self.layout, self.B, anchors, k, self.bs, self.shared_blocks, tbl, nb,
+                                         self.device, stream)
 
     def gather_inputs(self, m: dict, stream=None) -> torch.Tensor:
         return A.acache_gather_rows(self.x_src, m["row_src"], self.remap, stream=stream)
@@ -204,7 +266,6 @@ def block_row_index(batch: AffixBatch, k: int, block_begin: int, block_len: int)
     positions [block_begin, block_begin + block_len) of every request.  A
     request's rows are its anchors then its non-affix positions, each in
     ascending order; the block lies in the masked span, after the affix."""
-    import numpy as np
     S, ab, L, B = batch.S, batch.ab, batch.L, batch.B
     assert block_begin >= ab + L, "the generation block follows the affix"
     nonaffix = np.concatenate([np.arange(0, ab), np.arange(ab + L, S)])
@@ -226,7 +287,7 @@ class DecodePlan:
         self.k = batch.L if full else k
         self.anchors = (torch.arange(batch.L, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
                         if full else None)
-        self.rows, self.pos, self.row_pos, self.write_slots = [], [], [], []
+        self.rows, self.pos, self.row_pos, self.local = [], [], [], []
         nonaffix = np.concatenate([np.arange(0, batch.ab), np.arange(batch.ab + batch.L, S)])
         i32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
         for blk in range(n_blocks):
@@ -235,10 +296,19 @@ class DecodePlan:
             p = np.arange(p0, p0 + block_len)
             self.pos.append(i32((np.arange(B)[:, None] * S + p[None, :]).reshape(-1)))
             self.row_pos.append(i32(np.tile(p, B)))
-            # a request's refresh row i writes private slot L + b * stride + i
-            # (Section 4.1); the block's rows keep those slots while it decodes
-            local = self.k + np.searchsorted(nonaffix, p)
-            self.write_slots.append(i32((batch.L + np.arange(B)[:, None] * batch.stride + local[None, :]).reshape(-1)))
+            self.local.append(self.k + np.searchsorted(nonaffix, p))  # the rows' ranks in a request
+        self._slots, self._version = None, None
+
+    def write_slots(self, batch: AffixBatch, blk: int) -> torch.Tensor:
+        """[B * block_len] private slots of block blk's rows: the slots their
+        refresh rows wrote (Section 4.1), which the block keeps while it
+        decodes.  Rebuilt when the batch's slot plan has changed."""
+        if self._version != batch.table_version or self._slots is None:
+            slots = batch.private_slots(batch.rows_per_request(self.k))
+            self._slots = [torch.from_numpy(np.ascontiguousarray(slots[:, loc].reshape(-1), dtype=np.int32))
+                           .to(batch.device) for loc in self.local]
+            self._version = batch.table_version
+        return self._slots[blk]
 
 
 def decode_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, logits: torch.Tensor,
@@ -282,7 +352,7 @@ def decode_step(batch: AffixBatch, plan: DecodePlan, blk: int, read_slots: torch
     h = A.acache_gather_rows(batch.x_src, plan.pos[blk], batch.remap, stream=stream)
     for i in range(batch.model.n_layers):
         A.acache_layer_recompute(batch.model.dims, batch.model.lw[i], cu_rows, cu_keys, h, plan.row_pos[blk],
-                                 plan.write_slots[blk], read_slots, batch.k_pools[i], batch.v_pools[i],
+                                 plan.write_slots(batch, blk), read_slots, batch.k_pools[i], batch.v_pools[i],
                                  batch.ws, stream=stream)
     return h
 

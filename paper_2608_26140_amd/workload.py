@@ -49,7 +49,7 @@ class Setup:
 
 
 def build(w: W.Workload, device="cuda", n_layers: Optional[int] = None, keep_host: bool = True,
-          max_rows: Optional[int] = None) -> Setup:
+          max_rows: Optional[int] = None, block_size: Optional[int] = None) -> Setup:
     d, lay = w.dims, w.layout
     nl = d.n_layers if n_layers is None else n_layers
     host = {"layers": []}
@@ -76,7 +76,7 @@ def build(w: W.Workload, device="cuda", n_layers: Optional[int] = None, keep_hos
         x_src = upload(hidden.reshape(B * S, d.d_model), d.dtype, device)
         remap = None
     batch = AffixBatch(model, S, lay.affix_begin, lay.affix_len, lay.mask_begin, lay.mask_len, B, x_src,
-                       remap, device=device, max_rows=max_rows)
+                       remap, device=device, max_rows=max_rows, block_size=block_size)
 
     L = lay.affix_len
     if w.stale == "perturb":
@@ -85,14 +85,15 @@ def build(w: W.Workload, device="cuda", n_layers: Optional[int] = None, keep_hos
             host.update(donor=donor)
         dx = upload(donor, d.dtype, device)
         pos = upload_i32(np.arange(lay.affix_begin, lay.affix_end))
-        slots = upload_i32(np.arange(L))
-        batch.materialize_affix(dx, pos, slots, slots)
+        batch.materialize_affix(dx, pos, batch.affix_slots, batch.affix_slots)
     elif w.stale == "donor":
-        # donor request: all S positions; affix rows -> shared slots j, the
-        # rest -> request 0's private region (overwritten later)
+        # donor request: all S positions; affix rows -> the shared affix
+        # slots, the rest -> request 0's private slots (overwritten later)
         p = np.arange(S)
         in_affix = (p >= lay.affix_begin) & (p < lay.affix_end)
-        wslots = np.where(in_affix, p - lay.affix_begin, L + p).astype(np.int32)
+        wslots = np.empty(S, dtype=np.int64)
+        wslots[in_affix] = batch.affix_slots.cpu().numpy()
+        wslots[~in_affix] = batch.private_slots(S - L)[0]
         dx = A.acache_gather_rows(x_src, upload_i32(np.arange(S)), upload_i32(donor_ids))
         batch.materialize_affix(dx, upload_i32(p), upload_i32(wslots), upload_i32(wslots))
     else:

@@ -151,7 +151,7 @@ def test_decode_steps_against_oracle(serve):
     s.batch.remap.copy_(up_i32(ids.reshape(-1)))
     x, m = s.batch.refresh(up_i32(anchors), K)
     # the plan's write slots are the refresh's slots of the block's rows
-    np.testing.assert_array_equal(plan.write_slots[blk].cpu().numpy(),
+    np.testing.assert_array_equal(plan.write_slots(s.batch, blk).cpu().numpy(),
                                   m["write_slots"][plan.rows[blk].long()].cpu().numpy())
     refs = []
     for b in range(B):
@@ -159,7 +159,7 @@ def test_decode_steps_against_oracle(serve):
         req = O.Request(x0=emb[ids[b]], pos=base.pos, affix=base.affix, masked=base.masked)
         refs.append(O.selective_refresh(layers, dims, req, anchors[b], sk, sv))
 
-    wslots = plan.write_slots[blk].long()
+    wslots = plan.write_slots(s.batch, blk).long()
     kv = (w.dims.n_kv_heads, w.dims.head_dim)
     for step, seed in enumerate((72, 73)):
         ids = _block_ids(w, ids, blk, seed)
@@ -260,3 +260,46 @@ def test_threshold_schedule(serve, tau):
         np.testing.assert_array_equal(s.batch.remap.cpu().numpy(), ids_final)
     if tau > 1.0:
         assert steps == [blen] * n_blocks
+
+
+# ----------------------------------------------------------------------------- block-granular slots
+
+def test_paged_matches_flat():
+    """The paged slot plan changes where K/V live, not what is computed: the
+    probe, the selective refresh, a decode step and the threshold schedule
+    give identical bits under both plans, and the block pool holds exactly
+    the shared blocks plus one table of ceil(R / bs) blocks per request."""
+    import torch
+    from paper_2608_26140_amd import driver as D
+    from paper_2608_26140_amd import workload as WL
+    w = W.get_config("mini-serve")
+    dt, lay = w.dims.dtype, w.layout
+    B, K, blen, L = w.batch, w.n_anchors, w.decode_block, lay.affix_len
+    bs = 16
+    flat, paged = WL.build(w), WL.build(w, block_size=bs)
+    g_bits, head_bits = W.draw_lm_head(w)
+    out = {}
+    for name, s in (("flat", flat), ("paged", paged)):
+        anchors, scores = s.batch.select_anchors(K)
+        x, m = s.batch.refresh(anchors, K)
+        ws = m["write_slots"].long()
+        kv = [(down_bits(s.batch.k_pools[n][ws]), down_bits(s.batch.v_pools[n][ws])) for n in range(w.dims.n_layers)]
+        plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=False)
+        h = D.decode_step(s.batch, plan, 0, m["read_slots"])
+        head = D.Head(up(g_bits, dt), up(head_bits, dt))
+        steps = D.decode_threshold_schedule(s.batch, head, plan, K, 0.9, anchors=anchors)
+        out[name] = dict(scores=down_bits(scores), anchors=anchors.cpu().numpy(), x=down_bits(x), kv=kv,
+                         h=down_bits(h), steps=steps, ids=s.batch.remap.cpu().numpy())
+    a, b = out["flat"], out["paged"]
+    for key in ("scores", "anchors", "x", "h", "ids"):
+        np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+    assert a["steps"] == b["steps"]
+    for (ka, va), (kb, vb) in zip(a["kv"], b["kv"]):
+        np.testing.assert_array_equal(ka, kb)
+        np.testing.assert_array_equal(va, vb)
+    R = K + lay.seq_len - L
+    st = paged.batch.pages.stats()
+    assert st["in_use"] == -(-L // bs) + B * -(-R // bs)
+    paged.batch.release_private()
+    assert paged.batch.pages.stats()["in_use"] == -(-L // bs)
+    torch.cuda.synchronize()

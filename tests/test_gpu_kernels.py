@@ -104,6 +104,22 @@ def test_build_maps(A, layout, B, k):
     assert got["row_pos"].numel() == B * R
 
 
+@pytest.mark.parametrize("layout,B,k,bs", [((192, 0, 128, 160, 32), 3, 26, 16), ((5120, 512, 4096, 4864, 256), 4, 819, 256),
+                                           ((2432, 0, 2048, 2176, 256), 2, 0, 100), ((300, 40, 200, 260, 40), 2, 200, 1)])
+def test_build_maps_paged(A, layout, B, k, bs):
+    S, ab, L, mb, G = layout
+    anchors = np.stack([np.sort(W.draw_permutation(L, seed=b)[:k]) for b in range(B)]).astype(np.int32)
+    R = k + S - L
+    n_sh, nb = -(-L // bs), -(-R // bs) + 1          # one spare block per request
+    ids = W.draw_permutation(n_sh + B * nb, seed=30 + bs)
+    shared, private = ids[:n_sh], ids[n_sh:]
+    lay = A.Layout(S, ab, L, mb, G, 0, 0, 0)
+    got = A.acache_build_maps_paged(lay, B, up_i32(anchors) if k else None, k, bs, up_i32(shared), up_i32(private), nb)
+    ref = O.build_maps_paged(S, ab, L, mb, G, anchors, bs, shared, private, nb)
+    for name, r in zip(["row_pos", "row_src", "write_slots", "read_slots", "q_rows"], ref):
+        np.testing.assert_array_equal(got[name].cpu().numpy(), r, err_msg=name)
+
+
 # ----------------------------------------------------------------------------- RMSNorm, linear
 
 @pytest.mark.parametrize("dtype,d", [("bf16", 4096), ("f32", 256), ("bf16", 3584)])

@@ -327,3 +327,40 @@ def test_hkvd_one_layer_uses_layer_zero():
     k0, v0 = O.layer_kv(layers[0], dims, req.x0[req.affix], req.pos[req.affix])
     np.testing.assert_allclose(s, ((k0 - sk[0]) ** 2).sum(axis=(1, 2)) + ((v0 - sv[0]) ** 2).sum(axis=(1, 2)),
                                rtol=1e-12)
+
+
+@pytest.mark.parametrize("layout", [(40, 0, 24, 32, 8), (40, 6, 20, 34, 6)])
+@pytest.mark.parametrize("k", [0, 5, "all"])
+def test_paged_maps(layout, k):
+    """Block-granular slots (Section 4.1).  With one slot per block and the
+    flat plan's slots as the tables the paged maps are the flat maps; with
+    larger blocks every request writes only inside its own blocks, every
+    non-anchor affix position reads its shared block, and rows, positions
+    and query rows do not depend on the slot plan."""
+    S, ab, L, mb, G = layout
+    rng = np.random.default_rng(41)
+    B = 3
+    k = L if k == "all" else k
+    anchors = np.stack([np.sort(rng.choice(L, size=k, replace=False)) for _ in range(B)]) if k else np.zeros((B, 0), int)
+    R = S - L + k
+    flat = O.build_maps(S, ab, L, mb, G, anchors, 0, L, S)
+    priv1 = np.array([L + b * S + i for b in range(B) for i in range(S)])
+    paged1 = O.build_maps_paged(S, ab, L, mb, G, anchors, 1, np.arange(L), priv1, S)
+    for a, p in zip(flat, paged1):
+        np.testing.assert_array_equal(a, p)
+    bs = 8
+    nb_shared, nb = -(-L // bs), -(-R // bs)
+    ids = rng.permutation(nb_shared + B * nb + 5)
+    shared, private = ids[:nb_shared], ids[nb_shared:nb_shared + B * nb]
+    row_pos, row_src, wslots, rslots, q_rows = O.build_maps_paged(S, ab, L, mb, G, anchors, bs, shared, private, nb)
+    for a, p in zip((flat[0], flat[1], flat[4]), (row_pos, row_src, q_rows)):
+        np.testing.assert_array_equal(a, p)
+    assert len(set(wslots.tolist())) == B * R
+    for b in range(B):
+        own = set(int(i) for i in private[b * nb:(b + 1) * nb])
+        assert all(int(s) // bs in own for s in wslots[b * R:(b + 1) * R])
+        for i, p in enumerate(row_pos[b * R:(b + 1) * R]):
+            assert rslots[b * S + p] == wslots[b * R + i]
+        for j in sorted(set(range(L)) - set(int(a) for a in anchors[b])):
+            s = rslots[b * S + ab + j]
+            assert s // bs == shared[j // bs] and s % bs == j % bs
