@@ -48,6 +48,10 @@ def parse():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="instead of the workload, run the row-gather kernel as a plain copy of MIB MiB "
                          "--steps times (the known-size reference for the HBM byte counters)")
+    ap.add_argument("--block-size", type=int, default=256,
+                    help="KV block size of the serving schedule's paged slot plan (0: flat plan)")
+    ap.add_argument("--tau", type=float, default=0.9,
+                    help="confidence threshold of the serving schedule's decode steps (negative: skip them)")
     return ap.parse_args()
 
 
@@ -127,7 +131,8 @@ def main():
     print(f"[bench] building {w.name}: layers {d.n_layers} batch {B} S {S} L {L} K {K} R {R}", file=sys.stderr,
           flush=True)
     t0 = time.time()
-    setup = WL.build(w, keep_host=not args.no_cpu)
+    setup = WL.build(w, keep_host=not args.no_cpu,
+                     block_size=(args.block_size or None) if w.decode_block else None)
     if w.decode_block:
         print(f"[bench] setup {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
         schedule_bench(args, w, setup)
@@ -343,14 +348,54 @@ def schedule_bench(args, w, setup):
             total += e0.elapsed_time(e1)
         return total / n, durs
 
+    paged = batch.pages is not None
+    kv = {}
+
+    def footprint(mode):
+        # blocks each mode holds: private tables sized for it alone, the peak
+        # the pool saw while it ran
+        if paged:
+            st = batch.pages.stats()
+            shared = len(batch.shared_host)
+            kv[mode] = dict(peak_blocks=st["peak"], shared_blocks=shared, private_blocks=st["peak"] - shared)
+
+    def fresh(mode):
+        if paged:
+            batch.release_private()
+            batch.pages.reset_peak()
+
     for _ in range(args.warmup):
         run("selective", 1)
     print("[bench] warmed up", file=sys.stderr, flush=True)
+    fresh("selective")
     ms_sel, _ = run("selective", args.steps)
+    footprint("selective")
     ids_sel = committed.cpu()
+    fresh("full")
     ms_full, _ = run("full", max(1, min(args.steps, 2)))
+    footprint("full")
     print("[bench] timed", file=sys.stderr, flush=True)
     _, durs = run("selective", 1, timer_kernel="gemm_gate_up")
+
+    decode = None
+    if args.tau >= 0:
+        # block decoding with confidence-threshold commits: one run per mode
+        decode = {"tau": args.tau}
+        for mode in ("selective", "full"):
+            batch.remap.copy_(ids0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            steps = D.decode_threshold_schedule(batch, head, plans[mode], K, args.tau)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3
+            decode[mode] = {"ms": round(ms, 1), "steps_per_block": steps,
+                            "committed_tokens_per_s": round(B * G / (ms * 1e-3), 1)}
+            print(f"[bench] threshold decode {mode}: {ms:.0f} ms, steps {steps}", file=sys.stderr, flush=True)
+        decode["speedup_vs_full"] = round(decode["full"]["ms"] / decode["selective"]["ms"], 3)
+        # decode steps alone: the schedule minus its refreshes, per step
+        n_steps = sum(decode["selective"]["steps_per_block"]) - n_blocks
+        if n_steps > 0:
+            decode["decode_step_ms"] = round((decode["selective"]["ms"] - ms_sel) / n_steps, 3)
 
     fl, _ = flops_model(w)
     dom = "gemm_gate_up"
@@ -378,12 +423,26 @@ def schedule_bench(args, w, setup):
                      "recomputed_tokens_per_s": round(B * w.rows_selective * n_blocks / (ms_sel * 1e-3), 1),
                      "mfma_util": round(sched_flops / (ms_sel * 1e-3) / 1e12 / peak, 4),
                      "committed_ids_checksum": int(ids_sel.to(torch.int64).sum())},
+        "threshold_decode": decode,
         "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved, 1), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None,
                      "launches_per_step": len(durs),
                      "flops_per_launch": round(dom_flops / max(len(durs), 1)),
                      "mean_launch_us": round(1e3 * sum(durs) / max(len(durs), 1), 2)},
     }
+    if paged:
+        GiB = float(1 << 30)
+        sel, full = kv["selective"], kv["full"]
+        result["kv_memory"] = {
+            "block_size": batch.bs,
+            "selective_peak_GiB": round(batch.kv_bytes(sel["peak_blocks"]) / GiB, 3),
+            "selective_blocks": sel,
+            # a system without ACache holds no shared affix region: its
+            # requests' private blocks are its whole KV
+            "full_recompute_peak_GiB": round(batch.kv_bytes(full["private_blocks"]) / GiB, 3),
+            "full_blocks": full,
+            "reduction": round(1 - sel["peak_blocks"] / full["private_blocks"], 4),
+        }
     if not args.no_cpu:
         cb = cpu_baseline(w, setup.host, args.cpu_seconds)
         # one request's schedule on the oracle: a probe (with top-K) and n_blocks refreshes for G tokens
