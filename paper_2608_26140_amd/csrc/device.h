@@ -29,6 +29,52 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// 16-byte global -> LDS copy (global_load_lds_dwordx4): lane l's 16 bytes
+// from g land at lds + 16 l, lds being uniform across the wave.  Completion
+// is counted by vmcnt.
+__device__ __forceinline__ void dma16(const void* g, char* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
+// Raw buffer resource over [base, base + bytes) (gfx9 descriptor: stride 0,
+// num_records in bytes).  Loads through it past the end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// 16-byte buffer -> LDS copy (buffer_load_dwordx4 ... lds): lane l's 16 bytes
+// at voff + soff land at lds + 16 l (lds uniform across the wave); soff is
+// a wave-uniform byte offset held in an SGPR.  Completion is counted by vmcnt.
+__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, char* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0, 0);
+}
+
+// s_waitcnt on one counter, the others left at their maximum (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+template <int N>
+__device__ __forceinline__ void wait_lgkmcnt() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt field");
+  __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+}
+
+// Workgroup barrier that orders LDS only.  __syncthreads() also waits for
+// every outstanding global load, which would include loads in flight to
+// LDS for later stages; those are tracked with explicit vmcnt waits.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Workgroup barrier with no fence: the caller has already waited (vmcnt /
+// lgkmcnt) for whatever LDS traffic the other waves must see.  The asm's
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // Order-preserving 32-bit key of an fp32 bit pattern: larger float, larger
 // key; -0 is folded onto +0 and NaN maps below -inf (key 0).
 __device__ __forceinline__ uint32_t order_key(uint32_t u) {

@@ -446,16 +446,8 @@ struct PvArgs {
   float* part_ml;  // [splits][rows][H][2] (running max in log2 units, sum)
 };
 
-__device__ __forceinline__ void dma16(const char* g, char* lds) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
 __device__ __forceinline__ v4i16 ds_read_tr16(const char* lds) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)lds);
-}
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) {
@@ -576,7 +568,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   }
   for (int t = t_lo; t < t_hi; ++t) {
     // tile t (and the slot indices of t + 1) have landed in this wave
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    wait_vmcnt<0>();
     fix_absent(t);
     lds_barrier();
     if (t + 1 < t_hi) {

@@ -8,14 +8,13 @@
 // and puts both halves of every rotary pair (columns d and d + 64 of one
 // head) in the same lane.
 //
-// Workgroup tile: 256 weight rows x 256 activation rows x 64 K, 8 waves
-// (2 along N x 4 along M, two per SIMD), each wave 128 x 64 = 4 x 2 MFMA
-// 32x32x16 tiles.  LDS is double buffered with one barrier per K step;
-// global loads for step k+1 are in flight while step k computes.  Rows are
-// padded to 144 bytes so the 16-lane groups of a ds_read_b128 hit distinct
-// banks.  Workgroups are renumbered so that each XCD (8 per chip, own L2)
-// receives a contiguous run of tiles with the M index fastest: the tiles
-// sharing one weight tile run on the same L2.
+// Workgroup tile: 256 weight rows x 256 activation rows, 8 waves (2 along
+// N x 4 along M, two per SIMD), each wave 128 x 64 = 4 x 2 MFMA 32x32x16
+// tiles.  The main loop is a ping-pong schedule over 32-wide K units, fed by
+// buffer -> LDS copies into a 4-unit ring (see the kernel).  Workgroups are
+// renumbered so that each XCD (8 per chip, own L2) receives a contiguous
+// run of tiles with the M index fastest: the tiles sharing one weight tile
+// run on the same L2.
 //
 // Schedules.  Data-parallel: one tile (or one K split of a tile) per
 // workgroup.  Stream-K, for the recompute's small row counts where the
@@ -260,15 +259,36 @@ __device__ __forceinline__ void init_inv_freq(double* inv_freq, const GemmParams
   if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
 }
 
+// Main loop: a ping-pong schedule.  The K range is cut into 32-wide units.
+// The waves form two groups, waves 0-3 and 4-7, one wave of each on every
+// SIMD; each wave alternates a memory phase (read its MFMA fragments of the
+// next unit from LDS, issue buffer -> LDS copies of the unit kPPAhead units
+// ahead) and a compute phase (16 MFMAs back to back), and group 1 runs one
+// phase behind group 0.  Every phase ends at a workgroup barrier, so while
+// one wave of a SIMD issues matrix work the other does its memory work.  LDS
+// holds a ring of kPPStages units, each 256 weight rows and 256 activation
+// rows of 64 bytes, written by buffer_load_dwordx4 ... lds (no staging
+// registers; the copies' addresses are an SGPR base and offset plus one
+// fixed VGPR offset per lane); chunk c (16 B) of row r is stored at
+// c ^ ((r >> 2) & 3) so that the 16 rows read by one quarter-wave hit
+// distinct banks.  The wave index is made uniform so that LDS addresses and
+// the group branches stay scalar.
+constexpr int kPPStages = 4;
+constexpr int kPPAhead = 3;
+constexpr int kPPRowB = 64;                // one 32-element unit row
+constexpr int kPPStageB = 512 * kPPRowB;   // 32 KB
+
 template <int EPI, class C>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
-  constexpr int BN = C::BN, BM = C::BM, BK = C::BK, LDK = C::LDK, FM = C::FM;
-  __shared__ __attribute__((aligned(16))) bf16 sW[2][BN * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sX[2][BM * LDK];
+  static_assert(C::BN == 256 && C::BM == 256 && C::WN == 2 && C::WM == 4 && C::BK == 64, "ping-pong tile");
+  constexpr int FM = C::FM;
+  __shared__ __attribute__((aligned(1024))) char ring[kPPStages * kPPStageB];
   __shared__ double inv_freq[64];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS addresses in SGPRs
   const int wn = wave % C::WN, wm = wave / C::WN;
+  const int grp = wave >> 2;
   const int F = p.N >> 1;
   const bf16* __restrict__ X = (const bf16*)p.X;
   const bf16* __restrict__ W = (const bf16*)p.W;
@@ -277,14 +297,21 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
   const int w = logical_block();
   if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
 
+  // copies: wave v fills rows [32 v, 32 v + 32) of both operands, 16 rows per
+  // instruction; lane l takes row 16 i + l / 4 and physical chunk l % 4
+  const int crow = lane >> 2;
+  const int cchunk = (lane & 3) ^ ((lane >> 4) & 3);
+  // fragment reads: row (lane % 32) of each 32-row fragment; the swizzle
+  // of every such row is ((lane % 32) >> 2) & 3
+  const int fsw = ((lane & 31) >> 2) & 3;
   const int arow = wn * 128 + (lane & 31);
-  const int brow = wm * C::WAVE_M + (lane & 31);
-  const int kofs = (lane >> 5) * 8;
-  constexpr int KS = BK / 16;
-  constexpr int NCH = C::W_CHUNKS + C::X_CHUNKS;
+  const int brow = 256 + wm * C::WAVE_M + (lane & 31);
+  const int cofs0 = ((0 + (lane >> 5)) ^ fsw) * 16;  // slice 0: chunks 0 / 1
+  const int cofs1 = ((2 + (lane >> 5)) ^ fsw) * 16;  // slice 1: chunks 2 / 3
+  const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(W, (uint32_t)p.N * (uint32_t)K * 2u);
+  const __amdgpu_buffer_rsrc_t xres = buffer_rsrc(X, (uint32_t)p.M * (uint32_t)K * 2u);
 
   f32x16 acc[4][FM];
-  // Work items: dp_rounds whole tiles, then this workgroup's stream-K range.
   int item = 0;
   int u = 0, u_end = 0;
   if (tm.sk_groups > 0 && w < tm.sk_groups) {
@@ -297,7 +324,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     bool sk = false;
     if (item < tm.dp_rounds) {
       t = item * tm.dp_stride + w;
-      kb = -1;  // from the split index
+      kb = -1;
       kn = 0;
       ++item;
     } else if (u < u_end) {
@@ -316,45 +343,40 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
       kb = sp * nk_tile / tm.splits;
       kn = (sp + 1) * nk_tile / tm.splits - kb;
     }
-    const int k0 = kb * BK;
-    const int nk = kn;
+    const int k0 = kb * C::BK;
+    const int U = 2 * kn;  // 32-wide units
 
-    // global -> register staging, 16 B chunks; 32-bit element offsets from
-    // uniform base pointers keep the address registers few
-    int woff[C::W_CHUNKS], xoff[C::X_CHUNKS];
-    int wdst[C::W_CHUNKS], xdst[C::X_CHUNKS];
+    // byte offsets from the uniform base pointers (operands stay below 2^31
+    // elements), so the copies use the SGPR-base + 32-bit offset form
+    uint32_t wsrc[2], xsrc[2];
 #pragma unroll
-    for (int i = 0; i < C::W_CHUNKS; ++i) {
-      const int q = tid + i * C::THREADS;
-      const int r = q / C::CPR, ch = q % C::CPR;
-      woff[i] = weight_row<EPI, BN>(nt, r, F) * K + k0 + ch * 8;
-      wdst[i] = r * LDK + ch * 8;
+    for (int i = 0; i < 2; ++i) {
+      const int r = wave * 32 + i * 16 + crow;
+      wsrc[i] = (uint32_t)(weight_row<EPI, 256>(nt, r, F) * K + k0 + cchunk * 8) * 2u;
+      xsrc[i] = (uint32_t)(min(mt * 256 + r, p.M - 1) * K + k0 + cchunk * 8) * 2u;
     }
+    auto issue = [&](int v) {
+      char* st = ring + (v % kPPStages) * kPPStageB;
+      const uint32_t ko = (uint32_t)v * 64u;  // uniform: the SGPR offset of the buffer loads
 #pragma unroll
-    for (int i = 0; i < C::X_CHUNKS; ++i) {
-      const int q = tid + i * C::THREADS;
-      const int r = q / C::CPR, ch = q % C::CPR;
-      const int m = min(mt * BM + r, p.M - 1);
-      xoff[i] = m * K + k0 + ch * 8;
-      xdst[i] = r * LDK + ch * 8;
-    }
-    // loads of K step kt+1 are issued at the start of step kt and stored to
-    // the other LDS buffer before its barrier
-    u32x4 stage[NCH];
-    auto load_global = [&](int kt) {
-      const int ko = kt * BK;
-#pragma unroll
-      for (int i = 0; i < C::W_CHUNKS; ++i) stage[i] = *reinterpret_cast<const u32x4*>(W + woff[i] + ko);
-#pragma unroll
-      for (int i = 0; i < C::X_CHUNKS; ++i)
-        stage[C::W_CHUNKS + i] = *reinterpret_cast<const u32x4*>(X + xoff[i] + ko);
+      for (int i = 0; i < 2; ++i) {
+        dma16_buf(wres, wsrc[i], ko, st + (wave * 32 + i * 16) * kPPRowB);
+        dma16_buf(xres, xsrc[i], ko, st + (256 + wave * 32 + i * 16) * kPPRowB);
+      }
     };
-    auto store_lds = [&](int buf) {
+    bf16x8 af[2][4], bfr[2][FM];
+    auto read_frags = [&](int v) {
+      const char* st = ring + (v % kPPStages) * kPPStageB;
 #pragma unroll
-      for (int i = 0; i < C::W_CHUNKS; ++i) *reinterpret_cast<u32x4*>(&sW[buf][wdst[i]]) = stage[i];
+      for (int a = 0; a < 4; ++a) {
+        af[0][a] = *reinterpret_cast<const bf16x8*>(st + (arow + a * 32) * kPPRowB + cofs0);
+        af[1][a] = *reinterpret_cast<const bf16x8*>(st + (arow + a * 32) * kPPRowB + cofs1);
+      }
 #pragma unroll
-      for (int i = 0; i < C::X_CHUNKS; ++i)
-        *reinterpret_cast<u32x4*>(&sX[buf][xdst[i]]) = stage[C::W_CHUNKS + i];
+      for (int b = 0; b < FM; ++b) {
+        bfr[0][b] = *reinterpret_cast<const bf16x8*>(st + (brow + b * 32) * kPPRowB + cofs0);
+        bfr[1][b] = *reinterpret_cast<const bf16x8*>(st + (brow + b * 32) * kPPRowB + cofs1);
+      }
     };
 
 #pragma unroll
@@ -364,60 +386,40 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-    // MFMA fragments are double buffered in registers: the reads of k slice
-    // s+1 are issued before the MFMAs of slice s, so LDS latency overlaps
-    // with matrix work instead of stalling the wave.
-    bf16x8 af[2][4], bfr[2][FM];
-    auto read_frags = [&](const bf16* w_s, const bf16* x_s, int s, int slot) {
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-        af[slot][a] = *reinterpret_cast<const bf16x8*>(w_s + (arow + a * 32) * LDK + s * 16 + kofs);
-#pragma unroll
-      for (int b = 0; b < FM; ++b)
-        bfr[slot][b] = *reinterpret_cast<const bf16x8*>(x_s + (brow + b * 32) * LDK + s * 16 + kofs);
-    };
-    auto mfma_step = [&](int slot) {
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[slot][a], bfr[slot][b], acc[a][b]);
-    };
-    // K step kt (LDS buffer kt&1): its first fragments are already in
-    // registers.  The MFMAs of its last 16-wide slice are issued after the
-    // barrier, behind the fragment reads of the next K step, so the wait for
-    // those reads overlaps matrix work.
-    auto step = [&](int kt, int par) {
-      const bf16* w_s = sW[par];
-      const bf16* x_s = sX[par];
-      const bool more = kt + 1 < nk;
-      if (more) load_global(kt + 1);
-#pragma unroll
-      for (int s = 0; s + 1 < KS; ++s) {
-        read_frags(w_s, x_s, s + 1, (s + 1) & 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_step(s & 1);
-        __builtin_amdgcn_sched_barrier(0);
+    // the previous item's stores and copies are complete, and every wave is
+    // past its last LDS read of the previous item
+    wait_vmcnt<0>();
+    lds_barrier();
+    issue(0);
+    if (U > 1) issue(1);
+    if (U > 2) issue(2);
+    if (U > 2) wait_vmcnt<8>(); else if (U > 1) wait_vmcnt<4>(); else wait_vmcnt<0>();
+    bare_barrier();
+    if (grp == 1) bare_barrier();  // group 1 runs one phase behind
+    for (int v = 0; v < U; ++v) {
+      // memory phase
+      __builtin_amdgcn_sched_barrier(0);
+      read_frags(v);
+      if (v + kPPAhead < U) issue(v + kPPAhead);
+      // this wave's copies of unit v + 1 are complete before the barrier
+      if (v + 1 < U) {
+        if (v + 3 < U) wait_vmcnt<8>(); else if (v + 2 < U) wait_vmcnt<4>(); else wait_vmcnt<0>();
       }
-      if (more) store_lds(par ^ 1);
-      __syncthreads();
-      if (more) read_frags(sW[par ^ 1], sX[par ^ 1], 0, KS & 1);
+      wait_lgkmcnt<0>();
       __builtin_amdgcn_sched_barrier(0);
-      mfma_step((KS - 1) & 1);
+      bare_barrier();
       __builtin_amdgcn_sched_barrier(0);
-    };
-
-    // every wave has finished reading LDS for the previous item
-    __syncthreads();
-    load_global(0);
-    store_lds(0);
-    __syncthreads();
-    read_frags(sW[0], sX[0], 0, 0);
-    int kt = 0;
-    for (; kt + 1 < nk; kt += 2) {
-      step(kt, 0);
-      step(kt + 1, 1);
+      // compute phase
+#pragma unroll
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+          for (int b = 0; b < FM; ++b) acc[a][b] = mfma32x32x16(af[s][a], bfr[s][b], acc[a][b]);
+      __builtin_amdgcn_sched_barrier(0);
+      bare_barrier();
     }
-    if (kt < nk) step(kt, 0);
+    if (grp == 0) bare_barrier();  // the phase in which group 1 computes the last unit
 
     if (sk && kn < nk_tile) {
       float* slot = tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4);
@@ -524,7 +526,7 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
     // tiles.  Stream-K with g workgroups on the e tiles left after r full
     // rounds: r whole tiles, ceil(e nk / g) steps, and the partial pieces
     // (at most e + g, each 256 KB written and read back once), which cost
-    // about 1/16 of a K step each at HBM speed.  With g >= e every range
+    // about 1/8 of a K step each (measured).  With g >= e every range
     // spans at most nk steps and so touches at most two tiles (the two
     // partial slots of a workgroup).
     const int G = std::min(cu_count(), kMaxSkGroups);
@@ -533,7 +535,7 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
     double best = dp_cost;
     int best_g = 0;
     for (int g = e; e > 0 && g <= G; ++g) {
-      const double cost = (double)r * nk + (double)((e * nk + g - 1) / g) + (e + g) / 16.0;
+      const double cost = (double)r * nk + (double)((e * nk + g - 1) / g) + (e + g) / 8.0;
       if (cost < best) {
         best = cost;
         best_g = g;
