@@ -317,6 +317,33 @@ acache_status acache_rerotate_k(const acache_dims* dims, const void* k_src, cons
                                 int64_t n_slots, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_layer_decode — one block of a block-decoding step (Section 4.3:
+ * queries for the current block only; Appendix C.1: store, then attend over
+ * the read-slot view), computed as acache_layer_recompute would for `batch`
+ * requests of rows_per_request rows each (row i of request b is row
+ * b * rows_per_request + i of x, pos, write_slots), with request b's logical
+ * keys given as two sets instead of one read-slot list:
+ *   - the shared affix: slot affix_slots[j] for every affix-local index
+ *     j < affix_len that is not one of anchors[b, 0 .. k) (the positions a
+ *     refresh recomputed are read from private slots);
+ *   - its private keys: private_slots[b * private_len .. + private_len), the
+ *     slots of the request's recomputed rows (anchors and request-specific
+ *     positions; the block's own rows are among them).
+ * The queries of all requests are taken together against the shared affix
+ * keys, so each affix K/V tile is read once per 128 queries rather than once
+ * per request; the request's private keys follow, and the two softmax
+ * partials are merged.  The result equals acache_layer_recompute over the
+ * same view up to fp32 summation order.  bf16 only (ACACHE_ERR_UNSUPPORTED
+ * otherwise); batch <= 64, affix_len <= 65536.  ws: at least
+ * acache_workspace_size(dims, batch * rows_per_request, batch, affix_len)
+ * bytes. */
+acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_weights* w, int32_t batch,
+                                  int32_t rows_per_request, void* x, const int32_t* pos, const int32_t* write_slots,
+                                  const int32_t* affix_slots, int32_t affix_len, const int32_t* anchors, int32_t k,
+                                  const int32_t* private_slots, int32_t private_len, void* k_pool, void* v_pool,
+                                  int64_t pool_ld, int64_t n_slots, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * acache_argmax_commit — the commit half of the predict-then-commit loop
  * (Section 3.1; the online loop of Section 4.3), in its greedy form: for
  * every row i < rows, out[i] = the index of the largest of x[i, 0 .. n),

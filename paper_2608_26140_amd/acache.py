@@ -84,6 +84,8 @@ def _load():
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
                                    P, P, P, P, P, P, I64, I64, ctypes.POINTER(ScoreArgs), P, SZ, P],
+        "acache_layer_decode": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), I32, I32, P, P, P, P, I32, P, I32,
+                                P, I32, P, P, I64, I64, P, SZ, P],
         "acache_rmsnorm": [ctypes.POINTER(Dims), P, P, P, I32, P],
         "acache_linear": [ctypes.POINTER(Dims), P, P, P, I32, I32, I32, I32, P, SZ, P],
     }
@@ -319,6 +321,25 @@ def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tenso
         ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
         _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],
         ctypes.byref(sa) if sa is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def acache_layer_decode(dims: Dims, weights, batch: int, rows_per_request: int, x: torch.Tensor, pos: torch.Tensor,
+                        write_slots: torch.Tensor, affix_slots: torch.Tensor, anchors: Optional[torch.Tensor], k: int,
+                        private_slots: torch.Tensor, private_len: int, k_pool: torch.Tensor, v_pool: torch.Tensor,
+                        ws: torch.Tensor, stream=None):
+    """One block of a decode step, in place on x [batch * rows_per_request, d]:
+    the shared affix keys (minus each request's anchors) and each request's
+    private slots [batch, private_len] form its view."""
+    for t, n in ((pos, "pos"), (write_slots, "write_slots"), (affix_slots, "affix_slots"),
+                 (private_slots, "private_slots")):
+        _dev_i32(t, n)
+    if anchors is not None:
+        _dev_i32(anchors, "anchors")
+    lw = weights if isinstance(weights, LayerWeights) else layer_weights(weights)
+    _check("acache_layer_decode", lib.acache_layer_decode(
+        ctypes.byref(dims), ctypes.byref(lw), batch, rows_per_request, _ptr(x), _ptr(pos), _ptr(write_slots),
+        _ptr(affix_slots), affix_slots.numel(), _ptr(anchors) if k > 0 else None, k, _ptr(private_slots), private_len,
+        _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0], _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def acache_rmsnorm(dims: Dims, x: torch.Tensor, g: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):

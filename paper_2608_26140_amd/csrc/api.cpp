@@ -492,6 +492,74 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
                    stream);
 }
 
+// bf16 block pieces shared by acache_layer_recompute and acache_layer_decode.
+// QKV projection of the normalised rows y with rotary embedding; Q to q, the
+// fresh K/V to their pool slots.
+static acache_status run_qkv_bf16(const acache_dims* dims, const acache_layer_weights* w, int M, const void* y,
+                                  void* q, const int32_t* pos, const int32_t* write_slots, void* k_pool,
+                                  void* v_pool, int64_t pool_ld, int64_t n_slots, float* part, hipStream_t stream) {
+  const int d = dims->d_model, H = dims->n_heads, Hkv = dims->n_kv_heads, dh = dims->head_dim;
+  GemmParams g = {};
+  g.X = y;
+  g.W = w->w_qkv;
+  g.M = M;
+  g.N = (H + 2 * Hkv) * dh;
+  g.K = d;
+  g.splits = 1;
+  g.q_out = q;
+  g.k_pool = k_pool;
+  g.v_pool = v_pool;
+  g.pool_ld = pool_ld;
+  g.n_slots = n_slots;
+  g.write_slots = write_slots;
+  g.pos = pos;
+  g.hq_cols = H * dh;
+  g.hkv_cols = Hkv * dh;
+  g.rope_base = dims->rope_base;
+  g.sk_ws = part;
+  LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
+  return ACACHE_OK;
+}
+
+// O projection + residual + RMSNorm, SwiGLU MLP + residual, from the
+// attention output o; x is updated in place, y and hb are scratch.
+static acache_status run_out_mlp_bf16(const acache_dims* dims, const acache_layer_weights* w, int M, void* x,
+                                      void* y, const void* o, void* hb, float* part, hipStream_t stream) {
+  const int d = dims->d_model, hq = dims->n_heads * dims->head_dim, F = dims->d_ff;
+  GemmParams g = {};
+  g.X = o;
+  g.W = w->w_o;
+  g.M = M;
+  g.N = d;
+  g.K = hq;
+  g.splits = gemm_bf16_splits(M, d, hq);
+  g.P = part;
+  LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
+  LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
+  GemmParams u = {};
+  u.X = y;
+  u.W = w->w_gate_up;
+  u.M = M;
+  u.N = 2 * F;
+  u.K = d;
+  u.splits = 1;
+  u.C = hb;
+  u.ldc = F;
+  u.sk_ws = part;
+  LAUNCH_T(ACACHE_K_GEMM_GATE_UP, stream, launch_gemm_bf16(EPI_SWIGLU, u, stream));
+  GemmParams dn = {};
+  dn.X = hb;
+  dn.W = w->w_down;
+  dn.M = M;
+  dn.N = d;
+  dn.K = F;
+  dn.splits = gemm_bf16_splits(M, d, F);
+  dn.P = part;
+  LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_PARTIAL, dn, stream));
+  LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+  return ACACHE_OK;
+}
+
 acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer_weights* w,
                                      const acache_ragged* rg, void* x, const int32_t* pos,
                                      const int32_t* write_slots, const int32_t* read_slots,
@@ -541,25 +609,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
 
   LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
   if (dims->dtype == ACACHE_BF16) {
-    GemmParams g = {};
-    g.X = y;
-    g.W = w->w_qkv;
-    g.M = M;
-    g.N = nqkv;
-    g.K = d;
-    g.splits = 1;
-    g.q_out = q;
-    g.k_pool = k_pool;
-    g.v_pool = v_pool;
-    g.pool_ld = pool_ld;
-    g.n_slots = n_slots;
-    g.write_slots = write_slots;
-    g.pos = pos;
-    g.hq_cols = hq;
-    g.hkv_cols = hkv;
-    g.rope_base = dims->rope_base;
-    g.sk_ws = at<float>(ws, p.part);
-    LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
+    st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, at<float>(ws, p.part), stream);
+    if (st != ACACHE_OK) return st;
     // the part region is idle between the QKV fixup and the O projection
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse,
                                                                 at<float>(ws, p.part), p.part_bytes, stream));
@@ -578,38 +629,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     if (st != ACACHE_OK) return st;
   }
   if (dims->dtype == ACACHE_BF16) {
-    float* part = at<float>(ws, p.part);
-    GemmParams g = {};
-    g.X = o;
-    g.W = w->w_o;
-    g.M = M;
-    g.N = d;
-    g.K = hq;
-    g.splits = gemm_bf16_splits(M, d, hq);
-    g.P = part;
-    LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
-    LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
-    GemmParams u = {};
-    u.X = y;
-    u.W = w->w_gate_up;
-    u.M = M;
-    u.N = 2 * F;
-    u.K = d;
-    u.splits = 1;
-    u.C = hb;
-    u.ldc = F;
-    u.sk_ws = part;
-    LAUNCH_T(ACACHE_K_GEMM_GATE_UP, stream, launch_gemm_bf16(EPI_SWIGLU, u, stream));
-    GemmParams dn = {};
-    dn.X = hb;
-    dn.W = w->w_down;
-    dn.M = M;
-    dn.N = d;
-    dn.K = F;
-    dn.splits = gemm_bf16_splits(M, d, F);
-    dn.P = part;
-    LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_PARTIAL, dn, stream));
-    LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+    st = run_out_mlp_bf16(dims, w, M, x, y, o, hb, at<float>(ws, p.part), stream);
+    if (st != ACACHE_OK) return st;
   } else {
     float* gu = at<float>(ws, p.gu);
     LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_f32((const float*)o, (const float*)w->w_o, (float*)x, d, M, d, hq, 1, stream));
@@ -619,6 +640,58 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_f32((const float*)hb, (const float*)w->w_down, (float*)x, d, M, d, F, 1, stream));
   }
   return ACACHE_OK;
+}
+
+acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_weights* w, int32_t batch,
+                                  int32_t rows_per_request, void* x, const int32_t* pos, const int32_t* write_slots,
+                                  const int32_t* affix_slots, int32_t affix_len, const int32_t* anchors, int32_t k,
+                                  const int32_t* private_slots, int32_t private_len, void* k_pool, void* v_pool,
+                                  int64_t pool_ld, int64_t n_slots, void* ws, size_t ws_bytes, hipStream_t stream) {
+  acache_status st = check_layer_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(dims->dtype == ACACHE_BF16, ACACHE_ERR_UNSUPPORTED);
+  CHECK(batch >= 0 && batch <= 64 && rows_per_request >= 0 && affix_len >= 0 && affix_len <= 65536, ACACHE_ERR_SHAPE);
+  CHECK(k >= 0 && k <= affix_len && private_len >= 0, ACACHE_ERR_SHAPE);
+  const int64_t M64 = (int64_t)batch * rows_per_request;
+  CHECK(M64 < ((int64_t)1 << 31), ACACHE_ERR_SHAPE);
+  const int M = (int)M64;
+  if (M == 0) return ACACHE_OK;
+  CHECK(private_len > 0 || affix_len > k, ACACHE_ERR_SHAPE);  // every request has keys
+  CHECK(w && x && pos && write_slots && k_pool && v_pool, ACACHE_ERR_NULL);
+  CHECK(w->attn_norm && w->w_qkv && w->w_o && w->mlp_norm && w->w_gate_up && w->w_down, ACACHE_ERR_NULL);
+  CHECK(affix_len == k || affix_slots, ACACHE_ERR_NULL);
+  CHECK(k == 0 || affix_len == k || anchors, ACACHE_ERR_NULL);
+  CHECK(private_len == 0 || private_slots, ACACHE_ERR_NULL);
+  const int d = dims->d_model, H = dims->n_heads, Hkv = dims->n_kv_heads, dh = dims->head_dim, F = dims->d_ff;
+  const int hq = H * dh, hkv = Hkv * dh, nqkv = (H + 2 * Hkv) * dh;
+  CHECK(pool_ld >= hkv && n_slots > 0, ACACHE_ERR_SHAPE);
+  CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK((int64_t)M * std::max({d, hq, F}) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK((int64_t)std::max({nqkv, 2 * F, d}) * std::max({d, hq, F}) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK(aligned16(x) && aligned16(k_pool) && aligned16(v_pool) && (pool_ld * 2) % 16 == 0, ACACHE_ERR_ALIGN);
+  CHECK(aligned16(w->attn_norm) && aligned16(w->w_qkv) && aligned16(w->w_o) && aligned16(w->mlp_norm) &&
+            aligned16(w->w_gate_up) && aligned16(w->w_down),
+        ACACHE_ERR_ALIGN);
+  const WsPlan p = plan_ws(dims, M, batch, affix_len);
+  CHECK(ws && ws_bytes >= p.total && aligned16(ws), ACACHE_ERR_WORKSPACE);
+  // the anchor masks live in the scoring region, which a decode step does not use
+  const size_t mask_bytes = (size_t)batch * ((affix_len + 63) / 64) * sizeof(uint64_t);
+  CHECK(mask_bytes <= (size_t)batch * H * std::max(affix_len, 1) * sizeof(float), ACACHE_ERR_WORKSPACE);
+  CHECK((size_t)M * H * (dh * 4 + 8) * 2 <= p.part_bytes, ACACHE_ERR_WORKSPACE);
+  void* y = at<char>(ws, p.y);
+  void* q = at<char>(ws, p.q);
+  void* o = at<char>(ws, p.o);
+  void* hb = at<char>(ws, p.h);
+  float* part = at<float>(ws, p.part);
+
+  LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
+  st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, part, stream);
+  if (st != ACACHE_OK) return st;
+  LAUNCH_T(ACACHE_K_ATTENTION, stream,
+           launch_attention_decode_bf16(batch, rows_per_request, H, Hkv, q, affix_slots, affix_len, anchors, k,
+                                        private_slots, private_len, k_pool, v_pool, pool_ld, n_slots, o,
+                                        at<uint64_t>(ws, p.colsum), part, p.part_bytes, stream));
+  return run_out_mlp_bf16(dims, w, M, x, y, o, hb, part, stream);
 }
 
 }  // extern "C"

@@ -88,6 +88,16 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,
                                  float* part, size_t part_bytes, hipStream_t s);
+// Decode-step attention: the queries of all requests against the shared
+// affix slots (each request's anchors masked out), then each request's
+// queries against its private slots, merged.  mask: [batch][ceil(L / 64)]
+// scratch.  Returns hipErrorInvalidValue if part_bytes cannot hold two
+// partial sets.
+hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int Hkv, const void* q,
+                                        const int32_t* affix_slots, int L, const int32_t* anchors, int k,
+                                        const int32_t* private_slots, int private_len, const void* k_pool,
+                                        const void* v_pool, int64_t pool_ld, int64_t n_slots, void* out,
+                                        uint64_t* mask, float* part, size_t part_bytes, hipStream_t s);
 int attention_tile_rows();
 // Per masked row and head, natural-log LSE over the affix keys.
 hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,

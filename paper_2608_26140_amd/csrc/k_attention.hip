@@ -444,12 +444,23 @@ struct PvArgs {
   int splits;
   float* part_o;   // [splits][rows][H][128] unnormalised O (splits > 1)
   float* part_ml;  // [splits][rows][H][2] (running max in log2 units, sum)
+  // decode passes: both write partials into one buffer of part_rows rows,
+  // this launch's splits at indices split_base ..
+  int partial;
+  int split_base;
+  int64_t part_rows;
+  // MASK kernels: bit i of key_mask[(row / mask_rows) * mask_tiles + t] drops
+  // key 64 t + i for that query row
+  const uint64_t* key_mask;
+  int mask_tiles;
+  int mask_rows;
 };
 
 __device__ __forceinline__ v4i16 ds_read_tr16(const char* lds) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)lds);
 }
 
+template <bool MASK>
 __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) {
   __shared__ __attribute__((aligned(1024))) char ring[2 * kStageB];
   const AttnArgs& a = pa.a;
@@ -496,6 +507,11 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
       if (qrow >= 0) v = *reinterpret_cast<const u32x4*>(qp + s2 * 16);
       qf[s2] = __builtin_bit_cast(bf16x8, v);
     }
+  }
+
+  const uint64_t* mrow = nullptr;  // this query row's key mask (MASK)
+  if constexpr (MASK) {
+    if (q_ok) mrow = pa.key_mask + (int64_t)((a.row_start[b] + qi) / pa.mask_rows) * pa.mask_tiles;
   }
 
   // this lane's 4 keys of a tile (one per load): key 16 wave + 4 i + lane / 16,
@@ -590,8 +606,11 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
       for (int s2 = 0; s2 < 8; ++s2) st[kb] = mfma32x32x16(kf[s2], qf[s2], st[kb]);
     }
     const int kt0 = t * kTileK;
+    // keys of this tile dropped for this query: past the end, or masked
+    uint64_t drop = kt0 + kTileK <= S ? 0ull : ~0ull << (S - kt0);
+    if constexpr (MASK) drop |= mrow ? mrow[t] : 0ull;
     float mx = -INFINITY;
-    if (kt0 + kTileK <= S) {
+    if (drop == 0ull) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -601,8 +620,8 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
-          st[kb][r] = key < S ? st[kb][r] : -INFINITY;
+          const int key = kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
+          st[kb][r] = (drop >> key) & 1ull ? -INFINITY : st[kb][r];
           mx = fmaxf(mx, st[kb][r]);
         }
     }
@@ -619,12 +638,15 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 #pragma unroll
         for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
     }
+    // with masks a query may not have met a key yet (running max -inf, all
+    // its logits -inf): exponentiate against 0 then, which gives zeros
+    const float m_use = MASK && m_run == -INFINITY ? 0.f : m_run;
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(st[kb][r], scale, -m_run));
+        const float e = __builtin_amdgcn_exp2f(fmaf(st[kb][r], scale, -m_use));
         st[kb][r] = e;
         psum += e;
       }
@@ -651,9 +673,11 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   const float l_tot = l_part + __shfl_xor(l_part, 32);
   if (!q_ok) return;
   const int64_t row = a.row_start[b] + qi;
-  if (splits > 1) {
+  if (splits > 1 || pa.partial) {
     // unnormalised partial: O^T register r of block d holds dims 32 d + 8 (r / 4) + 4 hl + r % 4
-    float* po = pa.part_o + (((int64_t)split * a.row_start[a.batch] + row) * a.H + h) * kDh;
+    const int64_t prow = pa.partial ? pa.part_rows : (int64_t)a.row_start[a.batch];
+    const int psplit = pa.split_base + split;
+    float* po = pa.part_o + (((int64_t)psplit * prow + row) * a.H + h) * kDh;
 #pragma unroll
     for (int d = 0; d < 4; ++d)
 #pragma unroll
@@ -662,7 +686,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
         *reinterpret_cast<f32x4*>(po + d * 32 + 8 * gq + 4 * hl) = v;
       }
     if (hl == 0) {
-      float* pm = pa.part_ml + (((int64_t)split * a.row_start[a.batch] + row) * a.H + h) * 2;
+      float* pm = pa.part_ml + (((int64_t)psplit * prow + row) * a.H + h) * 2;
       pm[0] = m_run;
       pm[1] = l_tot;
     }
@@ -779,12 +803,117 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   pa.splits = splits;
   pa.part_o = part;
   pa.part_ml = part ? part + (size_t)splits * rows * H * kDh : nullptr;
-  hipLaunchKernelGGL(attention_pv_kernel, dim3(tiles * H * splits), dim3(kPvThreads), 0, s, pa);
+  hipLaunchKernelGGL(attention_pv_kernel<false>, dim3(tiles * H * splits), dim3(kPvThreads), 0, s, pa);
   if (splits > 1) {
     const int64_t pairs = rows * H;
     hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s,
                        (const float*)pa.part_o, (const float*)pa.part_ml, splits, rows, H, (bf16*)out, lse);
   }
+  return hipGetLastError();
+}
+
+// Key masks of the decode step's shared pass: bit j % 64 of word
+// [b][j / 64] is set iff affix-local index j is one of request b's anchors
+// (those positions are read from the request's private slots instead).  One
+// workgroup per request builds its words in LDS.
+__global__ __launch_bounds__(256) void anchor_mask_kernel(const int32_t* __restrict__ anchors, int k, int L,
+                                                          int n_words, uint64_t* __restrict__ mask) {
+  __shared__ unsigned long long words[1024];
+  const int b = blockIdx.x;
+  for (int i = threadIdx.x; i < n_words; i += 256) words[i] = 0ull;
+  __syncthreads();
+  for (int i = threadIdx.x; i < k; i += 256) {
+    const int j = anchors[(int64_t)b * k + i];
+    if (j >= 0 && j < L) atomicOr(&words[j >> 6], 1ull << (j & 63));
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < n_words; i += 256) mask[(int64_t)b * n_words + i] = words[i];
+}
+
+// Decode-step attention over a view made of the shared affix (minus each
+// request's anchors) and each request's private keys.  Pass 1 takes the
+// queries of all requests together against the shared affix keys, so each
+// K/V tile of the affix is read once per 128 queries instead of once per
+// request; pass 2 takes each request's queries against its private keys.
+// Both write (O, max, sum) partials, which the merge kernel combines.
+hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int Hkv, const void* q,
+                                        const int32_t* affix_slots, int L, const int32_t* anchors, int k,
+                                        const int32_t* private_slots, int private_len, const void* k_pool,
+                                        const void* v_pool, int64_t pool_ld, int64_t n_slots, void* out,
+                                        uint64_t* mask, float* part, size_t part_bytes, hipStream_t s) {
+  const int64_t rows = (int64_t)batch * rows_per_req;
+  if (rows == 0) return hipSuccess;
+  const bool shared = L > k;  // some affix position is read from the shared slots
+  const int64_t per_split = rows * H * (kDh * 4 + 8);
+  const int q_tiles_all = (int)((rows + kPvTileQ - 1) / kPvTileQ);
+  const int q_tiles_req = (rows_per_req + kPvTileQ - 1) / kPvTileQ;
+  const int n_kt_shared = (L + kTileK - 1) / kTileK;
+  if ((size_t)per_split * (shared ? 2 : 1) > part_bytes) return hipErrorInvalidValue;
+  const int sp_priv = 1;
+  const int sp_shared =
+      shared ? attention_splits(q_tiles_all * H, n_kt_shared, rows, H, part_bytes - (size_t)per_split * sp_priv) : 0;
+  const int total = sp_shared + sp_priv;
+
+  auto common = [&](PvArgs& pa) {
+    AttnArgs& a = pa.a;
+    a.q = (const bf16*)q;
+    a.q_ld = (int64_t)H * kDh;
+    a.q_n_rows = rows;
+    a.q_idx = nullptr;
+    a.k_pool = (const bf16*)k_pool;
+    a.v_pool = (const bf16*)v_pool;
+    a.pool_ld = pool_ld;
+    a.n_slots = n_slots;
+    a.out = (bf16*)out;
+    a.lse = nullptr;
+    a.H = H;
+    a.Hkv = Hkv;
+    pa.part_o = part;
+    pa.part_ml = part + (size_t)total * rows * H * kDh;
+    pa.partial = 1;
+    pa.part_rows = rows;
+  };
+  if (shared) {
+    hipLaunchKernelGGL(anchor_mask_kernel, dim3(batch), dim3(256), 0, s, anchors, k, L, n_kt_shared, mask);
+    PvArgs pa = {};
+    common(pa);
+    AttnArgs& a = pa.a;
+    a.slots = affix_slots;
+    a.batch = 1;
+    a.row_start[0] = 0;
+    a.row_start[1] = (int)rows;
+    a.key_start[0] = 0;
+    a.key_start[1] = L;
+    a.key_len[0] = L;
+    a.tile_start[0] = 0;
+    a.tile_start[1] = q_tiles_all;
+    pa.splits = sp_shared;
+    pa.split_base = 0;
+    pa.key_mask = mask;
+    pa.mask_tiles = n_kt_shared;
+    pa.mask_rows = rows_per_req;
+    hipLaunchKernelGGL(attention_pv_kernel<true>, dim3(q_tiles_all * H * sp_shared), dim3(kPvThreads), 0, s, pa);
+  }
+  {
+    PvArgs pa = {};
+    common(pa);
+    AttnArgs& a = pa.a;
+    a.slots = private_slots;
+    a.batch = batch;
+    for (int b = 0; b <= batch; ++b) {
+      a.row_start[b] = b * rows_per_req;
+      a.key_start[b] = b * private_len;
+      a.tile_start[b] = b * q_tiles_req;
+    }
+    for (int b = 0; b < batch; ++b) a.key_len[b] = private_len;
+    pa.splits = sp_priv;
+    pa.split_base = sp_shared;
+    hipLaunchKernelGGL(attention_pv_kernel<false>, dim3(batch * q_tiles_req * H * sp_priv), dim3(kPvThreads), 0, s,
+                       pa);
+  }
+  const int64_t pairs = rows * H;
+  hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s, (const float*)part,
+                     (const float*)(part + (size_t)total * rows * H * kDh), total, rows, H, (bf16*)out, nullptr);
   return hipGetLastError();
 }
 

@@ -339,21 +339,37 @@ def _on(stream):
     return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
 
-def decode_step(batch: AffixBatch, plan: DecodePlan, blk: int, read_slots: torch.Tensor, stream=None):
+def decode_step(batch: AffixBatch, plan: DecodePlan, blk: int, m: dict, anchors: Optional[torch.Tensor] = None,
+                split_shared: bool = True, stream=None):
     """One decoding step of block ``blk`` (Section 4.3, Appendix C.1): the
     block's rows, embedded from the current token ids, go through every
     layer with queries for those rows only; each layer writes their fresh
     K/V to the rows' private slots, then attention reads each request's
-    whole logical context through ``read_slots`` (the refresh's read-slot
-    map).  Returns the block's last-layer rows [B * block_len, d]."""
+    whole logical context, the view the refresh (maps ``m``, anchor set
+    ``anchors``) left.  With split_shared (bf16) the view is read as the
+    shared affix minus the anchors, taken for all requests together, plus
+    each request's private slots (acache_layer_decode); otherwise through
+    the read-slot map.  Returns the block's last-layer rows [B * block_len, d]."""
     B, blen = batch.B, plan.block_len
+    h = A.acache_gather_rows(batch.x_src, plan.pos[blk], batch.remap, stream=stream)
+    wslots = plan.write_slots(batch, blk)
+    k = plan.k
+    if split_shared and batch.model.dims.dtype == A.ACACHE_BF16:
+        R = batch.rows_per_request(k)
+        anc = plan.anchors if plan.full else anchors
+        if anc is None and k > 0:
+            raise ValueError("the shared/private split needs the refresh's anchor set")
+        for i in range(batch.model.n_layers):
+            A.acache_layer_decode(batch.model.dims, batch.model.lw[i], B, blen, h, plan.row_pos[blk], wslots,
+                                  batch.affix_slots, anc, k, m["write_slots"], R, batch.k_pools[i],
+                                  batch.v_pools[i], batch.ws, stream=stream)
+        return h
     cu_rows = [b * blen for b in range(B + 1)]
     cu_keys = [b * batch.S for b in range(B + 1)]
-    h = A.acache_gather_rows(batch.x_src, plan.pos[blk], batch.remap, stream=stream)
     for i in range(batch.model.n_layers):
         A.acache_layer_recompute(batch.model.dims, batch.model.lw[i], cu_rows, cu_keys, h, plan.row_pos[blk],
-                                 plan.write_slots(batch, blk), read_slots, batch.k_pools[i], batch.v_pools[i],
-                                 batch.ws, stream=stream)
+                                 wslots, m["read_slots"], batch.k_pools[i], batch.v_pools[i], batch.ws,
+                                 stream=stream)
     return h
 
 
@@ -418,6 +434,6 @@ def decode_threshold_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k
             step += 1
             if done >= n or (max_steps is not None and step >= max_steps):
                 break
-            h = decode_step(batch, plan, blk, m["read_slots"], stream=stream)
+            h = decode_step(batch, plan, blk, m, anchors, stream=stream)
         steps.append(step)
     return steps

@@ -131,7 +131,8 @@ def _block_ids(w, base_ids, blk, seed):
     return ids
 
 
-def test_decode_steps_against_oracle(serve):
+@pytest.mark.parametrize("split_shared", [True, False], ids=["shared-private", "read-slots"])
+def test_decode_steps_against_oracle(serve, split_shared):
     import torch
     from paper_2608_26140_amd import driver as D
     w, s, layers, dims, sk, sv, anchors = serve
@@ -167,7 +168,7 @@ def test_decode_steps_against_oracle(serve):
         keep = np.ones(s.batch.n_slots, dtype=bool)
         keep[wslots.cpu().numpy()] = False
         before = [down_bits(p[torch.from_numpy(np.flatnonzero(keep)).cuda()]) for p in s.batch.k_pools]
-        h = D.decode_step(s.batch, plan, blk, m["read_slots"])
+        h = D.decode_step(s.batch, plan, blk, m, up_i32(anchors), split_shared=split_shared)
         y = D.A.acache_rmsnorm(s.batch.model.dims, h, head.norm_g)
         logits = D.A.acache_linear(s.batch.model.dims, y, head.w)
         conf = torch.empty(B * blen, dtype=torch.float32, device="cuda")
@@ -285,7 +286,7 @@ def test_paged_matches_flat():
         ws = m["write_slots"].long()
         kv = [(down_bits(s.batch.k_pools[n][ws]), down_bits(s.batch.v_pools[n][ws])) for n in range(w.dims.n_layers)]
         plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=False)
-        h = D.decode_step(s.batch, plan, 0, m["read_slots"])
+        h = D.decode_step(s.batch, plan, 0, m, anchors)
         head = D.Head(up(g_bits, dt), up(head_bits, dt))
         steps = D.decode_threshold_schedule(s.batch, head, plan, K, 0.9, anchors=anchors)
         out[name] = dict(scores=down_bits(scores), anchors=anchors.cpu().numpy(), x=down_bits(x), kv=kv,
@@ -303,3 +304,29 @@ def test_paged_matches_flat():
     paged.batch.release_private()
     assert paged.batch.pages.stats()["in_use"] == -(-L // bs)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("full", [False, True], ids=["selective", "full"])
+def test_shared_private_split_matches_read_slots(serve, full):
+    """acache_layer_decode (shared affix for all requests, anchors masked,
+    then private slots) against acache_layer_recompute over the read-slot
+    view: the same attention up to fp32 summation order.  In full mode every
+    affix token is an anchor and the shared pass is empty."""
+    import torch
+    from paper_2608_26140_amd import driver as D
+    w, s, layers, dims, sk, sv, anchors = serve
+    dt, lay = w.dims.dtype, w.layout
+    B, K, blen = w.batch, w.n_anchors, w.decode_block
+    plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=full)
+    a = plan.anchors if full else up_i32(anchors)
+    outs, pools = [], []
+    for split in (True, False):
+        s.batch.remap.copy_(up_i32(s.host["ids"].reshape(-1)))
+        x, m = s.batch.refresh(a, plan.k)
+        h = D.decode_step(s.batch, plan, 2, m, a, split_shared=split)
+        ws = plan.write_slots(s.batch, 2).long()
+        outs.append(down(h))
+        pools.append([down(s.batch.k_pools[n][ws]) for n in range(w.dims.n_layers)])
+    assert_close(outs[0], outs[1], dt, "block rows")
+    for n in range(w.dims.n_layers):
+        assert_close(pools[0][n], pools[1][n], dt, f"fresh K layer {n}")
