@@ -111,6 +111,27 @@ def test_layer_recompute_validation(A):
                                       4096, 100, None, p, 1 << 30, None) == 2
 
 
+def test_layer_decode_validation(A):
+    lib = A.lib
+    dims = A.make_dims(4096, 32, 32, 128, 12288, "bf16")
+    w = A.LayerWeights(16, 16, 16, 16, 16, 16)
+    p = ctypes.c_void_p(16)
+
+    def call(dims=dims, batch=2, rows=8, L=64, k=8, plen=20, ws_bytes=1 << 30, anchors=p, priv=p):
+        return lib.acache_layer_decode(ctypes.byref(dims), ctypes.byref(w), batch, rows, p, p, p, p, L, anchors, k,
+                                       priv, plen, p, p, 4096, 1000, p, ws_bytes, None)
+    # fp32 is not implemented by this entry point
+    assert call(dims=A.make_dims(256, 4, 4, 64, 688, "f32")) == 4
+    assert call(batch=65) == 2                 # batch above 64
+    assert call(k=65) == 2                     # more anchors than affix positions
+    assert call(L=70000, k=8) == 2             # affix beyond 65536
+    assert call(L=8, k=8, plen=0) == 2         # a request without any key
+    assert call(anchors=None) == 1             # anchors needed when 0 < k < L
+    assert call(priv=None) == 1                # private slots needed when private_len > 0
+    assert call(ws_bytes=100) == 5             # workspace too small
+    assert call(batch=0) == 0 and call(rows=0) == 0   # nothing to do
+
+
 def test_offset_limits(A):
     """Operands whose element offsets would not fit 32 bits are rejected
     before any launch."""

@@ -330,3 +330,40 @@ def test_shared_private_split_matches_read_slots(serve, full):
     assert_close(outs[0], outs[1], dt, "block rows")
     for n in range(w.dims.n_layers):
         assert_close(pools[0][n], pools[1][n], dt, f"fresh K layer {n}")
+
+
+def test_decode_step_gqa_infix_against_oracle():
+    """A decode step on a grouped-KV model (H_kv = 1) with the affix in the
+    middle of the context: both attention paths against the oracle's step
+    over the refresh's view, for a block of the masked span."""
+    import torch
+    from paper_2608_26140_amd import driver as D
+    from paper_2608_26140_amd import workload as WL
+    w = W.get_config("mini-gqa-infix")
+    s = WL.build(w)
+    dt, lay = w.dims.dtype, w.layout
+    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    layers = oracle_layers(w, s.host)
+    dims = oracle_dims(w)
+    sk64, sv64 = oracle_stale(w, s.host, layers)
+    sk, sv = [], []
+    for n in range(len(layers)):
+        kb = W.bf16_bits_from_f32(sk64[n].astype(np.float32))
+        vb = W.bf16_bits_from_f32(sv64[n].astype(np.float32))
+        s.batch.k_pools[n][:L] = up(kb.reshape(L, -1), dt)
+        s.batch.v_pools[n][:L] = up(vb.reshape(L, -1), dt)
+        sk.append(O.from_bits(kb, dt))
+        sv.append(O.from_bits(vb, dt))
+    anchors = np.stack([O.topk_anchors(O.probe(layers, dims, oracle_request(w, s.host, b), sk, sv).scores, K)
+                        for b in range(B)])
+    blen, blk = 8, 3
+    plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=False)
+    emb = O.from_bits(s.host["embedding"], dt)
+    positions = np.arange(lay.mask_begin + blk * blen, lay.mask_begin + (blk + 1) * blen)
+    for split in (True, False):
+        x, m = s.batch.refresh(up_i32(anchors), K)
+        h = down(D.decode_step(s.batch, plan, blk, m, up_i32(anchors), split_shared=split))
+        for b in range(B):
+            ref = O.selective_refresh(layers, dims, oracle_request(w, s.host, b), anchors[b], sk, sv)
+            xb = O.decode_step(layers, dims, ref.views_k, ref.views_v, emb[s.host["ids"][b][positions]], positions)
+            assert_close(h[b * blen:(b + 1) * blen], xb, dt, f"split={split} request {b}")

@@ -8,7 +8,10 @@ use that cache (rounded to storage) as the common input.  For a sampled
 request the oracle then checks, against the GPU run over the whole batch:
 the probe's Eq. 4-5 scores, the Eq. 6 anchor set (overlap and tie band), and
 the selective refresh (output rows and the fresh K/V in the request's
-private slots) with the oracle's anchors.
+private slots) with the oracle's anchors.  The serving workload also runs a
+decode step of its first block for the whole batch (the shared affix for all
+requests together, anchors masked, then the private slots), checked for a
+sampled request against the oracle's step over the same view.
 """
 
 import numpy as np
@@ -76,3 +79,33 @@ def test_layer0_full_size(case):
     kv = w.dims.n_kv_heads, w.dims.head_dim
     assert_close(down(s.batch.k_pools[0][wslots]).reshape(R, *kv), ref.views_k[0][ref.rows], dt, "fresh K")
     assert_close(down(s.batch.v_pools[0][wslots]).reshape(R, *kv), ref.views_v[0][ref.rows], dt, "fresh V")
+
+
+def test_decode_step_full_size(case):
+    w, s, layer0, dims, sk, sv = case
+    if not w.decode_block:
+        pytest.skip("no decode schedule for this workload")
+    from paper_2608_26140_amd import driver as D
+    dt, lay = w.dims.dtype, w.layout
+    B, K, blen = w.batch, w.n_anchors, w.decode_block
+    b = B // 2
+    req = oracle_request(w, s.host, b)
+    ref_anchors = O.topk_anchors(O.probe([layer0], dims, req, sk, sv).scores, K)
+    anchors, _ = s.batch.select_anchors(K)
+    a = down(anchors).astype(np.int32)
+    a[b] = ref_anchors
+    a_dev = up_i32(a)
+    x, m = s.batch.refresh(a_dev, K)
+    plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=False)
+    h = D.decode_step(s.batch, plan, 0, m, a_dev)
+    # the oracle's view after the refresh, layer 0: K/V are row-local there, so
+    # the recomputed rows' entries are layer_kv of their inputs and the other
+    # affix positions keep the shared cache
+    rows = O.selective_rows(req, ref_anchors)
+    vk = np.empty((lay.seq_len, w.dims.n_kv_heads, w.dims.head_dim))
+    vv = np.empty_like(vk)
+    vk[req.affix], vv[req.affix] = sk[0], sv[0]
+    vk[rows], vv[rows] = O.layer_kv(layer0, dims, req.x0[rows], req.pos[rows])
+    positions = np.arange(lay.mask_begin, lay.mask_begin + blen)
+    xb = O.decode_step([layer0], dims, [vk], [vv], req.x0[positions], positions)
+    assert_close(down(h[b * blen:(b + 1) * blen]), xb, dt, f"decode step rows request {b}")
