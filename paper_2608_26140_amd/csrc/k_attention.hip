@@ -616,12 +616,13 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kb][r]);
     } else {
+      // register r of key block kb holds key 32 kb + 16 (r / 8) + 8 hl + r % 8
+      const uint32_t dw[2] = {(uint32_t)drop >> (8 * hl), (uint32_t)(drop >> 32) >> (8 * hl)};
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
-          st[kb][r] = (drop >> key) & 1ull ? -INFINITY : st[kb][r];
+          st[kb][r] = (dw[kb] >> (16 * (r >> 3) + (r & 7))) & 1u ? -INFINITY : st[kb][r];
           mx = fmaxf(mx, st[kb][r]);
         }
     }
@@ -785,11 +786,13 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   a.H = H;
   a.Hkv = Hkv;
   a.batch = rg.batch;
-  int tiles = 0, max_kt = 0;
   for (int b = 0; b <= rg.batch; ++b) {
     a.row_start[b] = rg.cu_rows[b];
     a.key_start[b] = rg.cu_keys[b];
   }
+  const int64_t rows = rg.cu_rows[rg.batch];
+  if (rows == 0) return hipSuccess;
+  int tiles = 0, max_kt = 0;
   for (int b = 0; b < rg.batch; ++b) {
     a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
     a.tile_start[b] = tiles;
@@ -798,7 +801,6 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   }
   a.tile_start[rg.batch] = tiles;
   if (tiles == 0) return hipSuccess;
-  const int64_t rows = rg.cu_rows[rg.batch];
   const int splits = part ? attention_splits(tiles * H, max_kt, rows, H, part_bytes) : 1;
   pa.splits = splits;
   pa.part_o = part;
