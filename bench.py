@@ -76,6 +76,10 @@ def flops_model(w):
     out = {}
     for phase, m in rows.items():
         out[phase] = {k: v * m * N for k, v in per_row.items()}
+    # the probe's last layer computes only what its score reads: the masked
+    # rows' queries (acache_layer_score under the affix-only normalisation)
+    out["probe"] = {k: v * B * P * (N - 1) for k, v in per_row.items()}
+    out["probe"]["gemm_qkv"] += 2 * d.d_model * hq * B * G
     score = 2 * 2 * G * L * hq * B * N
     out["probe"]["score_lse"] = score / 2
     out["probe"]["score_colsum"] = score / 2
@@ -90,12 +94,16 @@ def bytes_model(w):
     lay = w.layout
     B, S, L, N = w.batch, lay.seq_len, lay.affix_len, d.n_layers
     es = 2 if d.dtype == "bf16" else 4
-    rows = B * lay.n_nonaffix + B * w.rows_selective  # probe + refresh rows
+    P, R, G = B * lay.n_nonaffix, B * w.rows_selective, B * lay.mask_len
+    hq = d.n_heads * d.head_dim
+    rows = P + R  # probe + refresh rows
+    # the probe's last layer: its masked rows gathered and normalised, and
+    # their queries written by the split-K reduction (timed as "residual")
     return {
-        "gather": 2 * rows * d.d_model * es,
-        "rmsnorm": 2 * rows * d.d_model * es * N,
+        "gather": 2 * rows * d.d_model * es + 2 * G * d.d_model * es,
+        "rmsnorm": 2 * (P * (N - 1) + R * N + G) * d.d_model * es,
         # after the O projection: x in, x out, RMSNorm y out; after down: x in, x out
-        "residual": 5 * rows * d.d_model * es * N,
+        "residual": 5 * (P * (N - 1) + R * N) * d.d_model * es + G * hq * es,
         "topk": B * L * 4 + B * w.n_anchors * 4,
         "maps": 4 * (3 * rows + 2 * B * S),
         "score_reduce": 4 * (d.n_heads + 1) * B * L * N,
@@ -150,6 +158,9 @@ def main():
     def select():
         batch.select_anchors(K)
 
+    def select_full_probe():
+        batch.select_anchors(K, full_probe=True)
+
     anchors_fixed, _ = batch.select_anchors(K)
 
     def refresh():
@@ -179,7 +190,7 @@ def main():
     torch.cuda.synchronize()
 
     # per-kernel breakdown (one armed step per kernel, outside the timed region)
-    launches_per_step = 2 * d.n_layers + 4
+    launches_per_step = 4 * d.n_layers + 4
     breakdown = {}
     for kname in ([] if args.only_step else KERNELS):
         kt = A.KernelTimer(kname, 4 * launches_per_step)
@@ -218,9 +229,10 @@ def main():
         shift_dir[0] = -shift_dir[0]
 
     if args.only_step:
-        ms_select = ms_refresh = ms_full = ms_drop = ms_shift = ms_hkvd = None
+        ms_select = ms_refresh = ms_full = ms_drop = ms_shift = ms_hkvd = ms_select_fp = None
     else:
         ms_select = timed(select, args.steps)
+        ms_select_fp = timed(select_full_probe, args.steps)
         ms_refresh = timed(refresh, args.steps)
         ms_full = timed(full, args.steps)
         ms_drop = timed(refresh_dropna, args.steps)
@@ -275,7 +287,8 @@ def main():
                    "kv_heads": d.n_kv_heads, "d_ff": d.d_ff},
         "latency_ms_per_request": round(ms_step / B, 4),
         "phases_ms": None if ms_refresh is None else {
-            "select_anchors": round(ms_select, 4), "selective_refresh": round(ms_refresh, 4),
+            "select_anchors": round(ms_select, 4), "select_anchors_full_last_layer": round(ms_select_fp, 4),
+            "selective_refresh": round(ms_refresh, 4),
             "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4),
             "shift_affix": round(ms_shift, 4), "select_anchors_hkvd": round(ms_hkvd, 4)},
         "shift_affix_GB_per_s": None if ms_shift is None else round(

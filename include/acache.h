@@ -284,6 +284,33 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
                                      hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_layer_score — the probe's last layer (Section 3.2, Eq. 4-5) reduced
+ * to what its score reads.  After the last probe layer nothing consumes the
+ * probe rows' hidden states (the refresh recomputes every row from its
+ * layer-0 input), so only this layer's Eq. 4 weights matter: with
+ * y = RMSNorm(x), the masked rows' queries y W_q^T rotated at pos, against
+ * the affix keys, added into score->scores exactly as acache_layer_recompute
+ * with the same score arguments does (equal up to fp32 summation order in
+ * the query projection).
+ *   ACACHE_NORM_AFFIX: only the masked rows (score->q_rows) are normalised
+ *     and projected, to queries only; the pools are not written.
+ *   ACACHE_NORM_FULL: the normaliser is each masked row's LSE over all of
+ *     its request's keys, so every row's Q, K and V are projected, K and V
+ *     stored at write_slots, and the attention runs over read_slots (its
+ *     output is discarded).
+ * x [rows, d] is read only.  score is required.  write_slots, read_slots
+ * and v_pool may be NULL under ACACHE_NORM_AFFIX.  The weights read are
+ * attn_norm and w_qkv (its first H*d_h rows under AFFIX); the others may be
+ * NULL.  Other arguments, layouts, the workspace and the errors are those
+ * of acache_layer_recompute; bf16 under AFFIX also needs d_ff >= d_model.
+ * No masked rows or L == 0: no-op. */
+acache_status acache_layer_score(const acache_dims* dims, const acache_layer_weights* w, const acache_ragged* rg,
+                                 const void* x, const int32_t* pos, const int32_t* write_slots,
+                                 const int32_t* read_slots, void* k_pool, void* v_pool, int64_t pool_ld,
+                                 int64_t n_slots, const acache_score_args* score, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * acache_kv_deviation — the score of the CacheBlend-style selector the paper
  * compares against (appendix, "CacheBlend-Style Anchor Selection"): each
  * affix token's KV deviation between the shared affix-only cache and the

@@ -84,6 +84,8 @@ def _load():
         "acache_attention": [ctypes.POINTER(Dims), ctypes.POINTER(Ragged), P, P, P, P, I64, I64, P, P, P],
         "acache_layer_recompute": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
                                    P, P, P, P, P, P, I64, I64, ctypes.POINTER(ScoreArgs), P, SZ, P],
+        "acache_layer_score": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), ctypes.POINTER(Ragged),
+                               P, P, P, P, P, P, I64, I64, ctypes.POINTER(ScoreArgs), P, SZ, P],
         "acache_layer_decode": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), I32, I32, P, P, P, P, I32, P, I32,
                                 P, I32, P, P, I64, I64, P, SZ, P],
         "acache_rmsnorm": [ctypes.POINTER(Dims), P, P, P, I32, P],
@@ -321,6 +323,27 @@ def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tenso
         ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
         _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],
         ctypes.byref(sa) if sa is not None else None, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def acache_layer_score(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tensor, pos: torch.Tensor,
+                       write_slots: Optional[torch.Tensor], read_slots: Optional[torch.Tensor], k_pool: torch.Tensor,
+                       v_pool: Optional[torch.Tensor], ws: torch.Tensor, score: dict, stream=None):
+    """The probe's last layer reduced to its score: adds this layer's Eq. 4-5
+    contribution into score["scores"]; x is not modified.  write_slots,
+    read_slots and v_pool are needed only under ACACHE_NORM_FULL."""
+    _dev_i32(pos, "pos")
+    for t, n in ((write_slots, "write_slots"), (read_slots, "read_slots")):
+        if t is not None:
+            _dev_i32(t, n)
+    lw = weights if isinstance(weights, LayerWeights) else layer_weights(weights)
+    rg, keep = _ragged(cu_rows, cu_keys)
+    cq = _i32(score["cu_q"])
+    sa = ScoreArgs(score["q_rows"].data_ptr(), cq, score["affix_slots"].data_ptr(), score["affix_slots"].numel(),
+                   score.get("norm", ACACHE_NORM_AFFIX), score["scores"].data_ptr())
+    _check("acache_layer_score", lib.acache_layer_score(
+        ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
+        _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0], ctypes.byref(sa), _ptr(ws),
+        ws.numel(), _stream(stream)))
 
 
 def acache_layer_decode(dims: Dims, weights, batch: int, rows_per_request: int, x: torch.Tensor, pos: torch.Tensor,

@@ -136,15 +136,17 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
     // largest splits x rows over every row count up to `rows`, so one
     // workspace serves any smaller call (splits change only at row-tile
     // boundaries, every one of which is a multiple of 128 rows)
-    size_t part_rows = 0;
+    size_t part_elems = 0;
     for (int t = 1; (t - 1) * 128 < rows; ++t) {
       const int m = std::min(rows, t * 128);
       const int sp = std::max(gemm_bf16_splits(m, d->d_model, (int)hq), gemm_bf16_splits(m, d->d_model, d->d_ff));
-      part_rows = std::max(part_rows, (size_t)sp * (size_t)m);
+      part_elems = std::max(part_elems, (size_t)sp * (size_t)m * d->d_model);
+      // the query-only projection of the probe's last layer
+      part_elems = std::max(part_elems, (size_t)gemm_bf16_splits(m, (int)hq, d->d_model) * (size_t)m * hq);
     }
     // split-K partials of the O / down projections and the stream-K pieces
     // of the QKV / gate-up projections are never live at the same time
-    w.part_bytes = std::max(part_rows * d->d_model * sizeof(float), gemm_bf16_sk_ws_bytes());
+    w.part_bytes = std::max(part_elems * sizeof(float), gemm_bf16_sk_ws_bytes());
     w.part = take(w.part_bytes);
     w.qkv = w.gu = 0;
   } else {
@@ -640,6 +642,95 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_f32((const float*)hb, (const float*)w->w_down, (float*)x, d, M, d, F, 1, stream));
   }
   return ACACHE_OK;
+}
+
+acache_status acache_layer_score(const acache_dims* dims, const acache_layer_weights* w, const acache_ragged* rg,
+                                 const void* x, const int32_t* pos, const int32_t* write_slots,
+                                 const int32_t* read_slots, void* k_pool, void* v_pool, int64_t pool_ld,
+                                 int64_t n_slots, const acache_score_args* score, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  acache_status st = check_layer_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(score, ACACHE_ERR_NULL);
+  Ragged r;
+  st = make_ragged(rg, r);
+  if (st != ACACHE_OK) return st;
+  const int M = r.cu_rows[r.batch];
+  const int L = score->affix_len;
+  CHECK(L >= 0 && L <= 65536, ACACHE_ERR_SHAPE);
+  CHECK(score->norm == ACACHE_NORM_AFFIX || score->norm == ACACHE_NORM_FULL, ACACHE_ERR_UNSUPPORTED);
+  st = check_cu(score->cu_q, r.batch);
+  if (st != ACACHE_OK) return st;
+  CHECK(score->cu_q[r.batch] <= M, ACACHE_ERR_SHAPE);
+  const int Mq = score->cu_q[r.batch];
+  if (M == 0 || L == 0 || Mq == 0) return ACACHE_OK;  // nothing to add
+  CHECK(score->q_rows && score->affix_slots && score->scores, ACACHE_ERR_NULL);
+  const bool full = score->norm == ACACHE_NORM_FULL;
+  CHECK(w && x && pos && k_pool, ACACHE_ERR_NULL);
+  CHECK(w->attn_norm && w->w_qkv, ACACHE_ERR_NULL);
+  // the full softmax's normaliser needs every row's keys and the attention
+  CHECK(!full || (write_slots && read_slots && v_pool), ACACHE_ERR_NULL);
+  const int d = dims->d_model, H = dims->n_heads, Hkv = dims->n_kv_heads, dh = dims->head_dim;
+  const int hq = H * dh, hkv = Hkv * dh, nqkv = (H + 2 * Hkv) * dh;
+  CHECK(pool_ld >= hkv && n_slots > 0, ACACHE_ERR_SHAPE);
+  CHECK(n_slots * pool_ld < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK((int64_t)M * std::max(d, hq) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  CHECK((int64_t)nqkv * std::max(d, hq) < ((int64_t)1 << 31), ACACHE_ERR_UNSUPPORTED);
+  const int64_t es = (int64_t)elem_size(dims->dtype);
+  CHECK(aligned16(x) && aligned16(k_pool) && (pool_ld * es) % 16 == 0, ACACHE_ERR_ALIGN);
+  CHECK(!full || aligned16(v_pool), ACACHE_ERR_ALIGN);
+  CHECK(aligned16(w->attn_norm) && aligned16(w->w_qkv), ACACHE_ERR_ALIGN);
+  const WsPlan p = plan_ws(dims, M, r.batch, L);
+  CHECK(ws && ws_bytes >= p.total && aligned16(ws), ACACHE_ERR_WORKSPACE);
+  void* y = at<char>(ws, p.y);
+  void* q = at<char>(ws, p.q);
+  float* lse = full ? at<float>(ws, p.lse) : nullptr;
+
+  if (dims->dtype == ACACHE_BF16 && !full) {
+    // the masked rows only: gather, normalise, project to queries (split-K
+    // over the whole chip), then sum the splits and rotate
+    CHECK(dims->d_ff >= d, ACACHE_ERR_UNSUPPORTED);  // the gathered rows sit in the MLP region
+    void* xq = at<char>(ws, p.h);
+    LAUNCH_T(ACACHE_K_GATHER, stream, launch_gather_rows(x, (int64_t)d * 2, M, score->q_rows, nullptr, 0, Mq, d * 2,
+                                                         xq, (int64_t)d * 2, stream));
+    LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, xq, w->attn_norm, y, Mq, d, dims->rms_eps, stream));
+    GemmParams g = {};
+    g.X = y;
+    g.W = w->w_qkv;  // the query rows come first
+    g.M = Mq;
+    g.N = hq;
+    g.K = d;
+    g.splits = gemm_bf16_splits(Mq, hq, d);
+    g.P = at<float>(ws, p.part);
+    CHECK((size_t)g.splits * Mq * hq * sizeof(float) <= p.part_bytes, ACACHE_ERR_WORKSPACE);
+    LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
+    LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_q_rotary_reduce(g.P, g.splits, Mq, H, score->q_rows, pos,
+                                                               dims->rope_base, q, M, stream));
+  } else {
+    LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
+    if (dims->dtype == ACACHE_BF16) {
+      st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, at<float>(ws, p.part),
+                        stream);
+      if (st != ACACHE_OK) return st;
+      LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld,
+                                                                  n_slots, at<char>(ws, p.o), lse,
+                                                                  at<float>(ws, p.part), p.part_bytes, stream));
+    } else {
+      float* qkv = at<float>(ws, p.qkv);
+      LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));
+      // the pools are written only when the attention reads them (with
+      // n_slots 0 no slot is valid and nothing is stored; pos then stands
+      // in for the slot list, which the affix-only reading does not need)
+      LAUNCH(launch_rope_scatter_f32(qkv, M, H, Hkv, dh, pos, dims->rope_base, (float*)q, full ? write_slots : pos,
+                                     (float*)k_pool, (float*)v_pool, pool_ld, full ? n_slots : 0, stream));
+      if (full)
+        LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_f32(r, H, Hkv, dh, (const float*)q, read_slots,
+                                                                   (const float*)k_pool, (const float*)v_pool, pool_ld,
+                                                                   n_slots, at<float>(ws, p.o), lse, stream));
+    }
+  }
+  return run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots, score->affix_slots, L,
+                   score->norm, lse, score->scores, at<float>(ws, p.lse_aff), at<float>(ws, p.colsum), stream);
 }
 
 acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_weights* w, int32_t batch,

@@ -38,6 +38,10 @@ hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y
 // y[m] = RMSNorm(x[m]) * g.
 hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M, int d,
                                   const void* g, void* y, float eps, hipStream_t s);
+// q[rows[i]] = rotary(sum_s part[s][i], pos[rows[i]]) for the n rows of bf16
+// queries with head_dim 128 (fp32 partials [splits][n][H * 128]).
+hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
+                                  const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s);
 // scores[b][j] += sum_h part[b][h][j]
 hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
                               hipStream_t s);

@@ -8,10 +8,11 @@
 // and puts both halves of every rotary pair (columns d and d + 64 of one
 // head) in the same lane.
 //
-// Workgroup tile: 256 weight rows x 256 activation rows, 8 waves (2 along
-// N x 4 along M, two per SIMD), each wave 128 x 64 = 4 x 2 MFMA 32x32x16
-// tiles.  The main loop is a ping-pong schedule over 32-wide K units, fed by
-// buffer -> LDS copies into a 4-unit ring (see the kernel).  Workgroups are
+// Workgroup tile: 256 weight rows x 256 (or 128) activation rows, 8 waves
+// (2 along N x 4 along M, two per SIMD), each wave 128 x 64 (or 128 x 32)
+// = 4 x 2 (4 x 1) MFMA 32x32x16 tiles.  The main loop is a ping-pong
+// schedule over 32-wide K units, fed by buffer -> LDS copies into a ring of
+// units (see the kernel).  Workgroups are
 // renumbered so that each XCD (8 per chip, own L2) receives a contiguous
 // run of tiles with the M index fastest: the tiles sharing one weight tile
 // run on the same L2.
@@ -262,28 +263,49 @@ __device__ __forceinline__ void init_inv_freq(double* inv_freq, const GemmParams
 // Main loop: a ping-pong schedule.  The K range is cut into 32-wide units.
 // The waves form two groups, waves 0-3 and 4-7, one wave of each on every
 // SIMD; each wave alternates a memory phase (read its MFMA fragments of the
-// next unit from LDS, issue buffer -> LDS copies of the unit kPPAhead units
-// ahead) and a compute phase (16 MFMAs back to back), and group 1 runs one
+// next unit from LDS, issue buffer -> LDS copies of the unit kAhead units
+// ahead) and a compute phase (MFMAs back to back), and group 1 runs one
 // phase behind group 0.  Every phase ends at a workgroup barrier, so while
 // one wave of a SIMD issues matrix work the other does its memory work.  LDS
-// holds a ring of kPPStages units, each 256 weight rows and 256 activation
+// holds a ring of kAhead + 1 units, each 256 weight rows and BM activation
 // rows of 64 bytes, written by buffer_load_dwordx4 ... lds (no staging
 // registers; the copies' addresses are an SGPR base and offset plus one
-// fixed VGPR offset per lane); chunk c (16 B) of row r is stored at
-// c ^ ((r >> 2) & 3) so that the 16 rows read by one quarter-wave hit
-// distinct banks.  The wave index is made uniform so that LDS addresses and
-// the group branches stay scalar.
-constexpr int kPPStages = 4;
-constexpr int kPPAhead = 3;
-constexpr int kPPRowB = 64;                // one 32-element unit row
-constexpr int kPPStageB = 512 * kPPRowB;   // 32 KB
+// fixed VGPR offset per lane); the copy of unit v + kAhead reuses the slot of
+// unit v - 1, which both groups finished reading before the barrier that
+// opened this phase.  Chunk c (16 B) of row r is stored at c ^ ((r >> 2) & 3)
+// so that the 16 rows read by one quarter-wave hit distinct banks.  The wave
+// index is made uniform so that LDS addresses and the group branches stay
+// scalar.  Weights are streamed from HBM once per launch, so the depth of
+// the ring is what hides HBM latency when few workgroups run.
+constexpr int kPPRowB = 64;  // one 32-element unit row
+
+// Waits until at most n units of this wave's copies (NCP each) are in flight.
+template <int NCP, int MAXN>
+__device__ __forceinline__ void wait_units(int n) {
+  if constexpr (MAXN == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (n >= MAXN) wait_vmcnt<NCP * MAXN>();
+    else wait_units<NCP, MAXN - 1>(n);
+  }
+}
 
 template <int EPI, class C>
 __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, TileMap tm) {
-  static_assert(C::BN == 256 && C::BM == 256 && C::WN == 2 && C::WM == 4 && C::BK == 64, "ping-pong tile");
+  static_assert(C::BN == 256 && (C::BM == 256 || C::BM == 128) && C::WN == 2 && C::WM == 4 && C::BK == 64,
+                "ping-pong tile");
   constexpr int FM = C::FM;
-  __shared__ __attribute__((aligned(1024))) char ring[kPPStages * kPPStageB];
-  __shared__ double inv_freq[64];
+  constexpr int XI = C::BM / 128;               // activation copies per wave and unit
+  constexpr int NCP = 2 + XI;                   // copies per wave and unit
+  constexpr int kStageB = (256 + C::BM) * kPPRowB;
+  // ring depth: copies run kAhead units ahead of the fragment reads (deeper
+  // rings measured slower, also with weights streamed from HBM)
+  constexpr int kStages = 4;
+  constexpr int kAhead = kStages - 1;
+  __shared__ __attribute__((aligned(1024))) char ring[kStages * kStageB];
+  // the rotary frequencies live in the ring, written once the main loop of
+  // an item is over
+  double* inv_freq = reinterpret_cast<double*>(ring);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS addresses in SGPRs
@@ -295,10 +317,10 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
   const int K = p.K;
   const int nk_tile = tm.nk;
   const int w = logical_block();
-  if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
 
-  // copies: wave v fills rows [32 v, 32 v + 32) of both operands, 16 rows per
-  // instruction; lane l takes row 16 i + l / 4 and physical chunk l % 4
+  // copies: wave v fills weight rows [32 v, 32 v + 32) and activation rows
+  // [16 XI v, 16 XI v + 16 XI), 16 rows per instruction; lane l takes row
+  // 16 i + l / 4 and physical chunk l % 4
   const int crow = lane >> 2;
   const int cchunk = (lane & 3) ^ ((lane >> 4) & 3);
   // fragment reads: row (lane % 32) of each 32-row fragment; the swizzle
@@ -348,25 +370,28 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
 
     // byte offsets from the uniform base pointers (operands stay below 2^31
     // elements), so the copies use the SGPR-base + 32-bit offset form
-    uint32_t wsrc[2], xsrc[2];
+    uint32_t wsrc[2], xsrc[XI];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int r = wave * 32 + i * 16 + crow;
       wsrc[i] = (uint32_t)(weight_row<EPI, 256>(nt, r, F) * K + k0 + cchunk * 8) * 2u;
-      xsrc[i] = (uint32_t)(min(mt * 256 + r, p.M - 1) * K + k0 + cchunk * 8) * 2u;
+    }
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const int r = wave * 16 * XI + i * 16 + crow;
+      xsrc[i] = (uint32_t)(min(mt * C::BM + r, p.M - 1) * K + k0 + cchunk * 8) * 2u;
     }
     auto issue = [&](int v) {
-      char* st = ring + (v % kPPStages) * kPPStageB;
+      char* st = ring + (v % kStages) * kStageB;
       const uint32_t ko = (uint32_t)v * 64u;  // uniform: the SGPR offset of the buffer loads
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        dma16_buf(wres, wsrc[i], ko, st + (wave * 32 + i * 16) * kPPRowB);
-        dma16_buf(xres, xsrc[i], ko, st + (256 + wave * 32 + i * 16) * kPPRowB);
-      }
+      for (int i = 0; i < 2; ++i) dma16_buf(wres, wsrc[i], ko, st + (wave * 32 + i * 16) * kPPRowB);
+#pragma unroll
+      for (int i = 0; i < XI; ++i) dma16_buf(xres, xsrc[i], ko, st + (256 + wave * 16 * XI + i * 16) * kPPRowB);
     };
     bf16x8 af[2][4], bfr[2][FM];
     auto read_frags = [&](int v) {
-      const char* st = ring + (v % kPPStages) * kPPStageB;
+      const char* st = ring + (v % kStages) * kStageB;
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         af[0][a] = *reinterpret_cast<const bf16x8*>(st + (arow + a * 32) * kPPRowB + cofs0);
@@ -390,21 +415,19 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
     // past its last LDS read of the previous item
     wait_vmcnt<0>();
     lds_barrier();
-    issue(0);
-    if (U > 1) issue(1);
-    if (U > 2) issue(2);
-    if (U > 2) wait_vmcnt<8>(); else if (U > 1) wait_vmcnt<4>(); else wait_vmcnt<0>();
+#pragma unroll
+    for (int v = 0; v < kAhead; ++v)
+      if (v < U) issue(v);
+    wait_units<NCP, kAhead - 1>(min(U, kAhead) - 1);  // unit 0 is in LDS
     bare_barrier();
     if (grp == 1) bare_barrier();  // group 1 runs one phase behind
     for (int v = 0; v < U; ++v) {
       // memory phase
       __builtin_amdgcn_sched_barrier(0);
       read_frags(v);
-      if (v + kPPAhead < U) issue(v + kPPAhead);
+      if (v + kAhead < U) issue(v + kAhead);
       // this wave's copies of unit v + 1 are complete before the barrier
-      if (v + 1 < U) {
-        if (v + 3 < U) wait_vmcnt<8>(); else if (v + 2 < U) wait_vmcnt<4>(); else wait_vmcnt<0>();
-      }
+      if (v + 1 < U) wait_units<NCP, kAhead - 1>(min(U - 1, v + kAhead) - (v + 1));
       wait_lgkmcnt<0>();
       __builtin_amdgcn_sched_barrier(0);
       bare_barrier();
@@ -420,6 +443,11 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
       bare_barrier();
     }
     if (grp == 0) bare_barrier();  // the phase in which group 1 computes the last unit
+    // every wave is past its last read of the ring, and every copy has landed
+    if constexpr (EPI == EPI_QKV) {
+      init_inv_freq(inv_freq, p, tid);
+      lds_barrier();
+    }
 
     if (sk && kn < nk_tile) {
       float* slot = tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4);
@@ -466,17 +494,26 @@ __global__ __launch_bounds__(64) void gemm_bf16_fixup(GemmParams p, TileMap tm) 
 
 }  // namespace
 
-// 8 waves (2 per SIMD) on a 256 x 256 tile, each wave 128 x 64; BK 64.
+// 8 waves (2 per SIMD), each wave 128 weight rows x BM / 4 activation rows;
+// BK 64.  The 256 x 256 tile reads 0.75 KB of LDS per MFMA; the 256 x 128
+// tile (1.25 KB per MFMA) doubles the tile count for row counts that would
+// leave CUs idle.
 using GemmCfg = Cfg<256, 256, 2, 4, 64>;
+using GemmCfgH = Cfg<256, 128, 2, 4, 64>;
 
 namespace {
+
+// Time of one K step of a 256 x 128 tile relative to one of a 256 x 256 tile
+// at the same number of busy CUs (measured 0.65 - 0.71: the half tile reads
+// more LDS bytes per MFMA).
+constexpr double kHalfStep = 0.7;
 
 int cu_count() {
   static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return kMaxSkGroups;
   int n = cached[dev].load(std::memory_order_relaxed);
-  if (n <= 0) {
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
       n = kMaxSkGroups;
     cached[dev].store(n, std::memory_order_relaxed);
@@ -484,14 +521,19 @@ int cu_count() {
   return n;
 }
 
-// K splits for the split-K partial epilogue.  Cost in K steps of one
-// workgroup, on kMaxSkGroups CUs (fixed, so the workspace plan and the
-// launch agree on any device): ceil(T s / G) rounds of ceil(nk / s) steps,
-// plus s fp32 slices of M x N written here and read back by the reduction,
-// about M N 8 / 9.5e6 K steps each at HBM speed.  Splits need not divide
-// nk; each keeps at least kMinSkSteps steps.
 template <class C>
-int splits_for(int M, int N, int K) {
+constexpr double step_cost() {
+  return C::BM == 256 ? 1.0 : kHalfStep;
+}
+
+// K splits for the split-K partial epilogue, and their cost in 256 x 256 K
+// steps of one workgroup, on kMaxSkGroups CUs (fixed, so the workspace plan
+// and the launch agree on any device): ceil(T s / G) rounds of ceil(nk / s)
+// steps, plus s fp32 slices of M x N written here and read back by the
+// reduction, about M N 8 / 9.5e6 K steps each at HBM speed.  Splits need not
+// divide nk; each keeps at least kMinSkSteps steps.
+template <class C>
+int splits_for(int M, int N, int K, double* cost_out) {
   const int tiles = ((M + C::BM - 1) / C::BM) * (N / C::BN);
   const int nk = K / C::BK;
   const int G = kMaxSkGroups;
@@ -499,40 +541,57 @@ int splits_for(int M, int N, int K) {
   int best = 1;
   double best_cost = 1e30;
   for (int s = 1; s <= kMaxSplits && nk / s >= kMinSkSteps; ++s) {
-    const double cost = (double)((tiles * s + G - 1) / G) * ((nk + s - 1) / s) + s * slice;
+    const double cost =
+        (double)((tiles * s + G - 1) / G) * ((nk + s - 1) / s) * step_cost<C>() + s * slice;
     if (cost < best_cost) {
       best_cost = cost;
       best = s;
     }
   }
+  if (cost_out) *cost_out = best_cost;
   return best;
 }
 
+// The split-K epilogue's tile: a function of the shape only, so that the
+// caller's split count (which sizes its partial buffer) and the launch agree.
+bool partial_half(int M, int N, int K) {
+  double c256 = 0, c128 = 0;
+  splits_for<GemmCfg>(M, N, K, &c256);
+  splits_for<GemmCfgH>(M, N, K, &c128);
+  return c128 < c256;
+}
+
+struct Plan {
+  TileMap tm;
+  int grid;
+  int sk_tiles;
+  double cost;  // in 256 x 256 K steps of one workgroup
+};
+
 template <class C>
-hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
-  TileMap tm = {};
+Plan plan_cfg(GemmEpi epi, const GemmParams& p) {
+  Plan pl = {};
+  TileMap& tm = pl.tm;
   tm.m_tiles = (p.M + C::BM - 1) / C::BM;
   tm.n_tiles = epi == EPI_SWIGLU ? (p.N / 2) / (C::BN / 2) : p.N / C::BN;
   tm.splits = epi == EPI_PARTIAL ? p.splits : 1;
   tm.nk = p.K / C::BK;
   const int tiles = tm.m_tiles * tm.n_tiles * tm.splits;
   const int nk = tm.nk;
-  int grid = tiles;
+  const int G = std::min(cu_count(), kMaxSkGroups);
+  pl.grid = tiles;
   tm.dp_rounds = 1;
   tm.dp_stride = tiles;
-  int sk_tiles = 0;
+  const double dp_cost = (double)((tiles + G - 1) / G) * ((nk + tm.splits - 1) / tm.splits);
+  double best = dp_cost;
   if (epi != EPI_PARTIAL && p.sk_ws && nk >= kMinSkSteps) {
-    // Cost in K steps of one workgroup.  Data-parallel: ceil(T / G) whole
-    // tiles.  Stream-K with g workgroups on the e tiles left after r full
-    // rounds: r whole tiles, ceil(e nk / g) steps, and the partial pieces
-    // (at most e + g, each 256 KB written and read back once), which cost
-    // about 1/8 of a K step each (measured).  With g >= e every range
-    // spans at most nk steps and so touches at most two tiles (the two
-    // partial slots of a workgroup).
-    const int G = std::min(cu_count(), kMaxSkGroups);
+    // Stream-K with g workgroups on the e tiles left after r full rounds:
+    // r whole tiles, ceil(e nk / g) steps, and the partial pieces (at most
+    // e + g, each written and read back once), which cost about 1/8 of a K
+    // step each (measured).  With g >= e every range spans at most nk steps
+    // and so touches at most two tiles (the two partial slots of a
+    // workgroup).
     const int r = tiles / G, e = tiles % G;
-    const double dp_cost = (double)((tiles + G - 1) / G) * nk;
-    double best = dp_cost;
     int best_g = 0;
     for (int g = e; e > 0 && g <= G; ++g) {
       const double cost = (double)r * nk + (double)((e * nk + g - 1) / g) + (e + g) / 8.0;
@@ -548,20 +607,27 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
       tm.sk_units = e * nk;
       tm.sk_groups = best_g;
       tm.sk_part = p.sk_ws;
-      grid = r > 0 ? G : best_g;
-      sk_tiles = e;
+      pl.grid = r > 0 ? G : best_g;
+      pl.sk_tiles = e;
     }
   }
-  const dim3 block(C::THREADS);
+  pl.cost = best * step_cost<C>();
+  return pl;
+}
+
+template <class C>
+hipError_t launch_plan(GemmEpi epi, const GemmParams& p, const Plan& pl, hipStream_t s) {
+  const TileMap& tm = pl.tm;
+  const dim3 grid(pl.grid), block(C::THREADS);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), dim3(grid), block, 0, s, p, tm); break;
-    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), dim3(grid), block, 0, s, p, tm); break;
-    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), dim3(grid), block, 0, s, p, tm); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), dim3(grid), block, 0, s, p, tm); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), dim3(grid), block, 0, s, p, tm); break;
+    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
+    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
+    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
   }
-  if (sk_tiles > 0) {
-    const dim3 fgrid(sk_tiles * C::WAVES), fblock(64);
+  if (pl.sk_tiles > 0) {
+    const dim3 fgrid(pl.sk_tiles * C::WAVES), fblock(64);
     switch (epi) {
       case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
       case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
@@ -575,14 +641,24 @@ hipError_t launch_cfg(GemmEpi epi, const GemmParams& p, hipStream_t s) {
 
 }  // namespace
 
-int gemm_bf16_splits(int M, int N, int K) { return splits_for<GemmCfg>(M, N, K); }
+int gemm_bf16_splits(int M, int N, int K) {
+  return partial_half(M, N, K) ? splits_for<GemmCfgH>(M, N, K, nullptr) : splits_for<GemmCfg>(M, N, K, nullptr);
+}
 
 size_t gemm_bf16_sk_ws_bytes() {
+  // the 256 x 256 tile's pieces are the larger
   return (size_t)kMaxSkGroups * 2 * GemmCfg::WAVES * 64 * GemmCfg::ACC4 * 4 * sizeof(float);
 }
 
 hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s) {
-  return launch_cfg<GemmCfg>(epi, p, s);
+  bool half;
+  if (epi == EPI_PARTIAL) {
+    half = partial_half(p.M, p.N, p.K);
+  } else {
+    half = plan_cfg<GemmCfgH>(epi, p).cost < plan_cfg<GemmCfg>(epi, p).cost;
+  }
+  return half ? launch_plan<GemmCfgH>(epi, p, plan_cfg<GemmCfgH>(epi, p), s)
+              : launch_plan<GemmCfg>(epi, p, plan_cfg<GemmCfg>(epi, p), s);
 }
 
 }  // namespace acache

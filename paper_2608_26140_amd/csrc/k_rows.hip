@@ -135,6 +135,52 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, c
   for (int i = threadIdx.x; i < d; i += 256) yr[i] = from_f32<T>(to_f32(xr[i]) * inv * to_f32(g[i]));
 }
 
+// ---------------------------------------------------------------- split-K reduce + rotary (queries only)
+// The probe's last layer projects only the masked rows' queries, as fp32
+// split-K partials [splits][n][H * 128].  One thread per (row, head, 4 of
+// the 64 rotary pairs): the splits are summed in order, the pairs (d, d + 64)
+// are rotated by the row's position exactly as the Q/K/V projection's
+// epilogue does (fp64 angle, rotary_sincos), and the row is written to
+// q[rows[i]] (rows outside [0, q_n_rows) are skipped).
+__global__ __launch_bounds__(256) void q_rotary_reduce_kernel(const float* __restrict__ part, int splits, int n,
+                                                              int H, const int32_t* __restrict__ rows,
+                                                              const int32_t* __restrict__ pos, float rope_base,
+                                                              bf16* __restrict__ q, int64_t q_n_rows) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)n * H * 16) return;
+  const int i = (int)(t / (H * 16));
+  const int rem = (int)(t - (int64_t)i * H * 16);
+  const int h = rem >> 4, d0 = (rem & 15) * 4;
+  const int64_t hq = (int64_t)H * 128;
+  const int64_t r = rows[i];
+  if (r < 0 || r >= q_n_rows) return;
+  float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int sp = 0; sp < splits; ++sp) {
+    const float* pp = part + ((int64_t)sp * n + i) * hq + h * 128 + d0;
+    const f32x4 a = *reinterpret_cast<const f32x4*>(pp);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(pp + 64);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      lo[j] += a[j];
+      hi[j] += b[j];
+    }
+  }
+  const double ang_pos = (double)pos[r];
+  const double l2b = log2((double)rope_base);
+  bf16x4 olo, ohi;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int d = d0 + j;
+    float sn, cs;
+    rotary_sincos(ang_pos * exp2(-(2.0 * d / 128.0) * l2b), &sn, &cs);
+    olo[j] = (bf16)(lo[j] * cs - hi[j] * sn);
+    ohi[j] = (bf16)(hi[j] * cs + lo[j] * sn);
+  }
+  bf16* dst = q + r * hq + h * 128 + d0;
+  *reinterpret_cast<bf16x4*>(dst) = olo;
+  *reinterpret_cast<bf16x4*>(dst + 64) = ohi;
+}
+
 // ---------------------------------------------------------------- split-K reduce + residual (+ RMSNorm)
 // One workgroup per row; each thread keeps up to 4 chunks of 8 columns in
 // registers between the residual sum and the normalisation (d <= 8192).
@@ -496,6 +542,15 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
                                   const void* g, void* y, float eps, hipStream_t s) {
   hipLaunchKernelGGL(reduce_residual_kernel, dim3(M), dim3(256), 0, s, (bf16*)x, part, splits, M, d,
                      (const bf16*)g, (bf16*)y, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
+                                  const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t threads = (int64_t)n * H * 16;
+  hipLaunchKernelGGL(q_rotary_reduce_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, part, splits,
+                     n, H, rows, pos, rope_base, (bf16*)q, q_n_rows);
   return hipGetLastError();
 }
 

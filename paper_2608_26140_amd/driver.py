@@ -156,25 +156,31 @@ class AffixBatch:
         return [(b0, min(self.B, b0 + per)) for b0 in range(0, self.B, per)]
 
     def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None,
-                   drop_non_anchor: bool = False, upto: Optional[int] = None, stream=None):
+                   drop_non_anchor: bool = False, upto: Optional[int] = None, score_last_only: bool = False,
+                   stream=None):
         """drop_non_anchor: attention reads only the recomputed rows (DropNA,
         Section 5.3): their write slots serve as the read slots, R keys per
-        request, and the non-anchor affix entries are never read."""
+        request, and the non-anchor affix entries are never read.
+        score_last_only: the last layer only adds its score (acache_layer_score)
+        and x is left at the last layer's input."""
         R = self.rows_per_request(k)
         groups = self.request_groups(R)
         read, nk = (m["write_slots"], R) if drop_non_anchor else (m["read_slots"], self.S)
         if score is not None and len(groups) > 1:
             raise ValueError("probe batch too large for one call")
-        for n in range(self.model.n_layers if upto is None else min(upto, self.model.n_layers)):
+        n_run = self.model.n_layers if upto is None else min(upto, self.model.n_layers)
+        for n in range(n_run):
+            layer = A.acache_layer_recompute
+            if score is not None and score_last_only and n == self.model.n_layers - 1:
+                layer = A.acache_layer_score
             for b0, b1 in groups:
                 nb = b1 - b0
                 cu_rows = [b * R for b in range(nb + 1)]
                 cu_keys = [b * nk for b in range(nb + 1)]
                 rows = slice(b0 * R, b1 * R)
-                A.acache_layer_recompute(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows],
-                                         m["row_pos"][rows], m["write_slots"][rows],
-                                         read[b0 * nk:b1 * nk], self.k_pools[n],
-                                         self.v_pools[n], self.ws, score=score, stream=stream)
+                layer(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows], m["row_pos"][rows],
+                      m["write_slots"][rows], read[b0 * nk:b1 * nk], self.k_pools[n], self.v_pools[n], self.ws,
+                      score=score, stream=stream)
         return x
 
     # ------------------------------------------------------------------ the method
@@ -199,21 +205,24 @@ class AffixBatch:
         for k in self.k_pools:
             A.acache_rerotate_k(self.model.dims, k, slots, k, slots, d, stream=stream)
 
-    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None):
+    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None, outputs: bool = True):
         """One-shot probe (Section 3.2): forward the non-affix rows against the
         fixed shared affix cache and accumulate Eq. 5 over layers.  Returns
-        (scores [B, L] fp32, x rows, maps)."""
+        (scores [B, L] fp32, x rows, maps).  outputs=False: the last layer
+        computes only what its score reads (acache_layer_score), and the
+        returned x is None."""
         m = self.maps(None, 0, stream)
         x = self.gather_inputs(m, stream)
         scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
         score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
                      affix_slots=self.affix_slots, scores=scores, norm=norm)
-        self.run_layers(x, m, 0, score=score, stream=stream)
-        return scores, x, m
+        self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream)
+        return scores, (x if outputs else None), m
 
-    def select_anchors(self, k: int, norm: int = A.ACACHE_NORM_AFFIX, stream=None):
-        """Probe then Eq. 6.  Returns (anchors [B, k] int32 ascending, scores)."""
-        scores, _, _ = self.probe(norm, stream)
+    def select_anchors(self, k: int, norm: int = A.ACACHE_NORM_AFFIX, stream=None, full_probe: bool = False):
+        """Probe then Eq. 6.  Returns (anchors [B, k] int32 ascending, scores).
+        The probe's last layer stops at its score unless full_probe."""
+        scores, _, _ = self.probe(norm, stream, outputs=full_probe)
         if k == 0:
             return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
         return A.acache_topk(scores, k, stream=stream), scores

@@ -132,6 +132,32 @@ def test_layer_decode_validation(A):
     assert call(batch=0) == 0 and call(rows=0) == 0   # nothing to do
 
 
+def test_layer_score_validation(A):
+    """acache_layer_score rejects bad arguments before any launch."""
+    lib = A.lib
+    dims = A.make_dims(4096, 32, 32, 128, 12288, "bf16")
+    w = A.LayerWeights(16, 16, 0, 0, 0, 0)  # only attn_norm and w_qkv are read
+    p = ctypes.c_void_p(16)
+    cu_rows = (ctypes.c_int32 * 3)(0, 512, 1024)
+    cu_keys = (ctypes.c_int32 * 3)(0, 1536, 3072)
+    rg = A.Ragged(2, cu_rows, cu_keys)
+
+    def call(cu_q=(0, 256, 512), L=1024, norm=A.ACACHE_NORM_AFFIX, score=True, wslots=None, rslots=None, vpool=None,
+             ws_bytes=1 << 40):
+        cq = (ctypes.c_int32 * 3)(*cu_q)
+        sa = A.ScoreArgs(16, cq, 16, L, norm, 16)
+        return lib.acache_layer_score(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(rg), p, p, wslots, rslots, p,
+                                      vpool, 4096, 100000, ctypes.byref(sa) if score else None, p, ws_bytes, None)
+    assert call(score=False) == 1                      # score is required
+    assert call(norm=7) == 4                           # unknown normalisation
+    assert call(cu_q=(0, 256, 1025)) == 2              # more masked rows than rows
+    assert call(cu_q=(0, 300, 200)) == 2               # decreasing offsets
+    assert call(L=70000) == 2                          # affix beyond 65536
+    assert call(norm=A.ACACHE_NORM_FULL) == 1          # the full softmax needs the slot lists and V
+    assert call(ws_bytes=100) == 5                     # workspace too small
+    assert call(cu_q=(0, 0, 0)) == 0 and call(L=0) == 0  # nothing to add
+
+
 def test_offset_limits(A):
     """Operands whose element offsets would not fit 32 bits are rejected
     before any launch."""

@@ -132,6 +132,34 @@ def test_probe_scores_and_anchors(case, norm):
         np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], w.n_anchors))
 
 
+@pytest.mark.parametrize("norm", ["affix", "full"])
+def test_score_only_last_layer(case, norm):
+    """The probe whose last layer stops at its score (acache_layer_score):
+    scores and anchors against the oracle's full probe, scores close to the
+    GPU's full probe, and under the affix-only normalisation the last
+    layer's pools are not written."""
+    import torch
+    from paper_2608_26140_amd import acache as A
+    w, s, layers, sk, sv, oc = case
+    dt = w.dims.dtype
+    code = A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL
+    full_scores, _, _ = s.batch.probe(code)
+    before = (s.batch.k_pools[-1].clone(), s.batch.v_pools[-1].clone())
+    scores, x, _ = s.batch.probe(code, outputs=False)
+    torch.cuda.synchronize()
+    assert x is None
+    if norm == "affix":
+        assert torch.equal(s.batch.k_pools[-1], before[0]) and torch.equal(s.batch.v_pools[-1], before[1])
+    g = down(scores)
+    assert_close(g, down(full_scores), dt, "score-only against full probe")
+    anchors = A.acache_topk(scores, w.n_anchors).cpu().numpy()
+    for b in range(w.batch):
+        res = oc.probe(b, norm)
+        assert_close(g[b], res.scores, dt, f"scores request {b}")
+        ov = anchors_agree(anchors[b], O.topk_anchors(res.scores, w.n_anchors), res.scores, w.n_anchors, TOL[dt])
+        assert_overlap(ov, res.scores, w.n_anchors, TOL[dt], f"request {b}")
+
+
 def test_selective_refresh_with_common_anchors(case):
     """Both sides refresh with the oracle's anchor set."""
     w, s, layers, sk, sv, oc = case
