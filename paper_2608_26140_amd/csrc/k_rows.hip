@@ -135,6 +135,51 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, c
   for (int i = threadIdx.x; i < d; i += 256) yr[i] = from_f32<T>(to_f32(xr[i]) * inv * to_f32(g[i]));
 }
 
+// bf16 rows with d % 8 == 0, d <= 8192 and 16-byte aligned rows: 16-byte
+// loads, the row kept in registers between the sum of squares and the
+// scaling, and the gain loaded before the reduction.  Same arithmetic as
+// rmsnorm_kernel (x * inv * g per element).
+__global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const bf16* __restrict__ x, const bf16* __restrict__ g,
+                                                          bf16* __restrict__ y, int d, float eps) {
+  const int64_t row = blockIdx.x;
+  const int nch = d >> 3;
+  bf16x8 xv[4], gv[4];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch < nch) {
+      xv[c] = *reinterpret_cast<const bf16x8*>(x + row * d + (int64_t)ch * 8);
+      gv[c] = *reinterpret_cast<const bf16x8*>(g + (int64_t)ch * 8);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    if (threadIdx.x + c * 256 < nch) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = (float)xv[c][j];
+        ss += v * v;
+      }
+    }
+  }
+  __shared__ float red[4];
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  const float inv = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    if (ch < nch) {
+      bf16x8 o;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o[j] = (bf16)((float)xv[c][j] * inv * (float)gv[c][j]);
+      *reinterpret_cast<bf16x8*>(y + row * d + (int64_t)ch * 8) = o;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- split-K reduce + rotary (queries only)
 // The probe's last layer projects only the masked rows' queries, as fp32
 // split-K partials [splits][n][H * 128].  One thread per (row, head, 4 of
@@ -155,6 +200,7 @@ __global__ __launch_bounds__(256) void q_rotary_reduce_kernel(const float* __res
   const int64_t r = rows[i];
   if (r < 0 || r >= q_n_rows) return;
   float lo[4] = {0.f, 0.f, 0.f, 0.f}, hi[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
   for (int sp = 0; sp < splits; ++sp) {
     const float* pp = part + ((int64_t)sp * n + i) * hq + h * 128 + d0;
     const f32x4 a = *reinterpret_cast<const f32x4*>(pp);
@@ -182,39 +228,61 @@ __global__ __launch_bounds__(256) void q_rotary_reduce_kernel(const float* __res
 }
 
 // ---------------------------------------------------------------- split-K reduce + residual (+ RMSNorm)
-// One workgroup per row; each thread keeps up to 4 chunks of 8 columns in
+// One workgroup per row; each thread keeps NC chunks of 8 columns in
 // registers between the residual sum and the normalisation (d <= 8192).
+// Chunk c of thread t is column chunk t + 256 c; the loads are issued for
+// all NC chunks of a split (clamped to the last chunk, results of absent
+// chunks unused) so that they are in flight together.  Each element is
+// x + p_0 + p_1 + ... in split order.
+template <int NC>
 __global__ __launch_bounds__(256) void reduce_residual_kernel(bf16* __restrict__ x, const float* __restrict__ part,
                                                               int splits, int M, int d,
                                                               const bf16* __restrict__ g,
                                                               bf16* __restrict__ y, float eps) {
   const int64_t row = blockIdx.x;
   const int nch = d >> 3;
-  float v[4][8];
+  int64_t off[NC];
+  bool ok[NC];
+  float v[NC][8];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int ch = threadIdx.x + c * 256;
+    ok[c] = ch < nch;
+    off[c] = row * d + (int64_t)min(ch, nch - 1) * 8;
+    const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + off[c]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[c][j] = (float)xv[j];
+  }
+#pragma unroll 2
+  for (int sp = 0; sp < splits; ++sp) {
+    f32x4 a[NC], b[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float* pp = part + (int64_t)sp * M * d + off[c];
+      a[c] = *reinterpret_cast<const f32x4*>(pp);
+      b[c] = *reinterpret_cast<const f32x4*>(pp + 4);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[c][j] += a[c][j];
+        v[c][4 + j] += b[c][j];
+      }
+  }
   float ss = 0.f;
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int ch = threadIdx.x + c * 256;
-    if (ch < nch) {
-      const int64_t off = row * d + (int64_t)ch * 8;
-      const bf16x8 xv = *reinterpret_cast<const bf16x8*>(x + off);
+  for (int c = 0; c < NC; ++c) {
+    bf16x8 o;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[c][j] = (float)xv[j];
-      for (int sp = 0; sp < splits; ++sp) {
-        const float* pp = part + (int64_t)sp * M * d + off;
-        const f32x4 a = *reinterpret_cast<const f32x4*>(pp);
-        const f32x4 b = *reinterpret_cast<const f32x4*>(pp + 4);
+    for (int j = 0; j < 8; ++j) {
+      o[j] = (bf16)v[c][j];
+      v[c][j] = (float)o[j];
+    }
+    if (ok[c]) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) { v[c][j] += a[j]; v[c][4 + j] += b[j]; }
-      }
-      bf16x8 o;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        o[j] = (bf16)v[c][j];
-        v[c][j] = (float)o[j];
-        ss += v[c][j] * v[c][j];
-      }
-      *reinterpret_cast<bf16x8*>(x + off) = o;
+      for (int j = 0; j < 8; ++j) ss += v[c][j] * v[c][j];
+      *reinterpret_cast<bf16x8*>(x + off[c]) = o;
     }
   }
   if (!y) return;
@@ -224,21 +292,20 @@ __global__ __launch_bounds__(256) void reduce_residual_kernel(bf16* __restrict__
   __syncthreads();
   const float inv = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + eps);
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int ch = threadIdx.x + c * 256;
-    if (ch < nch) {
-      const int64_t off = row * d + (int64_t)ch * 8;
+  for (int c = 0; c < NC; ++c) {
+    if (ok[c]) {
+      const int ch = threadIdx.x + c * 256;
       const bf16x8 gv = *reinterpret_cast<const bf16x8*>(g + (int64_t)ch * 8);
       bf16x8 o;
 #pragma unroll
       for (int j = 0; j < 8; ++j) o[j] = (bf16)(v[c][j] * inv * (float)gv[j]);
-      *reinterpret_cast<bf16x8*>(y + off) = o;
+      *reinterpret_cast<bf16x8*>(y + off[c]) = o;
     }
   }
 }
 
 // ---------------------------------------------------------------- probe-score head reduction (Eq. 5)
-__global__ __launch_bounds__(256) void head_reduce_kernel(const float* __restrict__ part, int batch, int H,
+__global__ __launch_bounds__(64) void head_reduce_kernel(const float* __restrict__ part, int batch, int H,
                                                           int L, float* __restrict__ scores) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)batch * L) return;
@@ -246,7 +313,9 @@ __global__ __launch_bounds__(256) void head_reduce_kernel(const float* __restric
   const int j = (int)(t - (int64_t)b * L);
   const float* p = part + (int64_t)b * H * L + j;
   float s = 0.f;
-  for (int h = 0; h < H; ++h) s += p[(int64_t)h * L];  // fixed order over heads
+  // fixed order over heads; unrolled so that the loads are in flight together
+#pragma unroll 8
+  for (int h = 0; h < H; ++h) s += p[(int64_t)h * L];
   scores[t] += s;
 }
 
@@ -529,7 +598,12 @@ hipError_t launch_build_maps(const acache_layout& lay, const acache_paging* pagi
 
 hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y, int rows, int d,
                           float eps, hipStream_t s) {
-  if (dt == ACACHE_BF16)
+  const bool vec = d % 8 == 0 && d <= 8192 && (uintptr_t)x % 16 == 0 && (uintptr_t)g % 16 == 0 &&
+                   (uintptr_t)y % 16 == 0;
+  if (dt == ACACHE_BF16 && vec)
+    hipLaunchKernelGGL(rmsnorm_vec_kernel, dim3(rows), dim3(256), 0, s, (const bf16*)x, (const bf16*)g, (bf16*)y,
+                       d, eps);
+  else if (dt == ACACHE_BF16)
     hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x,
                        (const bf16*)g, (bf16*)y, d, eps);
   else
@@ -540,8 +614,14 @@ hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y
 
 hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M, int d,
                                   const void* g, void* y, float eps, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_residual_kernel, dim3(M), dim3(256), 0, s, (bf16*)x, part, splits, M, d,
-                     (const bf16*)g, (bf16*)y, eps);
+  const int nc = ((d >> 3) + 255) / 256;
+  auto go = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(M), dim3(256), 0, s, (bf16*)x, part, splits, M, d, (const bf16*)g, (bf16*)y, eps);
+  };
+  if (nc <= 1) go(reduce_residual_kernel<1>);
+  else if (nc == 2) go(reduce_residual_kernel<2>);
+  else if (nc == 3) go(reduce_residual_kernel<3>);
+  else go(reduce_residual_kernel<4>);
   return hipGetLastError();
 }
 
@@ -603,7 +683,8 @@ hipError_t launch_threshold_commit(int batch, int block, const int32_t* pick, co
 hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
                               hipStream_t s) {
   const int64_t work = (int64_t)batch * L;
-  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 255) / 256)), dim3(256), 0, s, part,
+  // 64-thread workgroups: a request's keys spread over more CUs
+  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 63) / 64)), dim3(64), 0, s, part,
                      batch, H, L, scores);
   return hipGetLastError();
 }

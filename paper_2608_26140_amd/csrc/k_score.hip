@@ -91,17 +91,23 @@ __global__ __launch_bounds__(64 * kQSplit) void colsum_kernel(ColsumArgs a) {
   for (int t = t0; t < nq; t += STEP) {
     if (t + STEP < nq) load_q(row_next, qnext);
     if (t + 2 * STEP < nq) row_next = row_of(t + 2 * STEP);
-    // log-sum-exp (base 2) of the 16 queries this lane's registers hold
+    // log-sum-exp (base 2) of the 16 queries this lane's registers hold.
+    // The loads are unconditional (clamped indices) so that all 16 are in
+    // flight together; absent queries then take +inf, i.e. exp2(-inf) = 0.
     float lse2[16];
+    int64_t lidx[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
-      float v = INFINITY;  // absent query: contributes exp2(-inf) = 0
-      if (qq < nq) {
-        const int64_t idx = a.lse_by_qrow ? (int64_t)(q0 + qq) : (int64_t)a.q_rows[q0 + qq];
-        if (a.lse_by_qrow || (idx >= 0 && idx < a.q_n_rows)) v = a.lse[idx * a.H + h] * kLog2e;
-      }
-      lse2[r] = v;
+      const int qc = min(qq, nq - 1);
+      lidx[r] = a.lse_by_qrow ? (int64_t)(q0 + qc) : (int64_t)a.q_rows[q0 + qc];
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
+      const bool ok = qq < nq && (a.lse_by_qrow || (lidx[r] >= 0 && lidx[r] < a.q_n_rows));
+      const float v = a.lse[(ok ? lidx[r] : 0) * a.H + h];
+      lse2[r] = ok ? v * kLog2e : INFINITY;
     }
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
