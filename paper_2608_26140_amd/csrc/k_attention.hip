@@ -492,6 +492,8 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   const int n_rows = a.row_start[b + 1] - a.row_start[b];
   const int qi = (tile - a.tile_start[b]) * kPvTileQ + wave * 32 + (lane & 31);
   const bool q_ok = qi < n_rows;
+  // a wavefront without a valid query only copies and synchronises
+  const bool live = __builtin_amdgcn_ballot_w64(q_ok) != 0;
   const int S = a.key_len[b];
   const int32_t* slots = a.slots + a.key_start[b];
   const int n_kt = (S + kTileK - 1) / kTileK;
@@ -591,6 +593,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
       issue(t + 1);  // into the slot of tile t - 1, which every wave has finished
       if (t + 2 < t_hi) load_slots(t + 2);
     }
+    if (!live) continue;
     const char* ks = ring + (t & 1) * kStageB;
     const char* vs = ks + kTileB;
     f32x16 st[2];
