@@ -19,6 +19,7 @@ namespace {
 
 constexpr int kDh = 128;
 constexpr int kQSplit = 4;  // wavefronts per workgroup, each a quarter of the query tiles
+constexpr int kLseStage = 2048;  // queries per request whose LSE is staged in LDS
 
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -43,6 +44,7 @@ __global__ __launch_bounds__(64 * kQSplit) void colsum_kernel(ColsumArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5;
   constexpr int STEP = 32 * kQSplit;  // query stride between a wavefront's tiles
   __shared__ float red[kQSplit][64];
+  __shared__ float lse_s[kLseStage];
   const int g = h / (a.H / a.Hkv);
   const float scale = kLog2e * rsqrtf((float)kDh);
 
@@ -88,6 +90,17 @@ __global__ __launch_bounds__(64 * kQSplit) void colsum_kernel(ColsumArgs a) {
   const int t0 = wave * 32;
   int64_t row_next = row_of(t0 + STEP);
   load_q(row_of(t0), qcur);
+  // the LSE (base 2) of every query of the request, staged in LDS with the
+  // first loads in flight (+inf for absent rows: exp2(-inf) = 0)
+  const bool staged = nq <= kLseStage;
+  if (staged) {
+    for (int i = threadIdx.x; i < nq; i += 64 * kQSplit) {
+      const int64_t idx = a.lse_by_qrow ? (int64_t)(q0 + i) : (int64_t)a.q_rows[q0 + i];
+      const bool ok = a.lse_by_qrow || (idx >= 0 && idx < a.q_n_rows);
+      lse_s[i] = ok ? a.lse[idx * a.H + h] * kLog2e : INFINITY;
+    }
+    __syncthreads();
+  }
   for (int t = t0; t < nq; t += STEP) {
     if (t + STEP < nq) load_q(row_next, qnext);
     if (t + 2 * STEP < nq) row_next = row_of(t + 2 * STEP);
@@ -95,19 +108,27 @@ __global__ __launch_bounds__(64 * kQSplit) void colsum_kernel(ColsumArgs a) {
     // The loads are unconditional (clamped indices) so that all 16 are in
     // flight together; absent queries then take +inf, i.e. exp2(-inf) = 0.
     float lse2[16];
-    int64_t lidx[16];
+    if (staged) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const int qc = min(qq, nq - 1);
-      lidx[r] = a.lse_by_qrow ? (int64_t)(q0 + qc) : (int64_t)a.q_rows[q0 + qc];
-    }
+      for (int r = 0; r < 16; ++r) {
+        const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
+        lse2[r] = qq < nq ? lse_s[qq] : INFINITY;
+      }
+    } else {
+      int64_t lidx[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
-      const bool ok = qq < nq && (a.lse_by_qrow || (lidx[r] >= 0 && lidx[r] < a.q_n_rows));
-      const float v = a.lse[(ok ? lidx[r] : 0) * a.H + h];
-      lse2[r] = ok ? v * kLog2e : INFINITY;
+      for (int r = 0; r < 16; ++r) {
+        const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
+        const int qc = min(qq, nq - 1);
+        lidx[r] = a.lse_by_qrow ? (int64_t)(q0 + qc) : (int64_t)a.q_rows[q0 + qc];
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qq = t + 8 * (r >> 2) + 4 * hl + (r & 3);
+        const bool ok = qq < nq && (a.lse_by_qrow || (lidx[r] >= 0 && lidx[r] < a.q_n_rows));
+        const float v = a.lse[(ok ? lidx[r] : 0) * a.H + h];
+        lse2[r] = ok ? v * kLog2e : INFINITY;
+      }
     }
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
