@@ -535,9 +535,21 @@ static acache_status run_out_mlp_bf16(const acache_dims* dims, const acache_laye
   g.N = d;
   g.K = hq;
   g.splits = gemm_bf16_splits(M, d, hq);
-  g.P = part;
-  LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
-  LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
+  if (g.splits == 1) {
+    // one K split: the projection adds itself to the residual in its
+    // epilogue (x + acc rounded once, as the reduction would), then RMSNorm
+    g.splits = 1;
+    g.C = x;
+    g.ldc = d;
+    g.sk_ws = part;
+    LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_ACCUM, g, stream));
+    LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, x, w->mlp_norm, y, M, d, dims->rms_eps, stream));
+  } else {
+    g.P = part;
+    LAUNCH_T(ACACHE_K_GEMM_O, stream, launch_gemm_bf16(EPI_PARTIAL, g, stream));
+    LAUNCH_T(ACACHE_K_RESIDUAL, stream,
+             launch_reduce_residual(x, part, g.splits, M, d, w->mlp_norm, y, dims->rms_eps, stream));
+  }
   GemmParams u = {};
   u.X = y;
   u.W = w->w_gate_up;
@@ -556,9 +568,17 @@ static acache_status run_out_mlp_bf16(const acache_dims* dims, const acache_laye
   dn.N = d;
   dn.K = F;
   dn.splits = gemm_bf16_splits(M, d, F);
-  dn.P = part;
-  LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_PARTIAL, dn, stream));
-  LAUNCH_T(ACACHE_K_RESIDUAL, stream, launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+  if (dn.splits == 1) {
+    dn.C = x;
+    dn.ldc = d;
+    dn.sk_ws = part;
+    LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_ACCUM, dn, stream));
+  } else {
+    dn.P = part;
+    LAUNCH_T(ACACHE_K_GEMM_DOWN, stream, launch_gemm_bf16(EPI_PARTIAL, dn, stream));
+    LAUNCH_T(ACACHE_K_RESIDUAL, stream,
+             launch_reduce_residual(x, part, dn.splits, M, d, nullptr, nullptr, dims->rms_eps, stream));
+  }
   return ACACHE_OK;
 }
 
