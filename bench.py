@@ -239,6 +239,26 @@ def main():
         ms_hkvd = timed(select_hkvd, args.steps)
         ms_shift = timed(shift, 2 * max(1, args.steps // 2))
 
+    # the step with cold caches: before each step a 512 MiB write evicts the
+    # 256 MB MALL and the L2s (weights and inputs then come from HBM)
+    cold = None
+    if not args.only_step:
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        n_cold = max(1, min(args.steps, 20))
+        tot = 0.0
+        for _ in range(n_cold):
+            flush.fill_(1)
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record()
+            step()
+            c1.record()
+            torch.cuda.synchronize()
+            tot += c0.elapsed_time(c1)
+        del flush
+        ms_cold = tot / n_cold
+        cold = {"ms_per_step": round(ms_cold, 4), "value": round(B * R / (ms_cold * 1e-3), 1), "steps": n_cold,
+                "flush_MiB": 512}
+
     peak, bound = PEAK[d.dtype]
     step_flops = sum(fl["probe"].values()) + sum(fl["refresh"].values())
     by = bytes_model(w)
@@ -291,6 +311,7 @@ def main():
             "selective_refresh": round(ms_refresh, 4),
             "full_refresh": round(ms_full, 4), "selective_refresh_dropna": round(ms_drop, 4),
             "shift_affix": round(ms_shift, 4), "select_anchors_hkvd": round(ms_hkvd, 4)},
+        "cold_caches": cold,
         "shift_affix_GB_per_s": None if ms_shift is None else round(
             2 * L * d.n_kv_heads * d.head_dim * (2 if d.dtype == "bf16" else 4) * d.n_layers / (ms_shift * 1e-3) / 1e9, 1),
         "refresh_speedup_vs_full": None if ms_refresh is None else round(ms_full / ms_refresh, 3),
