@@ -460,21 +460,29 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
   }
 }
 
-// Stream-K fixup: block = one wave of one split tile of the stream-K region.
-// Sums the tile's pieces in workgroup order and runs the epilogue.
+// Stream-K fixup: block = one wave-tile of one split tile of the stream-K
+// region.  Sums the tile's pieces in workgroup order and runs the epilogue.
+// The pieces are read four at a time: wave 0 adds the first of a round from
+// memory while waves 1-3 copy the next three to LDS, then wave 0 adds those
+// in order, so the sum is p_first + p_first+1 + ... as one sequential loop.
 template <int EPI, class C>
-__global__ __launch_bounds__(64) void gemm_bf16_fixup(GemmParams p, TileMap tm) {
+__global__ __launch_bounds__(256) void gemm_bf16_fixup(GemmParams p, TileMap tm) {
+  constexpr int kPieceF = 64 * C::ACC4 * 4;  // floats per wave piece
   __shared__ double inv_freq[64];
-  const int lane = threadIdx.x;
+  __shared__ __attribute__((aligned(16))) float stage[3][kPieceF];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int q = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
   const int wn = wave % C::WN, wm = wave / C::WN;
   const int nk_tile = tm.nk;
   const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
   if (first == last) return;  // the tile was finished by one workgroup
-  if constexpr (EPI == EPI_QKV) {
-    init_inv_freq(inv_freq, p, lane);
-    __syncthreads();
-  }
+  if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
+  // piece 0 of w if w's range starts in this tile, else its piece 1
+  auto piece = [&](int w) {
+    const int pc = sk_start(tm, w) / nk_tile == s ? 0 : 1;
+    return tm.sk_part + ((size_t)(w * 2 + pc) * C::WAVES + wave) * kPieceF;
+  };
   f32x16 acc[4][C::FM];
 #pragma unroll
   for (int a = 0; a < 4; ++a)
@@ -482,11 +490,23 @@ __global__ __launch_bounds__(64) void gemm_bf16_fixup(GemmParams p, TileMap tm) 
     for (int b = 0; b < C::FM; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-  for (int w = first; w <= last; ++w) {
-    // piece 0 of w if w's range starts in this tile, else its piece 1
-    const int piece = sk_start(tm, w) / nk_tile == s ? 0 : 1;
-    add_partial<C>(tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4), acc, lane);
+  for (int w0 = first; w0 <= last; w0 += 4) {
+    if (q > 0 && w0 + q <= last) {
+      const float* src = piece(w0 + q);
+      float* dst = stage[q - 1];
+#pragma unroll 8
+      for (int i = 0; i < C::ACC4; ++i)
+        *reinterpret_cast<f32x4*>(dst + (i * 64 + lane) * 4) =
+            *reinterpret_cast<const f32x4*>(src + (i * 64 + lane) * 4);
+    }
+    if (q == 0) add_partial<C>(piece(w0), acc, lane);
+    __syncthreads();
+    if (q == 0) {
+      for (int j = 1; j < 4 && w0 + j <= last; ++j) add_partial<C>(stage[j - 1], acc, lane);
+    }
+    __syncthreads();
   }
+  if (q != 0) return;
   int nt, mt, sp;
   tile_coords(tm, tm.sk_first + s, nt, mt, sp);
   epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane, inv_freq);
@@ -627,7 +647,7 @@ hipError_t launch_plan(GemmEpi epi, const GemmParams& p, const Plan& pl, hipStre
     case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
   }
   if (pl.sk_tiles > 0) {
-    const dim3 fgrid(pl.sk_tiles * C::WAVES), fblock(64);
+    const dim3 fgrid(pl.sk_tiles * C::WAVES), fblock(256);
     switch (epi) {
       case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
       case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
