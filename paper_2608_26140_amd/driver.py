@@ -343,6 +343,25 @@ def decode_schedule(batch: AffixBatch, head: Head, plan: DecodePlan, k: int, log
     return committed
 
 
+def capture(fn, warmup: int = 2):
+    """Records the launches of fn() (the library's kernels, torch's fills and
+    allocations) into a HIP graph: warmup calls on a side stream, then one
+    call under capture.  Returns (graph, fn's outputs); graph.replay() reruns
+    every launch with the same buffers and arguments, and rewrites the same
+    output tensors.  fn must not synchronise with the host, and the library's
+    kernel timer must not be armed while it is captured."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(warmup):
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out = fn()
+    return g, out
+
+
 def _on(stream):
     """torch's own copies and fills go to the stream the library calls use."""
     return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
