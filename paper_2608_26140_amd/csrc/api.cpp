@@ -710,10 +710,15 @@ acache_status acache_layer_score(const acache_dims* dims, const acache_layer_wei
     // the masked rows only: gather, normalise, project to queries (split-K
     // over the whole chip), then sum the splits and rotate
     CHECK(dims->d_ff >= d, ACACHE_ERR_UNSUPPORTED);  // the gathered rows sit in the MLP region
-    void* xq = at<char>(ws, p.h);
-    LAUNCH_T(ACACHE_K_GATHER, stream, launch_gather_rows(x, (int64_t)d * 2, M, score->q_rows, nullptr, 0, Mq, d * 2,
-                                                         xq, (int64_t)d * 2, stream));
-    LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, xq, w->attn_norm, y, Mq, d, dims->rms_eps, stream));
+    if (rmsnorm_rows_ok(x, w->attn_norm, y, d)) {
+      LAUNCH_T(ACACHE_K_RMSNORM, stream,
+               launch_rmsnorm_rows(x, M, score->q_rows, w->attn_norm, y, Mq, d, dims->rms_eps, stream));
+    } else {
+      void* xq = at<char>(ws, p.h);
+      LAUNCH_T(ACACHE_K_GATHER, stream, launch_gather_rows(x, (int64_t)d * 2, M, score->q_rows, nullptr, 0, Mq,
+                                                           d * 2, xq, (int64_t)d * 2, stream));
+      LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, xq, w->attn_norm, y, Mq, d, dims->rms_eps, stream));
+    }
     GemmParams g = {};
     g.X = y;
     g.W = w->w_qkv;  // the query rows come first

@@ -40,6 +40,12 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
                                   const void* g, void* y, float eps, hipStream_t s);
 // q[rows[i]] = rotary(sum_s part[s][i], pos[rows[i]]) for the n rows of bf16
 // queries with head_dim 128 (fp32 partials [splits][n][H * 128]).
+// bf16 RMSNorm of gathered rows: y[i] = norm(x[src_rows[i]]) (zero for an
+// index outside [0, n_src)); needs rmsnorm_rows_ok (d % 8 == 0, d <= 8192,
+// 16-byte aligned x, g and y).
+bool rmsnorm_rows_ok(const void* x, const void* g, const void* y, int d);
+hipError_t launch_rmsnorm_rows(const void* x, int64_t n_src, const int32_t* src_rows, const void* g, void* y,
+                               int rows, int d, float eps, hipStream_t s);
 hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
                                   const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s);
 // scores[b][j] += sum_h part[b][h][j]

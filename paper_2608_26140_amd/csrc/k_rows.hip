@@ -139,9 +139,19 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const T* __restrict__ x, c
 // loads, the row kept in registers between the sum of squares and the
 // scaling, and the gain loaded before the reduction.  Same arithmetic as
 // rmsnorm_kernel (x * inv * g per element).
+// With rows, output row i normalises x[rows[i]] (the gather fused in; a row
+// index outside [0, n_src) gives a zero row, as the gather does).
 __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const bf16* __restrict__ x, const bf16* __restrict__ g,
-                                                          bf16* __restrict__ y, int d, float eps) {
+                                                          bf16* __restrict__ y, int d, float eps,
+                                                          const int32_t* __restrict__ rows, int64_t n_src) {
   const int64_t row = blockIdx.x;
+  int64_t src = row;
+  bool ok = true;
+  if (rows != nullptr) {
+    src = rows[row];
+    ok = src >= 0 && src < n_src;
+    if (!ok) src = 0;
+  }
   const int nch = d >> 3;
   bf16x8 xv[4], gv[4];
   float ss = 0.f;
@@ -149,8 +159,9 @@ __global__ __launch_bounds__(256) void rmsnorm_vec_kernel(const bf16* __restrict
   for (int c = 0; c < 4; ++c) {
     const int ch = threadIdx.x + c * 256;
     if (ch < nch) {
-      xv[c] = *reinterpret_cast<const bf16x8*>(x + row * d + (int64_t)ch * 8);
+      xv[c] = *reinterpret_cast<const bf16x8*>(x + src * d + (int64_t)ch * 8);
       gv[c] = *reinterpret_cast<const bf16x8*>(g + (int64_t)ch * 8);
+      if (!ok) xv[c] = bf16x8{};
     }
   }
 #pragma unroll
@@ -602,13 +613,25 @@ hipError_t launch_rmsnorm(acache_dtype dt, const void* x, const void* g, void* y
                    (uintptr_t)y % 16 == 0;
   if (dt == ACACHE_BF16 && vec)
     hipLaunchKernelGGL(rmsnorm_vec_kernel, dim3(rows), dim3(256), 0, s, (const bf16*)x, (const bf16*)g, (bf16*)y,
-                       d, eps);
+                       d, eps, nullptr, (int64_t)0);
   else if (dt == ACACHE_BF16)
     hipLaunchKernelGGL(rmsnorm_kernel<bf16>, dim3(rows), dim3(256), 0, s, (const bf16*)x,
                        (const bf16*)g, (bf16*)y, d, eps);
   else
     hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(rows), dim3(256), 0, s, (const float*)x,
                        (const float*)g, (float*)y, d, eps);
+  return hipGetLastError();
+}
+
+bool rmsnorm_rows_ok(const void* x, const void* g, const void* y, int d) {
+  return d % 8 == 0 && d <= 8192 && (uintptr_t)x % 16 == 0 && (uintptr_t)g % 16 == 0 && (uintptr_t)y % 16 == 0;
+}
+
+hipError_t launch_rmsnorm_rows(const void* x, int64_t n_src, const int32_t* src_rows, const void* g, void* y,
+                               int rows, int d, float eps, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rmsnorm_vec_kernel, dim3(rows), dim3(256), 0, s, (const bf16*)x, (const bf16*)g, (bf16*)y, d,
+                     eps, src_rows, n_src);
   return hipGetLastError();
 }
 
