@@ -108,6 +108,10 @@ typedef struct {
   int32_t affix_len;          /* L */
   acache_norm norm;
   float* scores;              /* [batch, L] fp32, accumulated (+=) */
+  int32_t init;               /* nonzero: scores = this layer's sum, not read first (a probe's first
+                                 layer, so the caller need not clear scores).  Applies only to a call
+                                 that scores (L > 0 and some masked rows); otherwise scores is left
+                                 unchanged, as with init == 0 */
 } acache_score_args;
 
 /* Logical layout shared by every request of a batch, and its slot plan. */

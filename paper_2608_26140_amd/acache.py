@@ -45,7 +45,7 @@ class Ragged(ctypes.Structure):
 class ScoreArgs(ctypes.Structure):
     _fields_ = [("q_rows", ctypes.c_void_p), ("cu_q", ctypes.POINTER(ctypes.c_int32)),
                 ("affix_slots", ctypes.c_void_p), ("affix_len", ctypes.c_int32), ("norm", ctypes.c_int32),
-                ("scores", ctypes.c_void_p)]
+                ("scores", ctypes.c_void_p), ("init", ctypes.c_int32)]
 
 
 class Layout(ctypes.Structure):
@@ -318,7 +318,7 @@ def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tenso
         cq = _i32(score["cu_q"])
         sa = ScoreArgs(score["q_rows"].data_ptr(), cq, score["affix_slots"].data_ptr(),
                        score["affix_slots"].numel(), score.get("norm", ACACHE_NORM_AFFIX),
-                       score["scores"].data_ptr())
+                       score["scores"].data_ptr(), int(score.get("init", 0)))
     _check("acache_layer_recompute", lib.acache_layer_recompute(
         ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
         _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],
@@ -339,7 +339,7 @@ def acache_layer_score(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tensor, p
     rg, keep = _ragged(cu_rows, cu_keys)
     cq = _i32(score["cu_q"])
     sa = ScoreArgs(score["q_rows"].data_ptr(), cq, score["affix_slots"].data_ptr(), score["affix_slots"].numel(),
-                   score.get("norm", ACACHE_NORM_AFFIX), score["scores"].data_ptr())
+                   score.get("norm", ACACHE_NORM_AFFIX), score["scores"].data_ptr(), int(score.get("init", 0)))
     _check("acache_layer_score", lib.acache_layer_score(
         ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
         _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0], ctypes.byref(sa), _ptr(ws),

@@ -172,7 +172,7 @@ acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, co
                         int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows, const void* k_pool,
                         int64_t pool_ld, int64_t n_slots, const int32_t* affix_slots, int L,
                         acache_norm norm, const float* lse_full, float* scores, float* lse_aff,
-                        float* colsum, hipStream_t s) {
+                        float* colsum, int init, hipStream_t s) {
   const int H = d->n_heads, Hkv = d->n_kv_heads, dh = d->head_dim;
   const float* lse = lse_full;
   int by_qrow = 0;
@@ -193,7 +193,7 @@ acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, co
     LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
                                    (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
                                    colsum, s));
-  LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, H, L, scores, s));
+  LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, H, L, scores, init, s));
   return ACACHE_OK;
 }
 
@@ -490,7 +490,7 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
   const WsPlan w = plan_ws(dims, n_q, batch, affix_len);
   CHECK(ws && ws_bytes >= w.total, ACACHE_ERR_WORKSPACE);
   return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
-                   affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum),
+                   affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum), 0,
                    stream);
 }
 
@@ -647,7 +647,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   if (probe) {
     st = run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots,
                    score->affix_slots, L, score->norm, lse, score->scores, at<float>(ws, p.lse_aff),
-                   at<float>(ws, p.colsum), stream);
+                   at<float>(ws, p.colsum), score->init, stream);
     if (st != ACACHE_OK) return st;
   }
   if (dims->dtype == ACACHE_BF16) {
@@ -755,7 +755,8 @@ acache_status acache_layer_score(const acache_dims* dims, const acache_layer_wei
     }
   }
   return run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots, score->affix_slots, L,
-                   score->norm, lse, score->scores, at<float>(ws, p.lse_aff), at<float>(ws, p.colsum), stream);
+                   score->norm, lse, score->scores, at<float>(ws, p.lse_aff), at<float>(ws, p.colsum), score->init,
+                   stream);
 }
 
 acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_weights* w, int32_t batch,

@@ -49,7 +49,8 @@ hipError_t launch_rmsnorm_rows(const void* x, int64_t n_src, const int32_t* src_
 hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
                                   const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s);
 // scores[b][j] += sum_h part[b][h][j]
-hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
+// scores[b, j] (+)= sum over heads of part[b][h][j]; init: write instead of add
+hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores, int init,
                               hipStream_t s);
 
 // ---- bf16 MFMA GEMM (k_gemm.hip).  C = X W^T, X [M, K], W [N, K].

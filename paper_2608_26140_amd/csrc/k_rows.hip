@@ -317,7 +317,7 @@ __global__ __launch_bounds__(256) void reduce_residual_kernel(bf16* __restrict__
 
 // ---------------------------------------------------------------- probe-score head reduction (Eq. 5)
 __global__ __launch_bounds__(64) void head_reduce_kernel(const float* __restrict__ part, int batch, int H,
-                                                          int L, float* __restrict__ scores) {
+                                                          int L, float* __restrict__ scores, int init) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)batch * L) return;
   const int b = (int)(t / L);
@@ -327,7 +327,7 @@ __global__ __launch_bounds__(64) void head_reduce_kernel(const float* __restrict
   // fixed order over heads; unrolled so that the loads are in flight together
 #pragma unroll 8
   for (int h = 0; h < H; ++h) s += p[(int64_t)h * L];
-  scores[t] += s;
+  scores[t] = init ? s : scores[t] + s;
 }
 
 inline int grid_for(int64_t work, int per_block = 256, int cap = 65535) {
@@ -703,12 +703,12 @@ hipError_t launch_threshold_commit(int batch, int block, const int32_t* pick, co
   return hipGetLastError();
 }
 
-hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores,
+hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores, int init,
                               hipStream_t s) {
   const int64_t work = (int64_t)batch * L;
   // 64-thread workgroups: a request's keys spread over more CUs
   hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 63) / 64)), dim3(64), 0, s, part,
-                     batch, H, L, scores);
+                     batch, H, L, scores, init);
   return hipGetLastError();
 }
 

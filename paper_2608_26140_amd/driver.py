@@ -178,9 +178,10 @@ class AffixBatch:
                 cu_rows = [b * R for b in range(nb + 1)]
                 cu_keys = [b * nk for b in range(nb + 1)]
                 rows = slice(b0 * R, b1 * R)
+                sc = score if score is None or n == 0 else dict(score, init=0)
                 layer(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows], m["row_pos"][rows],
                       m["write_slots"][rows], read[b0 * nk:b1 * nk], self.k_pools[n], self.v_pools[n], self.ws,
-                      score=score, stream=stream)
+                      score=sc, stream=stream)
         return x
 
     # ------------------------------------------------------------------ the method
@@ -213,9 +214,14 @@ class AffixBatch:
         returned x is None."""
         m = self.maps(None, 0, stream)
         x = self.gather_inputs(m, stream)
-        scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
+        # the first layer writes the scores (init) and the others add to them;
+        # with no masked rows no layer scores, and they stay zero
+        if self.G > 0:
+            scores = torch.empty((self.B, self.L), dtype=torch.float32, device=self.device)
+        else:
+            scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
         score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
-                     affix_slots=self.affix_slots, scores=scores, norm=norm)
+                     affix_slots=self.affix_slots, scores=scores, norm=norm, init=int(self.G > 0))
         self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream)
         return scores, (x if outputs else None), m
 

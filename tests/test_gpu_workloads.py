@@ -160,6 +160,28 @@ def test_score_only_last_layer(case, norm):
         assert_overlap(ov, res.scores, w.n_anchors, TOL[dt], f"request {b}")
 
 
+def test_score_init_writes(case):
+    """init on the probe's first layer writes the scores instead of adding:
+    a buffer full of NaN ends with the same bits as the accumulating path on
+    a cleared buffer."""
+    import torch
+    from paper_2608_26140_amd import acache as A
+    w, s, layers, sk, sv, oc = case
+    b = s.batch
+    m = b.maps(None, 0)
+    out = {}
+    for init, fill in ((0, 0.0), (1, float("nan"))):
+        x = b.gather_inputs(m)
+        scores = torch.full((b.B, b.L), fill, dtype=torch.float32, device="cuda")
+        score = dict(q_rows=m["q_rows"], cu_q=[i * b.G for i in range(b.B + 1)], affix_slots=b.affix_slots,
+                     scores=scores, norm=A.ACACHE_NORM_AFFIX, init=init)
+        b.run_layers(x, m, 0, score=score)
+        torch.cuda.synchronize()
+        out[init] = scores.clone()
+    assert not torch.isnan(out[1]).any()
+    assert torch.equal(out[0], out[1])
+
+
 def test_selective_refresh_with_common_anchors(case):
     """Both sides refresh with the oracle's anchor set."""
     w, s, layers, sk, sv, oc = case
