@@ -13,7 +13,8 @@ the passage of "Affix Cache for Diffusion Large Language Models" it follows:
 * Section 3.2, Eq. 4: a_{j,k} = [softmax(Q_mask K_affix^T / sqrt(d_h))]_{k,j},
   the weight from masked query k to affix key j at layer n, head h.
 * Section 3.2, Eq. 5: s_j = sum over layers, heads and masked queries of a.
-* Section 3.2, Eq. 6: the anchor set A = TopK(s, K); S = F minus A.
+* Section 3.2, Eq. 6: the anchor set A = TopK(s, K); S = F minus A; K from
+  the anchor ratio rho as the integer nearest to rho * L.
 * Section 3.2 (probe): the request's non-affix positions are forwarded with
   the precomputed affix cache as fixed past KV; affix states are neither
   forwarded nor updated.
@@ -46,6 +47,7 @@ design notes):
 
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass
 from typing import List, Optional, Sequence
 
@@ -169,6 +171,14 @@ def layer_kv(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray):
     return rope(k, pos, dims.rope_base), v
 
 
+def layer_queries(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray) -> np.ndarray:
+    """The queries a block forms for rows x [R, d] at positions pos: RMSNorm,
+    the Q projection, rotation.  Returns q [R, H, d_h]."""
+    h = rms_norm(x, w.g1, dims.rms_eps)
+    q = (h @ w.wq.T).reshape(x.shape[0], dims.n_heads, dims.head_dim)
+    return rope(q, pos, dims.rope_base)
+
+
 def layer_forward(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray,
                   rows: np.ndarray, view_k: np.ndarray, view_v: np.ndarray):
     """One block over the recomputed rows (Section 4.3, Appendix C.1).
@@ -179,9 +189,8 @@ def layer_forward(w: Layer, dims: Dims, x: np.ndarray, pos: np.ndarray,
     whole view.  Returns (x_out [R, d], q [R, H, d_h] post-rotation,
     lse [R, H])."""
     r = x.shape[0]
-    nh, nkv, dh = dims.n_heads, dims.n_kv_heads, dims.head_dim
-    h = rms_norm(x, w.g1, dims.rms_eps)
-    q = rope((h @ w.wq.T).reshape(r, nh, dh), pos, dims.rope_base)
+    nh, dh = dims.n_heads, dims.head_dim
+    q = layer_queries(w, dims, x, pos)
     k, v = layer_kv(w, dims, x, pos)
     view_k[rows] = k
     view_v[rows] = v
@@ -222,6 +231,20 @@ def affix_attention_mass(q_masked: np.ndarray, k_affix: np.ndarray, norm: str = 
             raise ValueError(norm)
         s += a.sum(axis=0)
     return s
+
+
+def anchor_count(ratio: float, affix_len: int) -> int:
+    """Eq. 6 takes K tokens; the anchor ratio rho fixes K as the integer
+    nearest to rho * L, halves rounded up (the paper gives no rounding rule;
+    the tiny workload's "ratio 0.2 (26 tokens)" at L = 128 rules out the
+    floor), clamped to [0, L].  Exact rational arithmetic on the binary value
+    of rho, so no float rounding decides a half."""
+    from fractions import Fraction
+    r = Fraction(ratio)
+    if r < 0 or r > 1:
+        raise ValueError(f"anchor ratio {ratio} outside [0, 1]")
+    k = math.floor(r * affix_len + Fraction(1, 2))
+    return max(0, min(int(affix_len), int(k)))
 
 
 def topk_anchors(s: np.ndarray, k: int) -> np.ndarray:

@@ -79,6 +79,18 @@ def _silu_wrong(a):
 _orig_attention = O.attention
 
 
+def _anchor_count_ceil(ratio, L):
+    return min(L, int(np.ceil(ratio * L)))
+
+
+def _anchor_count_floor(ratio, L):
+    return int(ratio * L)
+
+
+def _anchor_count_half_down(ratio, L):
+    return min(L, int(np.ceil(ratio * L - 0.5)))
+
+
 def _layer_swapped_gate_up(w, dims, x, pos, rows, vk, vv):
     w2 = O.Layer(g1=w.g1, wq=w.wq, wk=w.wk, wv=w.wv, wo=w.wo, g2=w.g2, wg=w.wu, wu=w.wg, wd=w.wd)
     return _orig_layer(w2, dims, x, pos, rows, vk, vv)
@@ -109,7 +121,7 @@ def _run_pins(pins):
     for name, fn in pins:
         try:
             fn()
-        except AssertionError:
+        except (AssertionError, pytest.fail.Exception):
             failed.append(name)
     return failed
 
@@ -133,6 +145,9 @@ MUTATIONS = {
     "silu_sign": ("silu", _silu_wrong),
     "gate_up_swapped": ("layer_forward", _layer_swapped_gate_up),
     "attend_before_store": ("layer_forward", _layer_attend_before_store),
+    "anchor_count_ceil": ("anchor_count", _anchor_count_ceil),
+    "anchor_count_floor": ("anchor_count", _anchor_count_floor),
+    "anchor_count_half_down": ("anchor_count", _anchor_count_half_down),
 }
 
 
@@ -155,5 +170,8 @@ def test_planted_mistake_is_caught(name, monkeypatch):
         ("layer_torch", lambda: T_req.test_layer_matches_torch_block(2)),
         ("poison", lambda: T_req.test_anchor_poison_does_not_reach_outputs(fx)),
         ("ratio_one", lambda: T_req.test_ratio_one_is_full_recompute_and_ignores_stale(fx)),
+        ("k_workloads", T_ops.test_anchor_count_of_the_workloads),
+        ("k_nearest", lambda: T_ops.test_anchor_count_is_nearest_integer(10)),
+        ("k_halves", T_ops.test_anchor_count_halves_and_bounds),
     ]
     assert _run_pins(pins), f"planted mistake {name} passed every pin"

@@ -356,3 +356,47 @@ def test_confidence_and_threshold_commit():
             want = np.zeros(8, bool)
             want[min(np.flatnonzero(~done), key=lambda i: (-c[i], i))] = True
         np.testing.assert_array_equal(t, want)
+
+
+# ----------------------------------------------------------------------------- anchor count (Eq. 6's K)
+
+def anchor_count_brute(ratio, L):
+    """The integer K in [0, L] nearest to ratio * L, the larger one on a tie
+    (distance compared exactly in rationals)."""
+    from fractions import Fraction
+    t = Fraction(ratio) * L
+    best = None
+    for k in range(L + 1):
+        d = abs(Fraction(k) - t)
+        if best is None or d < best[0] or (d == best[0] and k > best[1]):
+            best = (d, k)
+    return best[1]
+
+
+def test_anchor_count_of_the_workloads():
+    # ratio 0.2 at the workloads' affix lengths: rho * L = 25.6, 204.8,
+    # 409.6, 819.2, 1638.4; the tiny workload states "26 tokens" for 0.2 x 128
+    assert O.anchor_count(0.2, 128) == 26
+    assert O.anchor_count(0.2, 1024) == 205
+    assert O.anchor_count(0.2, 2048) == 410
+    assert [O.anchor_count(r, 4096) for r in (0.1, 0.2, 0.4)] == [410, 819, 1638]
+    assert O.anchor_count(0.2, 8192) == 1638
+    # the readings it rules out: floor gives 25 at 25.6, ceil 820 at 819.2
+    assert math.floor(0.2 * 128) == 25 and math.ceil(0.2 * 4096) == 820
+
+
+@pytest.mark.parametrize("L", [0, 1, 2, 7, 10, 128, 250, 1000])
+def test_anchor_count_is_nearest_integer(L):
+    for ratio in (0.0, 0.05, 0.1, 0.125, 0.2, 0.25, 0.3, 1 / 3, 0.5, 0.75, 0.999, 1.0):
+        assert O.anchor_count(ratio, L) == anchor_count_brute(ratio, L), (ratio, L)
+
+
+def test_anchor_count_halves_and_bounds():
+    assert O.anchor_count(0.5, 1) == 1      # 0.5 exactly: up
+    assert O.anchor_count(0.25, 2) == 1     # 0.5 exactly: up
+    assert O.anchor_count(0.375, 4) == 2    # 1.5 exactly: up
+    assert O.anchor_count(0.0, 100) == 0 and O.anchor_count(1.0, 100) == 100
+    with pytest.raises(ValueError):
+        O.anchor_count(-0.1, 10)
+    with pytest.raises(ValueError):
+        O.anchor_count(1.5, 10)
