@@ -149,6 +149,14 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
                            hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_anchor_count — the K of Eq. 6 for anchor ratio `ratio` over an affix
+ * of affix_len tokens: the integer nearest to ratio * affix_len, a half
+ * rounded up (the paper states no rounding; 0.2 of 128 tokens is 26), within
+ * [0, affix_len].  Host-side arithmetic, no device work.  Returns -1 if
+ * ratio is outside [0, 1] (or NaN) or affix_len < 0. */
+int32_t acache_anchor_count(double ratio, int32_t affix_len);
+
+/* ---------------------------------------------------------------------------
  * acache_topk — Eq. 6: per request b, the k indices j of the largest
  * scores[b, j], written ascending to idx_out[b, 0..k).  Ties go to the lowest
  * index; -0 equals +0; NaN ranks below every other value (-inf included).
@@ -455,6 +463,14 @@ typedef enum {
 } acache_kernel_id;
 acache_status acache_time_kernel(int32_t kernel, hipEvent_t* starts, hipEvent_t* stops,
                                  int32_t capacity, int32_t* count);
+
+/* The K splits acache_layer_recompute uses for `rows` rows: of the output
+ * projection (*o_splits) and of the down projection (*down_splits).  One
+ * split: the projection adds itself to the residual in its epilogue (and
+ * RMSNorm runs as a kernel of its own after the output projection); more:
+ * fp32 partials reduced with the residual (and RMSNorm) by one kernel.  Both
+ * are 1 for fp32 dims or rows == 0.  Host arithmetic only. */
+acache_status acache_layer_schedule(const acache_dims* dims, int32_t rows, int32_t* o_splits, int32_t* down_splits);
 
 /* Workspace bytes needed by acache_layer_recompute, acache_score and
  * acache_linear for up to max_rows rows, `batch` requests and affix length

@@ -409,8 +409,14 @@ def hkvd_scores(layers, dims, req: Request, stale_k, stale_v) -> np.ndarray:
     forward of the request through that layer.  Returns s [L]."""
     n = hkvd_layer(len(layers))
     full = full_refresh(layers[:n + 1], dims, req)
-    dk = full.views_k[n][req.affix] - stale_k[n]
-    dv = full.views_v[n][req.affix] - stale_v[n]
+    return kv_deviation(full.views_k[n][req.affix], full.views_v[n][req.affix], stale_k[n], stale_v[n])
+
+
+def kv_deviation(k_a, v_a, k_b, v_b) -> np.ndarray:
+    """Per token, the squared difference of two caches' K and V summed over
+    heads and dimensions (the HKVD selector's deviation).  Each [L, H_kv, d_h]."""
+    dk = np.asarray(k_a) - np.asarray(k_b)
+    dv = np.asarray(v_a) - np.asarray(v_b)
     return (dk * dk).sum(axis=(1, 2)) + (dv * dv).sum(axis=(1, 2))
 
 

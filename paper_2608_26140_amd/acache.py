@@ -89,6 +89,7 @@ def _load():
         "acache_layer_decode": [ctypes.POINTER(Dims), ctypes.POINTER(LayerWeights), I32, I32, P, P, P, P, I32, P, I32,
                                 P, I32, P, P, I64, I64, P, SZ, P],
         "acache_rmsnorm": [ctypes.POINTER(Dims), P, P, P, I32, P],
+        "acache_layer_schedule": [ctypes.POINTER(Dims), I32, PI, PI],
         "acache_linear": [ctypes.POINTER(Dims), P, P, P, I32, I32, I32, I32, P, SZ, P],
     }
     for name, args in sig.items():
@@ -100,6 +101,8 @@ def _load():
     lib.acache_status_string.argtypes = [ctypes.c_int32]
     lib.acache_status_string.restype = ctypes.c_char_p
     lib.acache_version.restype = ctypes.c_int32
+    lib.acache_anchor_count.argtypes = [ctypes.c_double, I32]
+    lib.acache_anchor_count.restype = ctypes.c_int32
     return lib
 
 
@@ -149,6 +152,21 @@ def acache_workspace_size(dims: Dims, max_rows: int, batch: int, affix_len: int)
 
 def workspace(dims: Dims, max_rows: int, batch: int, affix_len: int, device="cuda") -> torch.Tensor:
     return torch.empty(acache_workspace_size(dims, max_rows, batch, affix_len), dtype=torch.uint8, device=device)
+
+
+def acache_layer_schedule(dims: Dims, rows: int):
+    """(o_splits, down_splits) acache_layer_recompute uses for `rows` rows."""
+    o, dn = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check("acache_layer_schedule", lib.acache_layer_schedule(ctypes.byref(dims), rows, ctypes.byref(o),
+                                                              ctypes.byref(dn)))
+    return o.value, dn.value
+
+
+def acache_anchor_count(ratio: float, affix_len: int) -> int:
+    k = lib.acache_anchor_count(float(ratio), int(affix_len))
+    if k < 0:
+        raise AcacheError("acache_anchor_count", 2, f"ratio {ratio} / affix length {affix_len} out of range")
+    return k
 
 
 def acache_topk(scores: torch.Tensor, k: int, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:

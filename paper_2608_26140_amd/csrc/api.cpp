@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 
 #include "internal.h"
@@ -239,6 +240,14 @@ size_t acache_workspace_size(const acache_dims* dims, int32_t max_rows, int32_t 
   return plan_ws(dims, max_rows, batch, affix_len).total;
 }
 
+int32_t acache_anchor_count(double ratio, int32_t affix_len) {
+  if (!(ratio >= 0.0 && ratio <= 1.0) || affix_len < 0) return -1;
+  // ratio * L is exact in double for L < 2^31 up to the product's rounding;
+  // the half-up rule is floor(x + 1/2)
+  const double k = std::floor(ratio * (double)affix_len + 0.5);
+  return (int32_t)std::min<double>(std::max(k, 0.0), (double)affix_len);
+}
+
 acache_status acache_topk(const float* scores, int32_t batch, int32_t L, int32_t k,
                           int32_t* idx_out, hipStream_t stream) {
   CHECK(batch >= 0 && L >= 0 && k >= 0 && k <= L, ACACHE_ERR_SHAPE);
@@ -463,12 +472,13 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
   return ACACHE_OK;
 }
 
-acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
-                           int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
-                           const void* k_pool, int64_t pool_ld, int64_t n_slots,
-                           const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
-                           acache_norm norm, float* scores, void* ws, size_t ws_bytes,
-                           hipStream_t stream) {
+// Host checks of acache_score.  Sets *noop when the
+// call has nothing to do.
+static acache_status check_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                                 int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q, const void* k_pool,
+                                 int64_t pool_ld, int64_t n_slots, const int32_t* affix_slots, int32_t affix_len,
+                                 const float* row_lse, acache_norm norm, const float* scores, bool* noop) {
+  *noop = true;
   acache_status st = check_dims(dims);
   if (st != ACACHE_OK) return st;
   CHECK(batch >= 0 && batch <= kMaxBatch && affix_len >= 0 && affix_len <= 65536, ACACHE_ERR_SHAPE);
@@ -476,8 +486,7 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
   if (batch == 0 || affix_len == 0) return ACACHE_OK;
   st = check_cu(cu_q, batch);
   if (st != ACACHE_OK) return st;
-  const int n_q = cu_q[batch];
-  if (n_q == 0) return ACACHE_OK;
+  if (cu_q[batch] == 0) return ACACHE_OK;
   CHECK(q && q_rows && k_pool && affix_slots && scores, ACACHE_ERR_NULL);
   CHECK(norm == ACACHE_NORM_FULL ? row_lse != nullptr : row_lse == nullptr, ACACHE_ERR_NULL);
   CHECK(q_ld >= (int64_t)dims->n_heads * dims->head_dim && q_n_rows >= 0, ACACHE_ERR_SHAPE);
@@ -486,12 +495,42 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
   const int64_t es = (int64_t)elem_size(dims->dtype);
   CHECK(aligned16(q) && aligned16(k_pool) && (q_ld * es) % 16 == 0 && (pool_ld * es) % 16 == 0,
         ACACHE_ERR_ALIGN);
+  *noop = false;
+  return ACACHE_OK;
+}
+
+acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                           int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
+                           const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                           const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
+                           acache_norm norm, float* scores, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  bool noop = true;
+  acache_status st = check_score(dims, batch, q, q_ld, q_n_rows, q_rows, cu_q, k_pool, pool_ld, n_slots,
+                                 affix_slots, affix_len, row_lse, norm, scores, &noop);
+  if (st != ACACHE_OK || noop) return st;
   // workspace: the lse and column-sum regions of a plan sized for n_q rows
-  const WsPlan w = plan_ws(dims, n_q, batch, affix_len);
+  const WsPlan w = plan_ws(dims, cu_q[batch], batch, affix_len);
   CHECK(ws && ws_bytes >= w.total, ACACHE_ERR_WORKSPACE);
   return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
                    affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum), 0,
                    stream);
+}
+
+
+acache_status acache_layer_schedule(const acache_dims* dims, int32_t rows, int32_t* o_splits, int32_t* down_splits) {
+  acache_status st = check_layer_dims(dims);
+  if (st != ACACHE_OK) return st;
+  CHECK(rows >= 0, ACACHE_ERR_SHAPE);
+  CHECK(o_splits && down_splits, ACACHE_ERR_NULL);
+  const int d = dims->d_model, hq = dims->n_heads * dims->head_dim;
+  if (dims->dtype != ACACHE_BF16 || rows == 0) {
+    *o_splits = *down_splits = 1;
+    return ACACHE_OK;
+  }
+  *o_splits = gemm_bf16_splits(rows, d, hq);
+  *down_splits = gemm_bf16_splits(rows, d, dims->d_ff);
+  return ACACHE_OK;
 }
 
 // bf16 block pieces shared by acache_layer_recompute and acache_layer_decode.

@@ -15,7 +15,7 @@ on one stream, without synchronising.
 from __future__ import annotations
 
 import contextlib
-from typing import List, Optional
+from typing import Callable, List, Optional
 
 import numpy as np
 import torch
@@ -133,6 +133,10 @@ class AffixBatch:
         return blocks * self.bs * self.model.kv_width * 2 * self.model.n_layers * self.k_pools[0].element_size()
 
     # ------------------------------------------------------------------ pieces
+    def anchor_count(self, ratio: float) -> int:
+        """Eq. 6's K for anchor ratio `ratio` over this batch's affix."""
+        return A.acache_anchor_count(ratio, self.L)
+
     def rows_per_request(self, k: int) -> int:
         return k + self.S - self.L
 
@@ -157,12 +161,16 @@ class AffixBatch:
 
     def run_layers(self, x: torch.Tensor, m: dict, k: int, score: Optional[dict] = None,
                    drop_non_anchor: bool = False, upto: Optional[int] = None, score_last_only: bool = False,
-                   stream=None):
+                   stream=None, layer_hook: Optional[Callable[[int, torch.Tensor], None]] = None):
         """drop_non_anchor: attention reads only the recomputed rows (DropNA,
         Section 5.3): their write slots serve as the read slots, R keys per
         request, and the non-anchor affix entries are never read.
         score_last_only: the last layer only adds its score (acache_layer_score)
-        and x is left at the last layer's input."""
+        and x is left at the last layer's input.
+        layer_hook(n, x): called on the host before layer n's launches are
+        issued (x then holds layer n's input in stream order), and once more
+        with n = the number of layers run after the last one; for inspection,
+        e.g. copies of the rows on the same stream."""
         R = self.rows_per_request(k)
         groups = self.request_groups(R)
         read, nk = (m["write_slots"], R) if drop_non_anchor else (m["read_slots"], self.S)
@@ -170,6 +178,8 @@ class AffixBatch:
             raise ValueError("probe batch too large for one call")
         n_run = self.model.n_layers if upto is None else min(upto, self.model.n_layers)
         for n in range(n_run):
+            if layer_hook is not None:
+                layer_hook(n, x)
             layer = A.acache_layer_recompute
             if score is not None and score_last_only and n == self.model.n_layers - 1:
                 layer = A.acache_layer_score
@@ -182,6 +192,8 @@ class AffixBatch:
                 layer(self.model.dims, self.model.lw[n], cu_rows, cu_keys, x[rows], m["row_pos"][rows],
                       m["write_slots"][rows], read[b0 * nk:b1 * nk], self.k_pools[n], self.v_pools[n], self.ws,
                       score=sc, stream=stream)
+        if layer_hook is not None:
+            layer_hook(n_run, x)
         return x
 
     # ------------------------------------------------------------------ the method
@@ -206,12 +218,13 @@ class AffixBatch:
         for k in self.k_pools:
             A.acache_rerotate_k(self.model.dims, k, slots, k, slots, d, stream=stream)
 
-    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None, outputs: bool = True):
+    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None, outputs: bool = True, layer_hook=None):
         """One-shot probe (Section 3.2): forward the non-affix rows against the
         fixed shared affix cache and accumulate Eq. 5 over layers.  Returns
         (scores [B, L] fp32, x rows, maps).  outputs=False: the last layer
         computes only what its score reads (acache_layer_score), and the
-        returned x is None."""
+        returned x is None.  layer_hook(n, x, scores): as run_layers', with
+        the score buffer (its sum over the layers before n)."""
         m = self.maps(None, 0, stream)
         x = self.gather_inputs(m, stream)
         # the first layer writes the scores (init) and the others add to them;
@@ -222,7 +235,8 @@ class AffixBatch:
             scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
         score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
                      affix_slots=self.affix_slots, scores=scores, norm=norm, init=int(self.G > 0))
-        self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream)
+        hook = None if layer_hook is None else (lambda n, xx: layer_hook(n, xx, scores))
+        self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream, layer_hook=hook)
         return scores, (x if outputs else None), m
 
     def select_anchors(self, k: int, norm: int = A.ACACHE_NORM_AFFIX, stream=None, full_probe: bool = False):
@@ -251,13 +265,14 @@ class AffixBatch:
             return torch.empty((self.B, 0), dtype=torch.int32, device=self.device), scores
         return A.acache_topk(scores, k, stream=stream), scores
 
-    def refresh(self, anchors: Optional[torch.Tensor], k: int, drop_non_anchor: bool = False, stream=None):
+    def refresh(self, anchors: Optional[torch.Tensor], k: int, drop_non_anchor: bool = False, stream=None,
+                layer_hook=None):
         """Selective recomputation (Section 3.3): anchors plus every
         request-specific row through all layers; with drop_non_anchor the
         DropNA ablation (Section 5.3).  Returns (x rows [B*R, d], maps)."""
         m = self.maps(anchors, k, stream)
         x = self.gather_inputs(m, stream)
-        self.run_layers(x, m, k, drop_non_anchor=drop_non_anchor, stream=stream)
+        self.run_layers(x, m, k, drop_non_anchor=drop_non_anchor, stream=stream, layer_hook=layer_hook)
         return x, m
 
     def full_refresh(self, stream=None):

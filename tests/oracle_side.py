@@ -6,6 +6,22 @@ import numpy as np
 from oracle import acache_oracle as O
 
 
+def anchor_count(w, ratio=None):
+    """Eq. 6's K for the workload's anchor ratio: the library's count, which
+    must equal the oracle's (each side derives it on its own)."""
+    from paper_2608_26140_amd import acache as A
+    r = w.ratio if ratio is None else ratio
+    k = A.acache_anchor_count(r, w.layout.affix_len)
+    ref = O.anchor_count(r, w.layout.affix_len)
+    assert k == ref, f"{w.name}: library K {k} != oracle K {ref} at ratio {r}"
+    return k
+
+
+def rows_selective(w, ratio=None):
+    """Recomputed rows per request: the K anchors plus every non-affix row."""
+    return anchor_count(w, ratio) + w.layout.n_nonaffix
+
+
 def oracle_dims(w):
     d = w.dims
     return O.Dims(d_model=d.d_model, n_heads=d.n_heads, n_kv_heads=d.n_kv_heads, head_dim=d.head_dim,
@@ -44,29 +60,32 @@ def oracle_stale(w, host, layers):
     return O.materialize_affix_cache(layers, dims, donor)
 
 
-def anchors_agree(got, ref, scores_ref, k, tol_rel):
-    """Overlap >= 99% of K, and every anchor in the symmetric difference has
-    an oracle score within tol_rel (relative to the K-th score) of the
-    oracle's K-th largest score (the tie band).  Returns the overlap."""
-    got, ref = set(int(v) for v in got), set(int(v) for v in ref)
+def check_anchors(got, scores_ref, k, score_err, what=""):
+    """The anchor-set gate for Eq. 6 when the scores carry rounding.
+
+    got: an anchor set chosen as the exact top-K of the GPU's scores;
+    scores_ref: the oracle's scores; score_err: max_j |g_j - r_j| of the GPU's
+    scores against them, measured by the calling test.  The oracle's set is
+    the top-K of scores_ref.  An anchor can change sides only where the two
+    scores' rounding reorders it with the K-th place: with every score within
+    e of the oracle's, each element of the symmetric difference lies within
+    2e of the oracle's K-th score.  The band is 3e.  Besides, when K >= 100
+    (one swap is at most 1% of K) the sets must overlap by at least 99%;
+    below that, any swap must still lie in the band.  Returns the overlap."""
+    got = set(int(v) for v in got)
+    ref_idx = O.topk_anchors(scores_ref, k)
+    ref = set(int(v) for v in ref_idx)
+    assert len(got) == k, f"{what}: {len(got)} distinct anchors, expected {k}"
     if k == 0:
         return 1.0
     overlap = len(got & ref) / k
-    kth = np.sort(scores_ref)[::-1][k - 1]
-    band = tol_rel * abs(kth)
-    for j in got ^ ref:
-        assert abs(scores_ref[j] - kth) <= band, f"anchor {j} outside the tie band ({scores_ref[j]} vs {kth})"
+    kth = np.sort(np.asarray(scores_ref, dtype=np.float64))[::-1][k - 1]
+    band = 3.0 * float(score_err)
+    for j in sorted(got ^ ref):
+        assert abs(scores_ref[j] - kth) <= band, (
+            f"{what}: anchor {j} changes sides outside the tie band (score {scores_ref[j]:.9g}, K-th {kth:.9g}, "
+            f"band {band:.3e})")
+    if k >= 100:
+        assert overlap >= 0.99, f"{what}: anchor overlap {overlap:.4f} < 0.99 (K = {k})"
+    print(f"[anchors] {what}: K {k} overlap {overlap:.4f} swaps {len(got - ref)} band {band:.3e}", flush=True)
     return overlap
-
-
-def assert_overlap(overlap, scores_ref, k, tol_rel, what=""):
-    """The anchor-set overlap must reach 99%, except where the oracle's own
-    K-th and (K+1)-th scores are closer than the tie band: then swapping
-    them is within the scores' tolerance and anchors_agree has already
-    checked that every swap lies in the band."""
-    if overlap >= 0.99 or k == 0 or k >= len(scores_ref):
-        return
-    s = np.sort(np.asarray(scores_ref, dtype=np.float64))[::-1]
-    gap = s[k - 1] - s[k]
-    assert gap <= tol_rel * abs(s[k - 1]), (
-        f"{what}: anchor overlap {overlap:.3f} < 0.99 with a clear boundary (K-th/K+1-th gap {gap:.3e})")

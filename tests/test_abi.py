@@ -173,3 +173,27 @@ def test_offset_limits(A):
     w = A.LayerWeights(16, 16, 16, 16, 16, 16)
     assert lib.acache_layer_recompute(ctypes.byref(dims), ctypes.byref(w), ctypes.byref(rg), p, p, p, p, p, p,
                                       4096, 100, None, p, 1 << 62, None) == 4
+
+
+def test_anchor_count_matches_the_oracle(A):
+    """acache_anchor_count (host arithmetic in the library) against the
+    oracle's exact-rational count, over the workloads' ratios and a grid of
+    ratios and affix lengths with exact halves."""
+    from oracle import acache_oracle as O
+    for L in (0, 1, 2, 3, 4, 7, 10, 100, 128, 200, 250, 1024, 2048, 4096, 8192, 65536):
+        for r in (0.0, 0.05, 0.1, 0.125, 0.2, 0.25, 0.3, 0.375, 0.4, 0.5, 0.6, 0.75, 0.9, 0.999, 1.0):
+            assert A.acache_anchor_count(r, L) == O.anchor_count(r, L), (r, L)
+    assert A.lib.acache_anchor_count(-0.1, 10) == -1
+    assert A.lib.acache_anchor_count(1.5, 10) == -1
+    assert A.lib.acache_anchor_count(float("nan"), 10) == -1
+    assert A.lib.acache_anchor_count(0.5, -1) == -1
+
+
+def test_workload_anchor_counts():
+    import workloads as W
+    from tests.oracle_side import anchor_count
+    want = {"tiny-f32": 26, "llada-layer": 205, "llada-stack-b8": 410, "dream-stack-b4": 819, "llada-serve-b32": 1638}
+    for name, k in want.items():
+        assert anchor_count(W.get_config(name)) == k
+    dream = W.get_config("dream-stack-b4")
+    assert [anchor_count(dream, r) for r in dream.ratios] == [410, 819, 1638]

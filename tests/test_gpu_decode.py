@@ -27,7 +27,7 @@ import pytest
 import workloads as W
 from oracle import acache_oracle as O
 from tests.gpu_util import TOL, assert_close, down, down_bits, up, up_i32
-from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
+from tests.oracle_side import anchor_count, rows_selective, oracle_dims, oracle_layers, oracle_request, oracle_stale
 
 pytestmark = pytest.mark.gpu
 
@@ -100,7 +100,7 @@ def serve():
     w = W.get_config("mini-serve")
     s = WL.build(w)
     dt, lay = w.dims.dtype, w.layout
-    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    L, K, B = lay.affix_len, anchor_count(w), w.batch
     layers = oracle_layers(w, s.host)
     dims = oracle_dims(w)
     sk64, sv64 = oracle_stale(w, s.host, layers)
@@ -137,7 +137,7 @@ def test_decode_steps_against_oracle(serve, split_shared):
     from paper_2608_26140_amd import driver as D
     w, s, layers, dims, sk, sv, anchors = serve
     dt, lay = w.dims.dtype, w.layout
-    B, K, blen, S = w.batch, w.n_anchors, w.decode_block, lay.seq_len
+    B, K, blen, S = w.batch, anchor_count(w), w.decode_block, lay.seq_len
     blk = 1
     p0 = lay.mask_begin + blk * blen
     positions = np.arange(p0, p0 + blen)
@@ -240,7 +240,7 @@ def test_threshold_schedule(serve, tau):
     from paper_2608_26140_amd import driver as D
     w, s, layers, dims, sk, sv, anchors = serve
     dt, lay = w.dims.dtype, w.layout
-    B, K, blen = w.batch, w.n_anchors, w.decode_block
+    B, K, blen = w.batch, anchor_count(w), w.decode_block
     n_blocks = lay.mask_len // blen
     g_bits, head_bits = W.draw_lm_head(w)
     head = D.Head(up(g_bits, dt), up(head_bits, dt))
@@ -275,7 +275,7 @@ def test_paged_matches_flat():
     from paper_2608_26140_amd import workload as WL
     w = W.get_config("mini-serve")
     dt, lay = w.dims.dtype, w.layout
-    B, K, blen, L = w.batch, w.n_anchors, w.decode_block, lay.affix_len
+    B, K, blen, L = w.batch, anchor_count(w), w.decode_block, lay.affix_len
     bs = 16
     flat, paged = WL.build(w), WL.build(w, block_size=bs)
     g_bits, head_bits = W.draw_lm_head(w)
@@ -316,7 +316,7 @@ def test_shared_private_split_matches_read_slots(serve, full):
     from paper_2608_26140_amd import driver as D
     w, s, layers, dims, sk, sv, anchors = serve
     dt, lay = w.dims.dtype, w.layout
-    B, K, blen = w.batch, w.n_anchors, w.decode_block
+    B, K, blen = w.batch, anchor_count(w), w.decode_block
     plan = D.DecodePlan(s.batch, K, blen, lay.mask_len // blen, full=full)
     a = plan.anchors if full else up_i32(anchors)
     outs, pools = [], []
@@ -342,7 +342,7 @@ def test_decode_step_gqa_infix_against_oracle():
     w = W.get_config("mini-gqa-infix")
     s = WL.build(w)
     dt, lay = w.dims.dtype, w.layout
-    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    L, K, B = lay.affix_len, anchor_count(w), w.batch
     layers = oracle_layers(w, s.host)
     dims = oracle_dims(w)
     sk64, sv64 = oracle_stale(w, s.host, layers)

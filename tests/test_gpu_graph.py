@@ -9,6 +9,7 @@ import torch
 import workloads as W
 from paper_2608_26140_amd import driver as D
 from paper_2608_26140_amd import workload as WL
+from tests.oracle_side import anchor_count
 
 pytestmark = pytest.mark.gpu
 
@@ -18,7 +19,7 @@ def test_graph_replay_matches_eager(name):
     torch.cuda.set_device(0)
     w = W.get_config(name)
     batch = WL.build(w, keep_host=False).batch
-    k = w.n_anchors
+    k = anchor_count(w)
 
     def step():
         anchors, scores = batch.select_anchors(k)

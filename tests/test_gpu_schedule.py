@@ -17,7 +17,7 @@ import pytest
 import workloads as W
 from oracle import acache_oracle as O
 from tests.gpu_util import TOL, up, up_i32
-from tests.oracle_side import oracle_dims, oracle_layers, oracle_request, oracle_stale
+from tests.oracle_side import anchor_count, rows_selective, oracle_dims, oracle_layers, oracle_request, oracle_stale
 
 pytestmark = pytest.mark.gpu
 
@@ -30,7 +30,7 @@ def test_decode_schedule_against_oracle():
     w = W.get_config("mini-serve")
     s = WL.build(w)
     dt, lay = w.dims.dtype, w.layout
-    L, K, B = lay.affix_len, w.n_anchors, w.batch
+    L, K, B = lay.affix_len, anchor_count(w), w.batch
     G, blk = lay.mask_len, w.decode_block
     n_blocks = G // blk
     layers = oracle_layers(w, s.host)

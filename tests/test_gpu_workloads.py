@@ -11,8 +11,8 @@ import pytest
 
 import workloads as W
 from oracle import acache_oracle as O
-from tests.gpu_util import TOL, assert_close, down, down_bits, up, up_i32
-from tests.oracle_side import anchors_agree, assert_overlap, oracle_dims, oracle_layers, oracle_request, oracle_stale
+from tests.gpu_util import TOL, assert_close, down, down_bits, errors, up, up_i32
+from tests.oracle_side import anchor_count, rows_selective, check_anchors, oracle_dims, oracle_layers, oracle_request, oracle_stale
 
 pytestmark = pytest.mark.gpu
 
@@ -74,7 +74,7 @@ class OracleCache:
         return self._get(("probe", b, norm), lambda: O.probe(self.layers, self.dims, self.req(b), self.sk, self.sv, norm))
 
     def anchors(self, b):
-        return self._get(("anchors", b), lambda: O.topk_anchors(self.probe(b).scores, self.w.n_anchors))
+        return self._get(("anchors", b), lambda: O.topk_anchors(self.probe(b).scores, anchor_count(self.w)))
 
     def selective(self, b):
         return self._get(("sel", b), lambda: O.selective_refresh(self.layers, self.dims, self.req(b), self.anchors(b),
@@ -111,25 +111,22 @@ def test_probe_scores_and_anchors(case, norm):
     dt = w.dims.dtype
     code = A.ACACHE_NORM_AFFIX if norm == "affix" else A.ACACHE_NORM_FULL
     scores, x_probe, m = s.batch.probe(code)
-    anchors = A.acache_topk(scores, w.n_anchors)
+    anchors = A.acache_topk(scores, anchor_count(w))
     g_scores = down(scores)
     g_anchors = anchors.cpu().numpy()
     P = w.layout.n_nonaffix
-    overlaps = []
+    K = anchor_count(w)
+    # anchors from the GPU scores are exactly the oracle's top-K of those scores
+    for b in range(w.batch):
+        np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], K))
     for b in range(w.batch):
         res = oc.probe(b, norm)
-        assert_close(g_scores[b], res.scores, dt, f"scores request {b}")
+        e = assert_close(g_scores[b], res.scores, dt, f"scores request {b}")
         assert_close(down(x_probe)[b * P:(b + 1) * P], res.x, dt, f"probe rows request {b}")
-        ref = O.topk_anchors(res.scores, w.n_anchors)
-        overlaps.append(anchors_agree(g_anchors[b], ref, res.scores, w.n_anchors, TOL[dt]))
+        check_anchors(g_anchors[b], res.scores, K, e["max_abs"], f"{w.name} request {b} ({norm})")
         if norm == "affix":
             np.testing.assert_allclose(g_scores[b].sum(), len(layers) * w.dims.n_heads * w.layout.mask_len,
                                        rtol=1e-3 if dt == "bf16" else 1e-5)
-    for b, ov in enumerate(overlaps):
-        assert_overlap(ov, oc.probe(b, norm).scores, w.n_anchors, TOL[dt], f"request {b}")
-    # anchors from the GPU scores are exactly the oracle's top-K of those scores
-    for b in range(w.batch):
-        np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], w.n_anchors))
 
 
 @pytest.mark.parametrize("norm", ["affix", "full"])
@@ -152,12 +149,12 @@ def test_score_only_last_layer(case, norm):
         assert torch.equal(s.batch.k_pools[-1], before[0]) and torch.equal(s.batch.v_pools[-1], before[1])
     g = down(scores)
     assert_close(g, down(full_scores), dt, "score-only against full probe")
-    anchors = A.acache_topk(scores, w.n_anchors).cpu().numpy()
+    K = anchor_count(w)
+    anchors = A.acache_topk(scores, K).cpu().numpy()
     for b in range(w.batch):
         res = oc.probe(b, norm)
-        assert_close(g[b], res.scores, dt, f"scores request {b}")
-        ov = anchors_agree(anchors[b], O.topk_anchors(res.scores, w.n_anchors), res.scores, w.n_anchors, TOL[dt])
-        assert_overlap(ov, res.scores, w.n_anchors, TOL[dt], f"request {b}")
+        e = assert_close(g[b], res.scores, dt, f"scores request {b}")
+        check_anchors(anchors[b], res.scores, K, e["max_abs"], f"{w.name} score-only request {b} ({norm})")
 
 
 def test_score_init_writes(case):
@@ -189,8 +186,8 @@ def test_selective_refresh_with_common_anchors(case):
     dt = w.dims.dtype
     anchors = [oc.anchors(b) for b in range(w.batch)]
     refs = [oc.selective(b) for b in range(w.batch)]
-    x, m = s.batch.refresh(up_i32(np.stack(anchors)), w.n_anchors)
-    R = w.rows_selective
+    x, m = s.batch.refresh(up_i32(np.stack(anchors)), anchor_count(w))
+    R = rows_selective(w)
     gx = down(x)
     wslots = m["write_slots"].cpu().numpy()
     for b in range(w.batch):
@@ -210,9 +207,9 @@ def test_end_to_end_own_anchors(case):
     w, s, layers, sk, sv, oc = case
     dims = oracle_dims(w)
     dt = w.dims.dtype
-    anchors, _ = s.batch.select_anchors(w.n_anchors)
-    x, m = s.batch.refresh(anchors, w.n_anchors)
-    R = w.rows_selective
+    anchors, _ = s.batch.select_anchors(anchor_count(w))
+    x, m = s.batch.refresh(anchors, anchor_count(w))
+    R = rows_selective(w)
     gx = down(x)
     pos = m["row_pos"].cpu().numpy()
     for b in range(w.batch):
@@ -270,14 +267,14 @@ def test_dropna_against_oracle_and_never_reads_non_anchors(case):
     entry may be read."""
     w, s, layers, sk, sv, oc = case
     dt = w.dims.dtype
-    L, R = w.layout.affix_len, w.rows_selective
+    L, R = w.layout.affix_len, rows_selective(w)
     anchors = np.stack([oc.anchors(b) for b in range(w.batch)])
     saved = [(k[:L].clone(), v[:L].clone()) for k, v in zip(s.batch.k_pools, s.batch.v_pools)]
     for k, v in zip(s.batch.k_pools, s.batch.v_pools):
         k[:L] = float("nan")
         v[:L] = float("nan")
     try:
-        x, _ = s.batch.refresh(up_i32(anchors), w.n_anchors, drop_non_anchor=True)
+        x, _ = s.batch.refresh(up_i32(anchors), anchor_count(w), drop_non_anchor=True)
         gx = down(x)
     finally:
         for (k0, v0), k, v in zip(saved, s.batch.k_pools, s.batch.v_pools):
@@ -302,19 +299,38 @@ def test_keepna_equals_dropna_at_ratio_one(case):
 
 def test_hkvd_selector_against_oracle(case):
     """The CacheBlend-style selector (KV deviation between the shared cache
-    and the full-prompt cache at the selection layer) and its top-K."""
+    and the full-prompt cache at the selection layer) and its top-K.
+
+    The deviation is a difference of two nearly equal caches, so the bf16
+    storage of the fresh K/V moves it far more than it moves either cache.
+    The fresh K/V are held to the fp64 oracle (the tolerance gates); the
+    deviation kernel and the anchor gate are checked on the K/V the GPU
+    stored (the oracle's deviation of those bits); the overlap with the
+    all-fp64 selection is reported."""
     w, s, layers, sk, sv, oc = case
     dims = oracle_dims(w)
     dt = w.dims.dtype
-    K = w.n_anchors
+    lay = w.layout
+    K = anchor_count(w)
+    n = O.hkvd_layer(len(layers))
     anchors, scores = s.batch.select_anchors_hkvd(K)
     g_scores, g_anchors = down(scores), anchors.cpu().numpy()
+    aff = np.arange(lay.affix_begin, lay.affix_end)
+    fresh_slots = s.batch.private_slots(lay.seq_len)[:, aff]
     for b in range(w.batch):
-        ref = O.hkvd_scores(layers, dims, oc.req(b), sk, sv)
-        assert_close(g_scores[b], ref, dt, f"KV deviation request {b}")
-        ov = anchors_agree(g_anchors[b], O.topk_anchors(ref, K), ref, K, TOL[dt])
-        assert_overlap(ov, ref, K, TOL[dt], f"HKVD request {b}")
         np.testing.assert_array_equal(g_anchors[b], O.topk_anchors(g_scores[b], K))
+        full = O.full_refresh(layers[:n + 1], dims, oc.req(b))
+        gk = _pool_rows(s.batch.k_pools[n], fresh_slots[b], w)
+        gv = _pool_rows(s.batch.v_pools[n], fresh_slots[b], w)
+        assert_close(gk, full.views_k[n][aff], dt, f"HKVD full-prompt K layer {n} request {b}")
+        assert_close(gv, full.views_v[n][aff], dt, f"HKVD full-prompt V layer {n} request {b}")
+        ref = O.kv_deviation(gk, gv, sk[n], sv[n])
+        # fp32 arithmetic on the same inputs: the fp32 bar
+        e = assert_close(g_scores[b], ref, "f32", f"KV deviation request {b}")
+        check_anchors(g_anchors[b], ref, K, e["max_abs"], f"{w.name} HKVD request {b}")
+        exact = O.hkvd_scores(layers, dims, oc.req(b), sk, sv)
+        ov = len(set(g_anchors[b].tolist()) & set(O.topk_anchors(exact, K).tolist())) / max(K, 1)
+        print(f"[anchors] {w.name} HKVD request {b}: overlap with the all-fp64 selection {ov:.4f}", flush=True)
 
 
 def test_anchor_stale_poison_and_determinism(case):
@@ -322,10 +338,10 @@ def test_anchor_stale_poison_and_determinism(case):
     repeated runs are bit-identical."""
     import torch
     w, s, layers, sk, sv, oc = case
-    anchors, scores = s.batch.select_anchors(w.n_anchors)
-    anchors2, scores2 = s.batch.select_anchors(w.n_anchors)
+    anchors, scores = s.batch.select_anchors(anchor_count(w))
+    anchors2, scores2 = s.batch.select_anchors(anchor_count(w))
     assert torch.equal(scores, scores2) and torch.equal(anchors, anchors2)
-    x_a, _ = s.batch.refresh(anchors, w.n_anchors)
+    x_a, _ = s.batch.refresh(anchors, anchor_count(w))
     ref = down_bits(x_a).copy()
     if w.batch == 1:
         a = anchors[0].long()
@@ -333,12 +349,12 @@ def test_anchor_stale_poison_and_determinism(case):
         for k, v in zip(s.batch.k_pools, s.batch.v_pools):
             k[a] = float("nan")
             v[a] = float("nan")
-        x_p, _ = s.batch.refresh(anchors, w.n_anchors)
+        x_p, _ = s.batch.refresh(anchors, anchor_count(w))
         for (k0, v0), k, v in zip(saved, s.batch.k_pools, s.batch.v_pools):
             k[a] = k0
             v[a] = v0
         np.testing.assert_array_equal(down_bits(x_p), ref)
-    x_b, _ = s.batch.refresh(anchors, w.n_anchors)
+    x_b, _ = s.batch.refresh(anchors, anchor_count(w))
     np.testing.assert_array_equal(down_bits(x_b), ref)
 
 
@@ -357,8 +373,8 @@ def test_materialized_chain_against_oracle_chain(case):
         k[:L] = k0
         v[:L] = v0
     try:
-        anchors, scores = s.batch.select_anchors(w.n_anchors)
-        x, m = s.batch.refresh(anchors, w.n_anchors)
+        anchors, scores = s.batch.select_anchors(anchor_count(w))
+        x, m = s.batch.refresh(anchors, anchor_count(w))
         g_scores, g_anchors, gx = down(scores), anchors.cpu().numpy(), down(x)
         pos = m["row_pos"].cpu().numpy()
     finally:
@@ -367,15 +383,50 @@ def test_materialized_chain_against_oracle_chain(case):
             v[:L] = v0
     sk64, sv64 = s.host["stale64"]
     dims = oracle_dims(w)
-    R = w.rows_selective
+    R = rows_selective(w)
+    K = anchor_count(w)
     overlaps = []
     for b in range(w.batch):
         req = oc.req(b)
-        a_ref, pr = O.select_anchors(layers, dims, req, sk64, sv64, w.n_anchors)
-        assert_close(g_scores[b], pr.scores, dt, f"scores request {b}")
-        overlaps.append(anchors_agree(g_anchors[b], a_ref, pr.scores, w.n_anchors, TOL[dt]))
-        ref = O.selective_refresh(layers, dims, req, a_ref, sk64, sv64)
+        a_ref, pr = O.select_anchors(layers, dims, req, sk64, sv64, K)
+        e = assert_close(g_scores[b], pr.scores, dt, f"scores request {b}")
+        overlaps.append(check_anchors(g_anchors[b], pr.scores, K, e["max_abs"], f"{w.name} independent chain {b}"))
+        # the refresh with the anchor set the GPU chose (the choice itself is
+        # gated just above): a swapped anchor changes which keys the rows read
+        ref = O.selective_refresh(layers, dims, req, g_anchors[b], sk64, sv64)
         keep = np.isin(pos[b * R:(b + 1) * R], req.nonaffix)
         assert_close(gx[b * R:(b + 1) * R][keep], ref.x[np.isin(ref.rows, req.nonaffix)], dt, f"rows request {b}")
     print(f"\n{w.name}: anchor overlap with the oracle chain {overlaps}")
-    assert min(overlaps) >= 0.95
+
+
+def test_refresh_error_is_that_of_bf16_storage(case):
+    """The GPU refresh loses no more accuracy than bf16 storage itself: exact
+    arithmetic that rounds to bf16 where the GPU path stores a value
+    (tests/bf16_reference.py), through every layer on the same inputs and
+    anchors, has about the same error against the fp64 oracle."""
+    from tests.bf16_reference import layer_forward_bf16
+    w, s, layers, sk, sv, oc = case
+    if w.dims.dtype != "bf16":
+        pytest.skip("the bf16 storage model applies to the bf16 path")
+    dims = oracle_dims(w)
+    R = rows_selective(w)
+    anchors = [oc.anchors(b) for b in range(w.batch)]
+    x, _ = s.batch.refresh(up_i32(np.stack(anchors)), anchor_count(w))
+    gx = down(x)
+    S = w.layout.seq_len
+    for b in range(w.batch):
+        req = oc.req(b)
+        ref = oc.selective(b)
+        rows = ref.rows
+        xe = req.x0[rows]
+        for n, lw in enumerate(layers):
+            vk = np.zeros((S, w.dims.n_kv_heads, w.dims.head_dim))
+            vv = np.zeros_like(vk)
+            vk[req.affix], vv[req.affix] = sk[n], sv[n]
+            xe = layer_forward_bf16(lw, dims, xe, req.pos[rows], rows, vk, vv)
+        e_gpu = errors(gx[b * R:(b + 1) * R], ref.x)
+        e_emu = errors(xe, ref.x)
+        print(f"[bf16 floor] {w.name} request {b}: GPU rms_rel {e_gpu['rms_rel']:.3e} elem_rel {e_gpu['elem_rel']:.3e}"
+              f"  bf16 storage rms_rel {e_emu['rms_rel']:.3e} elem_rel {e_emu['elem_rel']:.3e}", flush=True)
+        assert e_gpu["rms_rel"] <= 1.25 * e_emu["rms_rel"], (e_gpu, e_emu)
+        assert e_gpu["max_rel"] <= 1.5 * e_emu["max_rel"] + 1e-4, (e_gpu, e_emu)

@@ -12,7 +12,9 @@ from .gen import (
     draw_donor_rows,
     draw_embedding,
     draw_hidden_rows,
+    draw_layer_qkv,
     draw_layer_weights,
+    layer_norm_gains,
     draw_lm_head,
     draw_noise,
     draw_scores,
@@ -35,7 +37,9 @@ __all__ = [
     "draw_donor_rows",
     "draw_embedding",
     "draw_hidden_rows",
+    "draw_layer_qkv",
     "draw_layer_weights",
+    "layer_norm_gains",
     "draw_noise",
     "draw_scores",
     "draw_ints",

@@ -8,7 +8,9 @@ stack.  Generation length 256 and block length 32 follow the paper's
 default settings (Section 5, "Default Settings"); affix lengths are chosen
 per workload because the paper does not report token counts.
 
-The anchor count is K = floor(rho * L + 1/2), clamped to [0, L].
+A workload names its anchor ratio rho; the anchor count K it implies is the
+method's arithmetic and lives on each side (the library and the oracle),
+not here.
 """
 
 from __future__ import annotations
@@ -65,11 +67,6 @@ class SeqLayout:
         return [p for p in range(self.seq_len) if not (self.affix_begin <= p < self.affix_end)]
 
 
-def anchor_count(ratio: float, affix_len: int) -> int:
-    k = int(ratio * affix_len + 0.5)
-    return max(0, min(affix_len, k))
-
-
 @dataclass(frozen=True)
 class Workload:
     name: str
@@ -82,14 +79,6 @@ class Workload:
     mask_rows: str = "random"  # "random": N(0,1) per masked row; "shared": one mask vector
     ratios: Tuple[float, ...] = field(default=())
     decode_block: int = 0  # serving schedule: commit the masked span in blocks of this many tokens (0: none)
-
-    @property
-    def n_anchors(self) -> int:
-        return anchor_count(self.ratio, self.layout.affix_len)
-
-    @property
-    def rows_selective(self) -> int:
-        return self.n_anchors + self.layout.n_nonaffix
 
     def with_ratio(self, ratio: float) -> "Workload":
         return replace(self, ratio=ratio)

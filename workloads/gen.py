@@ -92,19 +92,32 @@ class LayerWeightsBits:
     w_down: np.ndarray
 
 
-def draw_layer_weights(w: Workload, layer: int, std: float = 0.02) -> LayerWeightsBits:
+def _layer_shapes(w: Workload):
     d = w.dims
-    hd = d.head_dim
-    shapes = [
+    return [
         (d.qkv_width, d.d_model),
-        (d.d_model, d.n_heads * hd),
+        (d.d_model, d.n_heads * d.head_dim),
         (2 * d.d_ff, d.d_model),
         (d.d_model, d.d_ff),
     ]
-    mats = [_store(_normal_f32(s, std, w.seed_id, 0, layer, i), d.dtype) for i, s in enumerate(shapes)]
-    ones = _store(np.ones(d.d_model, dtype=np.float32), d.dtype)
+
+
+def draw_layer_qkv(w: Workload, layer: int, std: float = 0.02) -> np.ndarray:
+    """w_qkv of one layer alone: the same bits draw_layer_weights returns."""
+    return _store(_normal_f32(_layer_shapes(w)[0], std, w.seed_id, 0, layer, 0), w.dims.dtype)
+
+
+def draw_layer_weights(w: Workload, layer: int, std: float = 0.02) -> LayerWeightsBits:
+    d = w.dims
+    mats = [_store(_normal_f32(s, std, w.seed_id, 0, layer, i), d.dtype) for i, s in enumerate(_layer_shapes(w))]
+    ones = layer_norm_gains(w)
     return LayerWeightsBits(attn_norm=ones, w_qkv=mats[0], w_o=mats[1], mlp_norm=ones.copy(),
                             w_gate_up=mats[2], w_down=mats[3])
+
+
+def layer_norm_gains(w: Workload) -> np.ndarray:
+    """The RMSNorm gains of every layer: ones."""
+    return _store(np.ones(w.dims.d_model, dtype=np.float32), w.dims.dtype)
 
 
 def draw_hidden_rows(w: Workload, n_req: Optional[int] = None) -> np.ndarray:
