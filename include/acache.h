@@ -149,6 +149,27 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
                            hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * acache_score_noalloc — acache_score without a workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, kernels and
+ * results as acache_score, bit for bit.  Its scratch (the per-row
+ * log-sum-exp and per-head column sums) is a fixed array in the library's
+ * device memory, one per GPU, held until the process ends; the call neither
+ * allocates nor frees.  Limit: cu_q[batch] * H * 4 + batch * H * affix_len * 4
+ * bytes (each rounded up to 256) must not exceed
+ * acache_score_noalloc_max_bytes() (64 MiB), else ACACHE_ERR_WORKSPACE with
+ * nothing enqueued.  Every call on one GPU uses that GPU's one scratch:
+ * calls that overlap on one GPU (other streams, other threads) race; calls
+ * ordered on one stream do not.  The first call on a device resolves the
+ * scratch address on that device (the device must be current). */
+acache_status acache_score_noalloc(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                                   int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
+                                   const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                                   const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
+                                   acache_norm norm, float* scores, hipStream_t stream);
+size_t acache_score_noalloc_max_bytes(void);
+
+/* ---------------------------------------------------------------------------
  * acache_anchor_count — the K of Eq. 6 for anchor ratio `ratio` over an affix
  * of affix_len tokens: the integer nearest to ratio * affix_len, a half
  * rounded up (the paper states no rounding; 0.2 of 128 tokens is 26), within

@@ -66,6 +66,7 @@ def _load():
     PI = ctypes.POINTER(ctypes.c_int32)
     sig = {
         "acache_score": [ctypes.POINTER(Dims), I32, P, I64, I64, P, PI, P, I64, I64, P, I32, P, I32, P, P, SZ, P],
+        "acache_score_noalloc": [ctypes.POINTER(Dims), I32, P, I64, I64, P, PI, P, I64, I64, P, I32, P, I32, P, P],
         "acache_topk": [P, I32, I32, I32, P, P],
         "acache_gather_rows": [P, I64, I64, P, P, I64, I32, I32, P, I64, P],
         "acache_kv_scatter": [P, P, I64, I32, P, P, P, I64, I64, I32, I32, P],
@@ -101,6 +102,8 @@ def _load():
     lib.acache_status_string.argtypes = [ctypes.c_int32]
     lib.acache_status_string.restype = ctypes.c_char_p
     lib.acache_version.restype = ctypes.c_int32
+    lib.acache_score_noalloc_max_bytes.argtypes = []
+    lib.acache_score_noalloc_max_bytes.restype = ctypes.c_size_t
     lib.acache_anchor_count.argtypes = [ctypes.c_double, I32]
     lib.acache_anchor_count.restype = ctypes.c_int32
     return lib
@@ -314,6 +317,22 @@ def acache_score(dims: Dims, q: torch.Tensor, q_rows: torch.Tensor, cu_q, k_pool
         ctypes.byref(dims), batch, _ptr(q), q.stride(0), q.shape[0], _ptr(q_rows), cq, _ptr(k_pool),
         k_pool.stride(0), k_pool.shape[0], _ptr(affix_slots), L, _ptr(row_lse), norm, _ptr(scores),
         _ptr(ws), ws.numel(), _stream(stream)))
+    return scores
+
+
+def acache_score_noalloc(dims: Dims, q: torch.Tensor, q_rows: torch.Tensor, cu_q, k_pool: torch.Tensor,
+                         affix_slots: torch.Tensor, scores: torch.Tensor, norm: int = ACACHE_NORM_AFFIX,
+                         row_lse: Optional[torch.Tensor] = None, stream=None):
+    """acache_score with the library's fixed scratch instead of a workspace."""
+    _dev_i32(q_rows, "q_rows")
+    _dev_i32(affix_slots, "affix_slots")
+    batch = len(cu_q) - 1
+    L = affix_slots.numel()
+    cq = _i32(cu_q)
+    _check("acache_score_noalloc", lib.acache_score_noalloc(
+        ctypes.byref(dims), batch, _ptr(q), q.stride(0), q.shape[0], _ptr(q_rows), cq, _ptr(k_pool),
+        k_pool.stride(0), k_pool.shape[0], _ptr(affix_slots), L, _ptr(row_lse), norm, _ptr(scores),
+        _stream(stream)))
     return scores
 
 

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "internal.h"
 
@@ -195,6 +196,31 @@ acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, co
                                    (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
                                    colsum, s));
   LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, H, L, scores, init, s));
+  return ACACHE_OK;
+}
+
+// Device memory of acache_score_noalloc: the library's own fixed scratch
+// (one copy per GPU, held until the process ends).  Host code never names
+// the array directly: its device address comes from hipGetSymbolAddress,
+// once per device, on the first call on that device.
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+__device__ __align__(256) char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address, resolved on its first use.
+acache_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ACACHE_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return ACACHE_ERR_DEVICE;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return ACACHE_OK;
 }
 
@@ -472,7 +498,7 @@ acache_status acache_attention(const acache_dims* dims, const acache_ragged* rg,
   return ACACHE_OK;
 }
 
-// Host checks of acache_score.  Sets *noop when the
+// Host checks of acache_score and acache_score_noalloc.  Sets *noop when the
 // call has nothing to do.
 static acache_status check_score(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
                                  int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q, const void* k_pool,
@@ -517,6 +543,29 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
                    stream);
 }
 
+acache_status acache_score_noalloc(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
+                                   int64_t q_n_rows, const int32_t* q_rows, const int32_t* cu_q,
+                                   const void* k_pool, int64_t pool_ld, int64_t n_slots,
+                                   const int32_t* affix_slots, int32_t affix_len, const float* row_lse,
+                                   acache_norm norm, float* scores, hipStream_t stream) {
+  bool noop = true;
+  acache_status st = check_score(dims, batch, q, q_ld, q_n_rows, q_rows, cu_q, k_pool, pool_ld, n_slots,
+                                 affix_slots, affix_len, row_lse, norm, scores, &noop);
+  if (st != ACACHE_OK || noop) return st;
+  // the lse and column-sum regions, laid out as in a workspace, must fit the
+  // fixed scratch; both are written in full before they are read, so the
+  // previous call's contents need no clearing
+  const size_t lse_bytes = align_up((size_t)cu_q[batch] * dims->n_heads * sizeof(float));
+  const size_t colsum_bytes = align_up((size_t)batch * dims->n_heads * (size_t)affix_len * sizeof(float));
+  CHECK(lse_bytes + colsum_bytes <= kNoallocScratchBytes, ACACHE_ERR_WORKSPACE);
+  void* base = nullptr;
+  st = scratch_address(&base);
+  if (st != ACACHE_OK) return st;
+  return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
+                   affix_len, norm, row_lse, scores, at<float>(base, 0), at<float>(base, lse_bytes), 0, stream);
+}
+
+size_t acache_score_noalloc_max_bytes(void) { return kNoallocScratchBytes; }
 
 acache_status acache_layer_schedule(const acache_dims* dims, int32_t rows, int32_t* o_splits, int32_t* down_splits) {
   acache_status st = check_layer_dims(dims);
