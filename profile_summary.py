@@ -1,0 +1,171 @@
+"""Summaries of rocprofv3 runs of bench.py for profiles/ (runs on the host, no GPU).
+
+    python profile_summary.py stats   RUN_DIR NAME BENCH_JSON OUT_TXT "COMMAND" [--steps N]
+    python profile_summary.py traffic FETCH_CSV WRITE_CSV COPY_FETCH_CSV COPY_WRITE_CSV WORKLOAD OUT_TXT \
+                                      "STEP_COMMAND" "COPY_COMMAND" [--steps N] [--copy-mib M]
+
+stats: the kernel statistics of a `rocprofv3 --kernel-trace --stats` run
+(RUN_DIR/NAME_kernel_stats.csv), and, from its kernel trace, the mean
+duration of the dominant kernel's launches over the run's last N steps
+beside bench.py's HIP-event figure for the same launches.
+
+traffic: HBM bytes per launch of each operation of the step from two
+`--pmc FETCH_SIZE` / `--pmc WRITE_SIZE` passes, scaled by what the same
+counters read for the row-gather kernel copying M MiB (bench.py
+--copy-calibration M); written to profiles/traffic.json (keyed by workload
+and operation, with the digest of the kernel sources they were taken on)
+and OUT_TXT.
+
+A step holds one top-K launch, between its probe and its refresh.  The
+run's last N steps are taken as the span from the launch after the
+(N+1)-th last top-K to the last top-K: N refreshes and N probes of
+identical steps.
+"""
+
+from __future__ import annotations
+
+import csv
+import json
+import os
+import re
+import sys
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+# operation -> (kernel-name patterns summed per launch unit, pattern that counts units)
+OPERATIONS = {
+    "gemm_gate_up": ([r"gemm_bf16_kernel<4,", r"gemm_bf16_fixup<4,"], r"gemm_bf16_kernel<4,"),
+    "gemm_qkv": ([r"gemm_bf16_kernel<3,", r"gemm_bf16_fixup<3,"], r"gemm_bf16_kernel<3,"),
+    "gemm_accum": ([r"gemm_bf16_kernel<1,", r"gemm_bf16_fixup<1,"], r"gemm_bf16_kernel<1,"),
+    "gemm_partial": ([r"gemm_bf16_kernel<2,"], r"gemm_bf16_kernel<2,"),
+    "attention": ([r"attention_pv_kernel", r"attention_merge_kernel"], r"attention_pv_kernel"),
+    "score_lse": ([r"attention_kernel<false"], r"attention_kernel<false"),
+    "score_colsum": ([r"colsum_kernel"], r"colsum_kernel"),
+    "rmsnorm": ([r"rmsnorm_vec_kernel", r"rmsnorm_rows_kernel"], r"rmsnorm_(vec|rows)_kernel"),
+    "residual": ([r"reduce_residual_kernel", r"q_rotary_reduce_kernel"], r"(reduce_residual|q_rotary_reduce)_kernel"),
+    "gather": ([r"gather_rows_kernel"], r"gather_rows_kernel"),
+}
+# bench.py's kernel names -> the operation whose launches it times
+BENCH_KERNEL = {"gemm_gate_up": "gemm_gate_up", "gemm_qkv": "gemm_qkv", "attention": "attention"}
+
+
+def short(name: str) -> str:
+    n = name.replace("acache::(anonymous namespace)::", "").replace("acache::", "").replace("void ", "")
+    return re.sub(r"\(.*\)$", "", n)[:90]
+
+
+def _rows(path):
+    return list(csv.DictReader(open(path)))
+
+
+def _col(row, *names):
+    for n in names:
+        if n in row:
+            return row[n]
+    raise KeyError(names)
+
+
+def _segment(rows, steps):
+    """Rows of the last `steps` steps (see the module docstring)."""
+    topk = [i for i, r in enumerate(rows) if "topk_kernel" in _col(r, "Kernel_Name", "Name")]
+    if len(topk) < steps + 1:
+        raise SystemExit(f"only {len(topk)} top-K launches; need {steps + 1}")
+    return rows[topk[-steps - 1] + 1:topk[-1] + 1]
+
+
+def stats(argv):
+    run_dir, name, bench_json, out, cmd = argv[:5]
+    steps = int(argv[argv.index("--steps") + 1]) if "--steps" in argv else 3
+    st = _rows(os.path.join(run_dir, f"{name}_kernel_stats.csv"))
+    bench = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    lines = [f"# rocprofv3 kernel statistics: {bench['config']['workload']} step", "",
+             "command (from the repository root on the GPU box):", f"  {cmd}", "",
+             f"{'kernel':92s} {'calls':>6s} {'avg_us':>10s} {'min_us':>9s} {'max_us':>9s} {'total_ms':>9s} {'pct':>6s}"]
+    for r in st:
+        lines.append(f"{short(r['Name']):92s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:10.2f} "
+                     f"{float(r['MinNs']) / 1e3:9.2f} {float(r['MaxNs']) / 1e3:9.2f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:9.3f} {float(r['Percentage']):6.2f}")
+    lines += ["", "The calls include the setup (the shared cache's materialisation), the warmup steps and the",
+              "timed steps."]
+    trace = os.path.join(run_dir, f"{name}_kernel_trace.csv")
+    roof = bench["roofline"]
+    op = BENCH_KERNEL.get(roof["kernel"])
+    if os.path.exists(trace) and op:
+        seg = _segment(_rows(trace), steps)
+        pats, unit = OPERATIONS[op]
+        durs, n_units = [], 0
+        for r in seg:
+            k = _col(r, "Kernel_Name", "Name")
+            if any(re.search(p, k) for p in pats):
+                d = int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))
+                if re.search(unit, k):
+                    durs.append(d)
+                    n_units += 1
+                else:
+                    durs[-1] += d
+        mean = sum(durs) / max(n_units, 1) / 1e3
+        lines += ["", f"Dominant kernel ({roof['kernel']}): {n_units} launches in the last {steps} steps of the trace "
+                  f"({n_units / steps:g} per step), mean {mean:.2f} us per launch (a stream-K launch counts its fixup);",
+                  f"bench.py's HIP events over its own timed region: {roof['mean_launch_us']:.2f} us "
+                  f"({100 * (roof['mean_launch_us'] / mean - 1):+.1f}%)."]
+    lines += ["", "bench.py line of the same run (timed region, HIP events):", json.dumps(bench)]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines[:40]))
+
+
+def traffic(argv):
+    fetch, write, cfetch, cwrite, workload, out, step_cmd, copy_cmd = argv[:8]
+    steps = int(argv[argv.index("--steps") + 1]) if "--steps" in argv else 1
+    mib = int(argv[argv.index("--copy-mib") + 1]) if "--copy-mib" in argv else 256
+    sys.path.insert(0, ROOT)
+    from paper_2608_26140_amd.build import source_digest
+
+    def copy_mean(path):
+        v = [float(_col(r, "Counter_Value")) for r in _rows(path) if "gather_rows_kernel" in _col(r, "Kernel_Name")]
+        return sum(v) / len(v)
+
+    n = mib * (1 << 20) // 8192
+    read_b, write_b = n * 8192 + 4 * n, n * 8192
+    rs = read_b / (copy_mean(cfetch) * 1024)
+    ws = write_b / (copy_mean(cwrite) * 1024)
+
+    def per_unit(path, pats, unit):
+        seg = _segment(_rows(path), steps)
+        tot, units = 0.0, 0
+        for r in seg:
+            k = _col(r, "Kernel_Name")
+            if any(re.search(p, k) for p in pats):
+                tot += float(_col(r, "Counter_Value"))
+                units += bool(re.search(unit, k))
+        return tot / max(units, 1), units / steps
+
+    lines = [f"# HBM traffic per launch: {workload} step (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
+             "commands (from the repository root on the GPU box), one pass per counter (C = FETCH_SIZE, WRITE_SIZE):",
+             f"  {step_cmd}", f"  {copy_cmd}", "",
+             f"calibration: gather_rows_kernel identity copy of {mib} MiB reads {read_b} B, writes {write_b} B per launch;",
+             f"  FETCH_SIZE reads {copy_mean(cfetch):.0f} KiB -> read scale {rs:.4f}; "
+             f"WRITE_SIZE {copy_mean(cwrite):.0f} KiB -> write scale {ws:.4f}", "",
+             f"Launches of the last {steps} step(s); a stream-K GEMM launch counts its fixup kernel, attention its",
+             "key-split merge kernel.", "",
+             f"{'operation':14s} {'per step':>8s} {'fetch_KiB':>11s} {'write_KiB':>11s} {'MB/launch':>10s}"]
+    tfile = os.path.join(ROOT, "profiles", "traffic.json")
+    rec = json.load(open(tfile)) if os.path.exists(tfile) else {}
+    rec = {k: v for k, v in rec.items() if not k.startswith(workload + ":")}
+    for op, (pats, unit) in OPERATIONS.items():
+        fk, per = per_unit(fetch, pats, unit)
+        wk, _ = per_unit(write, pats, unit)
+        if per == 0:
+            continue
+        b = fk * 1024 * rs + wk * 1024 * ws
+        lines.append(f"{op:14s} {per:8g} {fk:11.0f} {wk:11.0f} {b / 1e6:10.1f}")
+        rec[f"{workload}:{op}"] = {"source_digest": source_digest(), "bytes_per_launch": round(b),
+                                   "fetch_kib_per_launch": round(fk, 1), "write_kib_per_launch": round(wk, 1),
+                                   "read_scale": round(rs, 4), "write_scale": round(ws, 4)}
+    lines.append(f"\nsource digest of the measured kernels: {source_digest()}")
+    json.dump(rec, open(tfile, "w"), indent=1)
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+if __name__ == "__main__":
+    {"stats": stats, "traffic": traffic}[sys.argv[1]](sys.argv[2:])
