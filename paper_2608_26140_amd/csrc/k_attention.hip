@@ -740,34 +740,432 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
   if (lse && c == 0) lse[pair] = (m + __log2f(l)) * kLn2;
 }
 
+
+// ============================================================================
+// Read-slot attention, wide query tiles (the recompute's large row counts).
+//
+// A workgroup holds 32 QB WAVES queries of one head: WAVES wavefronts of QB
+// 32-query MFMA blocks each, one workgroup per CU.  The 128 KB of LDS hold a
+// ring of four 64-key stages (K + V tiles), filled by buffer -> LDS copies
+// issued from inline assembly three tiles ahead of the tile being finished
+// (the compiler's wait analysis does not see them and does not drain them
+// before each LDS read; the kernel waits for them itself with vmcnt,
+// counting a fixed number of copies per tile).  The slot indices of a tile
+// are copied to LDS the same way one tile earlier still.  Keys past the
+// request's end and out-of-range slots take a buffer offset beyond the
+// pool, which loads zeros.
+//
+// The tile loop is software pipelined: iteration t computes S(t+1) = K Q^T
+// of the next tile while it exponentiates tile t's logits, then O += V P of
+// tile t while it takes the row maxima of tile t+1, so matrix and vector
+// work are independent within each half of the iteration.  The running max
+// moves only when a tile exceeds it by more than 2^8 (lazy rescale), after
+// tile t's P V has been added.  Per query the keys are visited in the same
+// order and tiles, with the same MFMA sequences, as attention_pv_kernel, so
+// the two kernels give the same bits.
+//
+// Measured (8 wavefronts of 32 queries, two per SIMD, against
+// attention_pv_kernel's two 128-query workgroups per CU): 9-15% faster for
+// the probe's 512 rows and the Dream-shaped refresh, equal for the serving
+// refresh, slower for grids that fill less than one round (fewer,
+// longer-lived workgroups).  Four wavefronts of 64 queries halve the LDS
+// reads per MFMA but run one wavefront per SIMD, and lose: LDS throughput
+// and the overlap of matrix and vector work need two wavefronts per SIMD.
+// ============================================================================
+
+typedef uint32_t rsrc_words __attribute__((ext_vector_type(4)));
+
+// Raw buffer descriptor over [base, base + bytes) in SGPRs (stride 0: loads
+// at or past `bytes` return zeros).
+__device__ __forceinline__ rsrc_words buffer_words(const void* base, uint32_t bytes) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  rsrc_words w;
+  w.x = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  w.y = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32) & 0xFFFFu);
+  w.z = __builtin_amdgcn_readfirstlane(bytes);
+  w.w = 0x00020000u;
+  return w;
+}
+// 16 bytes per lane, buffer -> LDS at lds + 16 * lane (lds wave-uniform).
+__device__ __forceinline__ void dma16_asm(rsrc_words r, uint32_t voff, const char* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(m0) : "memory");
+}
+// 4 bytes per lane, buffer -> LDS at lds + 4 * lane.
+__device__ __forceinline__ void dma4_asm(rsrc_words r, uint32_t voff, const char* lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("buffer_load_dword %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(m0) : "memory");
+}
+// s_waitcnt vmcnt(N) that the compiler cannot move memory accesses across.
+template <int N>
+__device__ __forceinline__ void wait_vm_asm() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+constexpr int kWdStages = 4;                     // K + V stages in the ring
+constexpr int kWdSlotB = kTileK * 4;             // one tile's slot indices
+// buffer offset of an absent key: past every pool the launcher admits
+// (n_slots * pool_ld * 2 <= kWdAbsent), so its loads return zeros
+constexpr uint32_t kWdAbsent = 0xF0000000u;
+
+// QB 32-query blocks per wavefront, WAVES wavefronts: 32 QB WAVES queries
+// per workgroup.
+template <int QB, int WAVES>
+struct WideCfg {
+  static constexpr int kTileQ = 32 * QB * WAVES;
+  static constexpr int kThreads = 64 * WAVES;
+  static constexpr int kDma = kTileB / 1024 / WAVES;  // 1 KB K (and V) copies per wave and tile
+  static constexpr int kOps = 2 * kDma;               // K/V copies per wave and tile
+  static constexpr int kKeysPerWave = kTileK / WAVES;
+  static_assert(kDma * WAVES * 1024 == kTileB && kKeysPerWave == 4 * kDma, "copy split");
+};
+
+template <int QB, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa) {
+  using C = WideCfg<QB, WAVES>;
+
+  __shared__ __attribute__((aligned(1024))) char ring[kWdStages * kStageB];
+  __shared__ __attribute__((aligned(16))) char slot_ring[WAVES * 4 * kWdSlotB];
+  const AttnArgs& a = pa.a;
+  const int splits = pa.splits;
+
+  // XCD-contiguous, head-major order of (head, query tile, key split)
+  const int n_tiles_q = a.tile_start[a.batch];
+  int h, tile, split;
+  {
+    const int nb = gridDim.x, i = blockIdx.x;
+    const int q8 = nb >> 3, r8 = nb & 7, x = i & 7;
+    const int t = x * q8 + min(x, r8) + (i >> 3);
+    h = t / (n_tiles_q * splits);
+    const int rem = t - h * n_tiles_q * splits;
+    tile = rem / splits;
+    split = rem - tile * splits;
+  }
+  int b = 0;
+  {
+    int lo = 0, hi = a.batch - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+  }
+  const int g = h / (a.H / a.Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, hl = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n_rows = a.row_start[b + 1] - a.row_start[b];
+  const int q0 = (tile - a.tile_start[b]) * C::kTileQ + wave * 32 * QB;
+  int qi[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) qi[qb] = q0 + 32 * qb + (lane & 31);
+  const bool live = q0 < n_rows;  // wave-uniform: a wave without a valid query only copies
+  const int S = a.key_len[b];
+  const int n_kt = (S + kTileK - 1) / kTileK;
+  const int t_lo = split * n_kt / splits, t_hi = (split + 1) * n_kt / splits;
+
+  // query fragments of the 32-query blocks: Q[q][16 s + 8 hl .. +7]
+  bf16x8 qf[QB][8];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const bool ok = qi[qb] < n_rows;
+    const int64_t qrow = ok ? (int64_t)a.row_start[b] + qi[qb] : 0;
+    const bf16* qp = a.q + qrow * a.q_ld + h * kDh + hl * 8;
+#pragma unroll
+    for (int s2 = 0; s2 < 8; ++s2) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (ok) v = *reinterpret_cast<const u32x4*>(qp + s2 * 16);
+      qf[qb][s2] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  const uint32_t pool_bytes = (uint32_t)(a.n_slots * a.pool_ld * 2);  // < 2^31 (host check)
+  const rsrc_words kres = buffer_words(a.k_pool, pool_bytes);
+  const rsrc_words vres = buffer_words(a.v_pool, pool_bytes);
+  const rsrc_words sres = buffer_words(a.slots + a.key_start[b], (uint32_t)S * 4u);
+  const int pch = lane & 15;
+  const uint32_t head_b = (uint32_t)g * kRowB;
+  const uint32_t ld_b = (uint32_t)a.pool_ld * 2u;
+  char* const my_slots = slot_ring + wave * 4 * kWdSlotB;
+
+  // the slot indices of tile t (all 64 keys) into this wave's entry t % 4
+  auto issue_slots = [&](int t) {
+    dma4_asm(sres, (uint32_t)(t * kTileK + lane) * 4u, my_slots + (t & 3) * kWdSlotB);
+  };
+  // K and V rows of tile t into stage t % 4: this lane's keys (64 / WAVES)
+  // wave + 4 i + lane / 16, chunk lane % 16 (K chunks XOR-swizzled by row & 15, V by
+  // 2 (row & 3)); reads the tile's slot indices from LDS
+  auto issue_kv = [&](int t) {
+    char* st = ring + (t & 3) * kStageB;
+    const char* sl = my_slots + (t & 3) * kWdSlotB;
+    uint32_t off[C::kDma];
+#pragma unroll
+    for (int i = 0; i < C::kDma; ++i) {
+      const int kk = wave * C::kKeysPerWave + 4 * i + (lane >> 4);
+      const int key = t * kTileK + kk;
+      const int slot = *reinterpret_cast<const int*>(sl + kk * 4);
+      const bool ok = key < S && slot >= 0 && slot < a.n_slots;
+      off[i] = ok ? (uint32_t)slot * ld_b + head_b : kWdAbsent;
+    }
+#pragma unroll
+    for (int i = 0; i < C::kDma; ++i) {
+      const int r = (wave * C::kKeysPerWave + 4 * i + (lane >> 4)) & (kTileK - 1);
+      const int ck = pch ^ (r & 15), cv = pch ^ ((r & 3) << 1);
+      const int dst = (wave * C::kDma + i) * 1024;
+      dma16_asm(kres, off[i] + ck * 16, st + dst);
+      dma16_asm(vres, off[i] + cv * 16, st + kTileB + dst);
+    }
+  };
+
+  const float scale = kLog2e * rsqrtf((float)kDh);
+  const int krow = key_perm(lane & 31);
+  const int k_row_off = krow * kRowB;
+  const int k_sw = krow & 15;
+  const int vgrp = lane >> 4, gi = lane & 15;
+  const int v_key = 8 * (vgrp >> 1) + (gi >> 2);
+  const int v_chunk_lo = 2 * (vgrp & 1) + ((gi & 3) >> 1);
+  const int v_byte = (gi & 1) * 8;
+  const int v_sw = (gi >> 2) << 1;
+
+  // S^T of tile t for both query blocks: st[qb][kb], register r of key block
+  // kb holding key 32 kb + 16 (r / 8) + 8 hl + r % 8 of the tile
+  auto scores = [&](int t, f32x16 (&st)[QB][2]) {
+    const char* ks = ring + (t & 3) * kStageB;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[qb][kb][r] = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) {
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8*>(ks + kb * 32 * kRowB + k_row_off + (((2 * s2 + hl) ^ k_sw) << 4));
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) st[qb][kb] = mfma32x32x16(kf, qf[qb][s2], st[qb][kb]);
+      }
+    }
+  };
+  // keys of tile t past the end: -inf; returns the scaled row maxima
+  auto row_max = [&](int t, f32x16 (&st)[QB][2], float (&mx)[QB]) {
+    const int kt0 = t * kTileK;
+    const uint64_t drop = kt0 + kTileK <= S ? 0ull : ~0ull << (S - kt0);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float m = -INFINITY;
+      if (drop == 0ull) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) m = fmaxf(m, st[qb][kb][r]);
+      } else {
+        const uint32_t dw[2] = {(uint32_t)drop >> (8 * hl), (uint32_t)(drop >> 32) >> (8 * hl)};
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            st[qb][kb][r] = (dw[kb] >> (16 * (r >> 3) + (r & 7))) & 1u ? -INFINITY : st[qb][kb][r];
+            m = fmaxf(m, st[qb][kb][r]);
+          }
+      }
+      mx[qb] = fmaxf(m, __shfl_xor(m, 32)) * scale;
+    }
+  };
+
+  f32x16 o_acc[QB][4];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o_acc[qb][d][r] = 0.f;
+  float m_run[QB], l_part[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    m_run[qb] = -INFINITY;
+    l_part[qb] = 0.f;
+  }
+  // moves the running max of a block whose tile maximum exceeds it by more
+  // than 2^8, rescaling what has been accumulated
+  auto rescale = [&](const float (&mx)[QB]) {
+    bool any = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) any |= mx[qb] > m_run[qb] + 8.f;
+    if (__builtin_amdgcn_ballot_w64(any)) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const bool bp = mx[qb] > m_run[qb] + 8.f;
+        const float m_new = bp ? mx[qb] : m_run[qb];
+        const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
+        m_run[qb] = m_new;
+        l_part[qb] *= alpha;
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o_acc[qb][d][r] *= alpha;
+      }
+    }
+  };
+
+  constexpr int kOps = C::kOps;
+  f32x16 st_a[QB][2], st_b[QB][2];
+  float mx[QB];
+  if (t_lo < t_hi) {
+    // prologue: slot indices of the first three tiles, then their K/V rows
+    issue_slots(t_lo);
+    issue_slots(t_lo + 1);
+    issue_slots(t_lo + 2);
+    wait_vm_asm<2>();
+    issue_kv(t_lo);
+    wait_vm_asm<kOps + 1>();
+    issue_kv(t_lo + 1);
+    wait_vm_asm<2 * kOps>();
+    issue_slots(t_lo + 3);
+    issue_kv(t_lo + 2);
+    wait_vm_asm<2 * kOps + 1>();  // tile t_lo has landed in this wave
+    bare_barrier();
+    if (live) {
+      scores(t_lo, st_a);
+      row_max(t_lo, st_a, mx);
+      rescale(mx);
+    }
+  }
+  // one iteration: P(t) from cur, S(t+1) into nxt, O += V P(t), max of t+1
+  auto step = [&](int t, f32x16 (&cur)[QB][2], f32x16 (&nxt)[QB][2]) {
+    wait_vm_asm<kOps + 1>();  // tile t+1 has landed in this wave
+    bare_barrier();           // ... in every wave, and every wave is done with tile t-1
+    issue_slots(t + 4);
+    wait_vm_asm<kOps + 1>();  // the slot indices of tile t+3
+    issue_kv(t + 3);   // into the stage of tile t-1
+    if (!live) return;
+    // P(t): exp2 of the scaled logits against the running max, packed to bf16
+    bf16x8 pb[QB][2][2];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float psum = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int g2 = 0; g2 < 2; ++g2)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float e = __builtin_amdgcn_exp2f(fmaf(cur[qb][kb][8 * g2 + j], scale, -m_run[qb]));
+            psum += e;
+            pb[qb][kb][g2][j] = (bf16)e;
+          }
+      l_part[qb] += psum;
+    }
+    // S(t+1) unconditionally (past the range it reads a tile copied for
+    // nothing and is not used), so the block has no branch between the
+    // exponentials and these MFMAs
+    scores(t + 1, nxt);
+    // O^T += V^T P^T of tile t
+    const char* vs = ring + (t & 3) * kStageB + kTileB;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int g2 = 0; g2 < 2; ++g2) {
+        const int row0 = kb * 32 + g2 * 16 + v_key;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const int off = ((4 * d + v_chunk_lo) ^ v_sw) * 16 + v_byte;
+          const v4i16 lo = ds_read_tr16(vs + row0 * kRowB + off);
+          const v4i16 hi = ds_read_tr16(vs + (row0 + 4) * kRowB + off);
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o_acc[qb][d] = mfma32x32x16(vf, pb[qb][kb][g2], o_acc[qb][d]);
+        }
+      }
+    if (t + 1 < t_hi) {
+      row_max(t + 1, nxt, mx);
+      rescale(mx);
+    }
+  };
+  int t = t_lo;
+  for (; t + 1 < t_hi; t += 2) {
+    step(t, st_a, st_b);
+    step(t + 1, st_b, st_a);
+  }
+  if (t < t_hi) step(t, st_a, st_b);
+  // every copy this wave issued has landed before the workgroup ends
+  wait_vm_asm<0>();
+
+  if (!live) return;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float l_tot = l_part[qb] + __shfl_xor(l_part[qb], 32);
+    if (qi[qb] >= n_rows) continue;
+    const int64_t row = a.row_start[b] + qi[qb];
+    if (splits > 1) {
+      const int64_t prow = (int64_t)a.row_start[a.batch];
+      float* po = pa.part_o + (((int64_t)split * prow + row) * a.H + h) * kDh;
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          const f32x4 v = {o_acc[qb][d][4 * gq], o_acc[qb][d][4 * gq + 1], o_acc[qb][d][4 * gq + 2],
+                           o_acc[qb][d][4 * gq + 3]};
+          *reinterpret_cast<f32x4*>(po + d * 32 + 8 * gq + 4 * hl) = v;
+        }
+      if (hl == 0) {
+        float* pm = pa.part_ml + (((int64_t)split * prow + row) * a.H + h) * 2;
+        pm[0] = m_run[qb];
+        pm[1] = l_tot;
+      }
+      continue;
+    }
+    if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run[qb] + __log2f(l_tot)) * kLn2;
+    const float inv = 1.f / l_tot;
+    bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        bf16x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = (bf16)(o_acc[qb][d][4 * gq + j] * inv);
+        *reinterpret_cast<bf16x4*>(op + d * 32 + 8 * gq + 4 * hl) = w;
+      }
+  }
+}
+
 }  // namespace
 
 int attention_tile_rows() { return kTileQ; }
 
 
 // Key splits for the read-slot attention.  Cost in 64-key tiles of one
-// workgroup (about 1 us each): rounds of 512 resident workgroups (two per
-// CU) times the tiles per split, plus the merge traffic (each split's fp32
-// O and (m, l) written and read back at about 4 TB/s).  The partials must
-// fit in part_bytes.
-static int attention_splits(int n_wg, int n_kt, int64_t rows, int H, size_t part_bytes) {
+// 128-query workgroup (about 1 us each): rounds of `slots` resident
+// workgroups times the tiles per split times the cost of one tile, plus the
+// merge traffic (each split's fp32 O and (m, l) written and read back at
+// about 4 TB/s).  The partials must fit in part_bytes.  Returns the splits;
+// *cost receives the estimate.
+static int attention_splits(int n_wg, int slots, double tile_cost, int n_kt, int64_t rows, int H,
+                            size_t part_bytes, double* cost) {
   const int64_t per_split = rows * H * (kDh * 4 + 8);
   int best = 1;
   double best_cost = 1e30;
   for (int s = 1; s <= 8 && s <= n_kt; ++s) {
     if (s > 1 && (size_t)(per_split * s) > part_bytes) break;
-    const double rounds = (double)((n_wg * s + 511) / 512);
+    const double rounds = (double)((n_wg * s + slots - 1) / slots);
     const double tiles = (double)((n_kt + s - 1) / s);
     // merge: 2 x per_split x s bytes at ~4 TB/s, one 64-key tile of a workgroup ~1 us
     const double merge = s > 1 ? 2.0 * per_split * s / 4e12 / 1e-6 : 0.0;
-    const double cost = rounds * tiles + merge;
-    if (cost < best_cost) {
-      best_cost = cost;
+    const double c = rounds * tiles * tile_cost + merge;
+    if (c < best_cost) {
+      best_cost = c;
       best = s;
     }
   }
+  *cost = best_cost;
   return best;
 }
+
+// One 64-key tile of a 256-query workgroup of attention_wide_kernel (one
+// per CU), in units of a 128-query workgroup's tile (two per CU), measured.
+constexpr double kWideTileCost = 0.95;
+constexpr int kWideQB = 1, kWideWaves = 8;
+using WideQ = WideCfg<kWideQB, kWideWaves>;
 
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
@@ -795,20 +1193,38 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   }
   const int64_t rows = rg.cu_rows[rg.batch];
   if (rows == 0) return hipSuccess;
-  int tiles = 0, max_kt = 0;
+  int tiles = 0, tiles_w = 0, max_kt = 0;
   for (int b = 0; b < rg.batch; ++b) {
     a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
-    a.tile_start[b] = tiles;
-    tiles += (a.row_start[b + 1] - a.row_start[b] + kPvTileQ - 1) / kPvTileQ;
+    const int nr = a.row_start[b + 1] - a.row_start[b];
+    tiles += (nr + kPvTileQ - 1) / kPvTileQ;
+    tiles_w += (nr + WideQ::kTileQ - 1) / WideQ::kTileQ;
     max_kt = std::max(max_kt, (a.key_len[b] + kTileK - 1) / kTileK);
   }
-  a.tile_start[rg.batch] = tiles;
   if (tiles == 0) return hipSuccess;
-  const int splits = part ? attention_splits(tiles * H, max_kt, rows, H, part_bytes) : 1;
+  const size_t pbytes = part ? part_bytes : 0;
+  double cost_n = 0.0, cost_w = 0.0;
+  const int splits_n = attention_splits(tiles * H, 512, 1.0, max_kt, rows, H, pbytes, &cost_n);
+  const int splits_w = attention_splits(tiles_w * H, 256, kWideTileCost, max_kt, rows, H, pbytes, &cost_w);
+  // the wide kernel only where its workgroups fill at least one round of CUs
+  const bool wide = cost_w < cost_n && tiles_w * H * splits_w >= 256 &&
+                    (uint64_t)n_slots * (uint64_t)pool_ld * 2u <= (uint64_t)kWdAbsent;
+  const int tq = wide ? WideQ::kTileQ : kPvTileQ;
+  const int splits = wide ? splits_w : splits_n;
+  int acc_tiles = 0;
+  for (int b = 0; b < rg.batch; ++b) {
+    a.tile_start[b] = acc_tiles;
+    acc_tiles += (a.row_start[b + 1] - a.row_start[b] + tq - 1) / tq;
+  }
+  a.tile_start[rg.batch] = acc_tiles;
   pa.splits = splits;
   pa.part_o = part;
   pa.part_ml = part ? part + (size_t)splits * rows * H * kDh : nullptr;
-  hipLaunchKernelGGL(attention_pv_kernel<false>, dim3(tiles * H * splits), dim3(kPvThreads), 0, s, pa);
+  if (wide)
+    hipLaunchKernelGGL((attention_wide_kernel<kWideQB, kWideWaves>), dim3(acc_tiles * H * splits),
+                       dim3(WideQ::kThreads), 0, s, pa);
+  else
+    hipLaunchKernelGGL(attention_pv_kernel<false>, dim3(acc_tiles * H * splits), dim3(kPvThreads), 0, s, pa);
   if (splits > 1) {
     const int64_t pairs = rows * H;
     hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s,
@@ -855,8 +1271,10 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
   const int n_kt_shared = (L + kTileK - 1) / kTileK;
   if ((size_t)per_split * (shared ? 2 : 1) > part_bytes) return hipErrorInvalidValue;
   const int sp_priv = 1;
-  const int sp_shared =
-      shared ? attention_splits(q_tiles_all * H, n_kt_shared, rows, H, part_bytes - (size_t)per_split * sp_priv) : 0;
+  double cost_unused = 0.0;
+  const int sp_shared = shared ? attention_splits(q_tiles_all * H, 512, 1.0, n_kt_shared, rows, H,
+                                                  part_bytes - (size_t)per_split * sp_priv, &cost_unused)
+                               : 0;
   const int total = sp_shared + sp_priv;
 
   auto common = [&](PvArgs& pa) {

@@ -207,6 +207,35 @@ def test_attention(A, dtype, H, Hkv, dh, rows, keys):
     assert_close(down(lse), lse_ref, dtype, "attention lse")
 
 
+@pytest.mark.parametrize("H,Hkv,rows,keys", [
+    (32, 32, [1000, 700, 300], [900, 650, 130]),   # grids that pick the wide-tile kernel
+    (28, 4, [2304, 2560], [1300, 77]),
+])
+def test_attention_wide_tiles_and_absent_slots(A, H, Hkv, rows, keys):
+    """Launch shapes whose grid fills whole rounds of CUs (the launcher's
+    wide-tile kernel), ragged rows and keys, and some out-of-range slots:
+    those keys read zeros (logit 0, value 0)."""
+    torch = _torch()
+    dtype, dh = "bf16", 128
+    q, kp, vp, slots, cu_rows, cu_keys, n_slots = _attn_case(dtype, H, Hkv, dh, rows, keys, seed=sum(rows) + H)
+    bad = W.draw_permutation(len(slots), seed=7)[:9]
+    slots = slots.copy()
+    slots[bad[:5]] = -1
+    slots[bad[5:]] = n_slots + 3
+    dims = A.make_dims(4096, H, Hkv, dh, 128, dtype)
+    lse = torch.empty((sum(rows), H), dtype=torch.float32, device="cuda")
+    out = A.acache_attention(dims, cu_rows, cu_keys, up(q, dtype), up_i32(slots), up(kp, dtype), up(vp, dtype),
+                             lse=lse)
+    f = lambda a: O.from_bits(a, dtype)
+    # the oracle's view: an absent key is a zero row of the pools
+    kz = np.concatenate([f(kp).reshape(-1, Hkv, dh), np.zeros((1, Hkv, dh))])
+    vz = np.concatenate([f(vp).reshape(-1, Hkv, dh), np.zeros((1, Hkv, dh))])
+    sl = np.where((slots < 0) | (slots >= n_slots), n_slots, slots)
+    o_ref, lse_ref = O.attention_via_slots(f(q).reshape(-1, H, dh), kz, vz, sl, cu_rows, cu_keys)
+    assert_close(down(out), o_ref.reshape(sum(rows), H * dh), dtype, "attention out")
+    assert_close(down(lse), lse_ref, dtype, "attention lse")
+
+
 def test_attention_rows_sum_to_one(A):
     """V = 1 gives O = 1 exactly up to rounding: attention rows sum to one."""
     torch = _torch()
