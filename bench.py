@@ -68,7 +68,8 @@ def parse():
 def flops_model(w, K):
     """Algorithmic FLOPs of one step, by kernel (see the design notes):
     linear 2 * params / layer / row, attention 4 * S * H * d_h / row / layer,
-    probe scoring 2 passes * 2 * G * L * H * d_h / request / layer."""
+    probe scoring 2 sweeps * 2 * G * L * H * d_h / request / layer (timed as
+    score_colsum on the bf16 path, where both sweeps are one kernel)."""
     d = w.dims
     lay = w.layout
     B, S, L, G, N = w.batch, lay.seq_len, lay.affix_len, lay.mask_len, d.n_layers
@@ -91,8 +92,12 @@ def flops_model(w, K):
     out["probe"] = {k: v * B * P * (N - 1) for k, v in per_row.items()}
     out["probe"]["gemm_qkv"] += 2 * d.d_model * hq * B * G
     score = 2 * 2 * G * L * hq * B * N
-    out["probe"]["score_lse"] = score / 2
-    out["probe"]["score_colsum"] = score / 2
+    if d.dtype == "bf16":
+        # one kernel: the log-sum-exp sweep and the column-sum sweep
+        out["probe"]["score_colsum"] = score
+    else:
+        out["probe"]["score_lse"] = score / 2
+        out["probe"]["score_colsum"] = score / 2
     return out, rows
 
 

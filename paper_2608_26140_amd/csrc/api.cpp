@@ -115,7 +115,7 @@ acache_status check_cu(const int32_t* cu, int batch) {
 
 // Workspace plan for `rows` rows (layer_recompute / score / linear).
 struct WsPlan {
-  size_t y, q, o, h, part, qkv, gu, lse, lse_aff, colsum, total;
+  size_t y, q, o, h, part, qkv, gu, lse, lse_aff, colsum, colsum_bytes, total;
   size_t part_bytes;  // size of the part region (split-K / stream-K / attention key-split partials)
 };
 
@@ -158,7 +158,10 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
   }
   w.lse = take(M * d->n_heads * sizeof(float));
   w.lse_aff = take(M * d->n_heads * sizeof(float));
-  w.colsum = take((size_t)(batch > 0 ? batch : 1) * d->n_heads * (size_t)(L > 0 ? L : 1) * sizeof(float));
+  // column sums per head and per query split (up to 8 splits at this size;
+  // the scoring kernel takes as many as fit)
+  w.colsum_bytes = (size_t)(batch > 0 ? batch : 1) * d->n_heads * (size_t)(L > 0 ? L : 1) * sizeof(float) * 8;
+  w.colsum = take(w.colsum_bytes);
   w.total = off;
   return w;
 }
@@ -170,31 +173,34 @@ T* at(void* ws, size_t off) {
 
 // Eq. 4-5 for one layer (shared by acache_score and the probe mode of
 // acache_layer_recompute).  lse_full: [q_n_rows, H] natural log, or NULL.
+// colsum: colsum_bytes of scratch for the per-head (and per-split) column
+// sums; lse_aff: [q_n_rows, H] scratch of the fp32 path.
 acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, const void* q,
                         int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows, const void* k_pool,
                         int64_t pool_ld, int64_t n_slots, const int32_t* affix_slots, int L,
                         acache_norm norm, const float* lse_full, float* scores, float* lse_aff,
-                        float* colsum, int init, hipStream_t s) {
+                        float* colsum, size_t colsum_bytes, int init, hipStream_t s) {
   const int H = d->n_heads, Hkv = d->n_kv_heads, dh = d->head_dim;
+  if (d->dtype == ACACHE_BF16) {
+    int rows = H;
+    LAUNCH_T(ACACHE_K_SCORE_COLSUM, s,
+             launch_score_fused_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots,
+                                     affix_slots, L, norm == ACACHE_NORM_FULL ? lse_full : nullptr, colsum,
+                                     colsum_bytes, &rows, s));
+    LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, rows, L, scores, init, s));
+    return ACACHE_OK;
+  }
   const float* lse = lse_full;
   int by_qrow = 0;
   if (norm == ACACHE_NORM_AFFIX) {
-    if (d->dtype == ACACHE_BF16)
-      LAUNCH_T(ACACHE_K_SCORE_LSE, s, launch_score_lse_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
-                                   n_slots, affix_slots, L, lse_aff, s));
-    else
-      LAUNCH_T(ACACHE_K_SCORE_LSE, s, launch_score_lse_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
-                                  (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse_aff, s));
+    LAUNCH_T(ACACHE_K_SCORE_LSE, s, launch_score_lse_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+                                (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse_aff, s));
     lse = lse_aff;
     by_qrow = 1;
   }
-  if (d->dtype == ACACHE_BF16)
-    LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld,
-                                    n_slots, affix_slots, L, lse, by_qrow, colsum, s));
-  else
-    LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
-                                   (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
-                                   colsum, s));
+  LAUNCH_T(ACACHE_K_SCORE_COLSUM, s, launch_score_colsum_f32(batch, cu_q, H, Hkv, dh, (const float*)q, q_ld, q_n_rows, q_rows,
+                                 (const float*)k_pool, pool_ld, n_slots, affix_slots, L, lse, by_qrow,
+                                 colsum, s));
   LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, H, L, scores, init, s));
   return ACACHE_OK;
 }
@@ -539,8 +545,8 @@ acache_status acache_score(const acache_dims* dims, int32_t batch, const void* q
   const WsPlan w = plan_ws(dims, cu_q[batch], batch, affix_len);
   CHECK(ws && ws_bytes >= w.total, ACACHE_ERR_WORKSPACE);
   return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
-                   affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum), 0,
-                   stream);
+                   affix_len, norm, row_lse, scores, at<float>(ws, w.lse_aff), at<float>(ws, w.colsum),
+                   w.colsum_bytes, 0, stream);
 }
 
 acache_status acache_score_noalloc(const acache_dims* dims, int32_t batch, const void* q, int64_t q_ld,
@@ -562,7 +568,8 @@ acache_status acache_score_noalloc(const acache_dims* dims, int32_t batch, const
   st = scratch_address(&base);
   if (st != ACACHE_OK) return st;
   return run_score(dims, batch, cu_q, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots, affix_slots,
-                   affix_len, norm, row_lse, scores, at<float>(base, 0), at<float>(base, lse_bytes), 0, stream);
+                   affix_len, norm, row_lse, scores, at<float>(base, 0), at<float>(base, lse_bytes),
+                   kNoallocScratchBytes - lse_bytes, 0, stream);
 }
 
 size_t acache_score_noalloc_max_bytes(void) { return kNoallocScratchBytes; }
@@ -735,7 +742,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   if (probe) {
     st = run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots,
                    score->affix_slots, L, score->norm, lse, score->scores, at<float>(ws, p.lse_aff),
-                   at<float>(ws, p.colsum), score->init, stream);
+                   at<float>(ws, p.colsum), p.colsum_bytes, score->init, stream);
     if (st != ACACHE_OK) return st;
   }
   if (dims->dtype == ACACHE_BF16) {
@@ -843,8 +850,8 @@ acache_status acache_layer_score(const acache_dims* dims, const acache_layer_wei
     }
   }
   return run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots, score->affix_slots, L,
-                   score->norm, lse, score->scores, at<float>(ws, p.lse_aff), at<float>(ws, p.colsum), score->init,
-                   stream);
+                   score->norm, lse, score->scores, at<float>(ws, p.lse_aff), at<float>(ws, p.colsum),
+                   p.colsum_bytes, score->init, stream);
 }
 
 acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_weights* w, int32_t batch,

@@ -48,8 +48,8 @@ hipError_t launch_rmsnorm_rows(const void* x, int64_t n_src, const int32_t* src_
                                int rows, int d, float eps, hipStream_t s);
 hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
                                   const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s);
-// scores[b][j] += sum_h part[b][h][j]
-// scores[b, j] (+)= sum over heads of part[b][h][j]; init: write instead of add
+// scores[b, j] (+)= sum over the request's H partial rows of part[b][r][j], in
+// a fixed order; init: write instead of add
 hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores, int init,
                               hipStream_t s);
 
@@ -109,20 +109,15 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
                                         const int32_t* private_slots, int private_len, const void* k_pool,
                                         const void* v_pool, int64_t pool_ld, int64_t n_slots, void* out,
                                         uint64_t* mask, float* part, size_t part_bytes, hipStream_t s);
-int attention_tile_rows();
-// Per masked row and head, natural-log LSE over the affix keys.
-hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
-                                 int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
-                                 const void* k_pool, int64_t pool_ld, int64_t n_slots,
-                                 const int32_t* affix_slots, int L, float* lse_out,
-                                 hipStream_t s);
-// part[b][h][j] = sum over request b's masked rows of exp(logit - lse);
-// lse indexed by q_rows position (lse_by_qrow) or by row (row_lse, [rows, H]).
-hipError_t launch_score_colsum_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
-                                    int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
-                                    const void* k_pool, int64_t pool_ld, int64_t n_slots,
-                                    const int32_t* affix_slots, int L, const float* lse,
-                                    int lse_by_qrow, float* part, hipStream_t s);
+// Eq. 4-5 for one layer in one launch: part[b][r][j] for r < *rows_per_request
+// (heads x query splits) such that the layer's score of affix key j of
+// request b is the sum over r in order.  row_lse: [q_n_rows, H] natural-log
+// normaliser (full-softmax reading) or null (affix-only, computed).
+// hipErrorInvalidValue if part_bytes cannot hold batch * H * L floats.
+hipError_t launch_score_fused_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q, int64_t q_ld,
+                                   int64_t q_n_rows, const int32_t* q_rows, const void* k_pool, int64_t pool_ld,
+                                   int64_t n_slots, const int32_t* affix_slots, int L, const float* row_lse,
+                                   float* part, size_t part_bytes, int* rows_per_request, hipStream_t s);
 
 // ---- fp32 VALU path (k_f32.hip)
 hipError_t launch_gemm_f32(const float* X, const float* W, float* C, int64_t ldc, int M, int N,

@@ -1,32 +1,21 @@
 // Read-slot flash attention for gfx950 (Appendix C.1): bidirectional, no
 // mask, grouped KV heads, keys and values gathered through a slot map.
 //
-// Each wavefront owns 32 queries of one head.  A workgroup holds 64 queries
-// and KS key groups of 2 wavefronts: group g streams its own contiguous
-// range of the key tiles (64 keys each) through its own LDS tiles, double
-// buffered, with the loads of tile t+1 in flight while tile t computes.  At
-// the end the groups merge their (max, sum, O) through LDS.  Splitting the
-// keys inside the workgroup fills the SIMDs when there are few queries per
-// head (the recompute has a few hundred rows) at no extra HBM traffic.
-// Per tile:
-//
-//   S^T = K Q^T       MFMA 32x32x16, K tile as the A operand, the wave's Q
-//                     fragments (registers) as B.  Lane l then holds query
-//                     l%32 and 16 keys per 32-key block, so the softmax row
-//                     statistics are an in-register reduction plus one
-//                     exchange with lane l^32.
-//   O^T += V^T P^T    the lane's own exp'd logits, packed to bf16, are the B
-//                     operand directly.  For that the rows of S^T are a fixed
-//                     permutation of the keys inside each 16-key group,
-//                     chosen so that B element j of lane half h is key 8h+j;
-//                     the A operand then reads 8 consecutive keys of the
-//                     transposed V tile (one ds_read_b128).
-//
-// The V tile is transposed on its way into LDS: each thread loads 4 keys x 8
-// dims (four 16-byte loads) and writes 8 packed 4-key runs.  Softmax runs in
-// base 2 on log2(e)/sqrt(d_h)-prescaled logits (hardware exp2).  The same
-// kernel without the V half computes only the row log-sum-exp; it serves the
-// affix-only normalisation of the probe scores (Eq. 4).
+// attention_pv_kernel   128 queries per workgroup (4 wavefronts x 32), a
+//                       two-stage LDS ring of 64-key K and V tiles; two
+//                       workgroups per CU.  Optional per-query key masks
+//                       (the decode step's shared pass) and key splits
+//                       merged by attention_merge_kernel.
+// attention_wide_kernel 256 queries per workgroup (8 wavefronts x 32), a
+//                       four-stage ring filled three tiles ahead, one
+//                       workgroup per CU; for grids that fill whole rounds.
+// Both form S^T = K Q^T with the K tile as the MFMA A operand, so each lane
+// owns one query (in-lane softmax statistics plus one exchange between the
+// lane halves), and O^T += V^T P^T with the lane's own exp'd logits as the
+// B operand (a fixed key permutation inside each 16-key group makes that
+// layout line up); V is stored untransposed and read as V^T through
+// transposing LDS reads.  Softmax runs in base 2 on log2(e)/sqrt(d_h)-
+// prescaled logits (hardware exp2) with a lazy rescale of the running max.
 #include <algorithm>
 
 #include "device.h"
@@ -37,11 +26,7 @@ namespace acache {
 namespace {
 
 constexpr int kDh = 128;
-constexpr int kTileQ = 64;           // queries per workgroup (2 waves per key group)
 constexpr int kTileK = 64;           // keys per LDS stage
-constexpr int kLdK = kDh + 8;        // K tile row (elements)
-constexpr int kLdV = kTileK + 8;     // transposed V tile row (elements)
-constexpr int kGroupThreads = 128;   // threads of one key group
 
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
@@ -70,341 +55,6 @@ __device__ __forceinline__ int key_perm(int i) {
   const int r = i & 15;
   return (i & 16) | (8 * ((r >> 2) & 1) + (r & 3) + 4 * (r >> 3));
 }
-
-template <bool PV, int KS>
-__global__ __launch_bounds__(kGroupThreads * KS) void attention_kernel(AttnArgs a) {
-  constexpr int kKBytes = 2 * kTileK * kLdK * 2;      // one group's double-buffered K tiles
-  constexpr int kVBytes = PV ? 2 * kDh * kLdV * 2 : 0;
-  constexpr int kMergeBytes = (KS - 1) * 2 * 64 * (2 + (PV ? 64 : 0)) * 4;
-  constexpr int kTileBytes = KS * (kKBytes + kVBytes);
-  __shared__ __attribute__((aligned(16))) char smem[kTileBytes > kMergeBytes ? kTileBytes : kMergeBytes];
-
-  // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
-  // renumber them so each XCD gets a contiguous run of the head-major
-  // logical order: all query tiles of a head (and the heads sharing a KV
-  // head) run on one XCD and fetch that head's K/V into one L2.
-  const int n_tiles_q = a.tile_start[a.batch];
-  int h, tile;
-  {
-    const int nb = gridDim.x, i = blockIdx.x;
-    const int q8 = nb >> 3, r8 = nb & 7, x = i & 7;
-    const int t = x * q8 + min(x, r8) + (i >> 3);
-    h = t / n_tiles_q;
-    tile = t - h * n_tiles_q;
-  }
-  int b = 0;
-  {
-    int lo = 0, hi = a.batch - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (a.tile_start[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    b = lo;
-  }
-  const int g = h / (a.H / a.Hkv);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, hl = lane >> 5;
-  const int gk = wave >> 1, wq = wave & 1;    // key group, query half
-  const int tid = threadIdx.x & (kGroupThreads - 1);  // thread within the key group
-  bf16* const sK0 = reinterpret_cast<bf16*>(smem + gk * (kKBytes + kVBytes));
-  bf16* const sV0 = reinterpret_cast<bf16*>(smem + gk * (kKBytes + kVBytes) + kKBytes);
-  auto sK = [&](int buf) { return sK0 + buf * (kTileK * kLdK); };
-  auto sV = [&](int buf) { return sV0 + buf * (kDh * kLdV); };
-  const int n_rows = a.row_start[b + 1] - a.row_start[b];
-  const int qi = (tile - a.tile_start[b]) * kTileQ + wq * 32 + (lane & 31);
-  const bool q_ok = qi < n_rows;
-  const int S = a.key_len[b];
-  const int32_t* slots = a.slots + a.key_start[b];
-
-  // query fragments: Q[q][16 s + 8 hl .. +7], s = 0..7
-  int64_t qrow = -1;
-  if (q_ok) {
-    qrow = a.row_start[b] + qi;
-    if (a.q_idx) qrow = a.q_idx[qrow];
-    if (qrow < 0 || qrow >= a.q_n_rows) qrow = -1;
-  }
-  bf16x8 qf[8];
-  {
-    const bf16* qp = a.q + (qrow < 0 ? 0 : qrow) * a.q_ld + h * kDh + hl * 8;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (qrow >= 0) v = *reinterpret_cast<const u32x4*>(qp + s * 16);
-      qf[s] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
-
-  // staging: K 8 chunks, V 2 items of 4 keys x 8 dims per thread.  The
-  // slot indices of a tile are loaded one tile ahead of its K/V rows, so
-  // issuing the row loads never waits on a dependent index load.  Offsets
-  // are 32-bit element offsets (the host checks n_slots * pool_ld < 2^31);
-  // an absent key (past the end, or an out-of-range slot) reads slot 0 and
-  // its data is zeroed, so the loads need no branches.
-  u32x4 kreg[8];
-  u32x4 vreg[PV ? 8 : 1];
-  int kslot[8];
-  int vslot[PV ? 4 : 1];
-  const int head_off = g * kDh;
-  const int pool_ld = (int)a.pool_ld;
-  // Raw slot loads only (clamped index, unconditional): nothing consumes
-  // them until the next tile, so no wait is placed behind the K/V loads.
-  auto raw_slot = [&](int key) -> int { return slots[min(key, S - 1)]; };
-  // element offset of a key's row, or -1 when the key is absent
-  auto off_of = [&](int key, int slot) -> int {
-    return (key < S && slot >= 0 && slot < a.n_slots) ? slot * pool_ld + head_off : -1;
-  };
-  int tile_loaded = 0;  // tile whose slots sit in kslot / vslot
-  // thread's keys in a tile: K chunk i -> key (tid >> 4) + 8 i;
-  // V items -> keys 4 (tid & 15) + r (the same for both items)
-  auto load_slots = [&](int t) {
-    const int k0 = t * kTileK;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) kslot[i] = raw_slot(k0 + (tid >> 4) + 8 * i);
-    if constexpr (PV) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vslot[r] = raw_slot(k0 + 4 * (tid & 15) + r);
-    }
-    tile_loaded = t;
-  };
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  // absent keys of the staged tile, applied (zeroed) when the stage is
-  // written to LDS, so the loaded registers are not consumed early
-  unsigned absent = 0;
-  auto load_tile = [&]() {
-    const int k0 = tile_loaded * kTileK;
-    absent = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int ch = (tid + i * kGroupThreads) & 15;
-      const int off = off_of(k0 + (tid >> 4) + 8 * i, kslot[i]);
-      absent |= (off < 0 ? 1u : 0u) << i;
-      kreg[i] = *reinterpret_cast<const u32x4*>(a.k_pool + (off < 0 ? 0 : off) + ch * 8);
-    }
-    if constexpr (PV) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int off = off_of(k0 + 4 * (tid & 15) + r, vslot[r]);
-        absent |= (off < 0 ? 1u : 0u) << (8 + r);
-#pragma unroll
-        for (int it = 0; it < 2; ++it) {
-          const int dc = (tid + it * kGroupThreads) >> 4;
-          vreg[it * 4 + r] = *reinterpret_cast<const u32x4*>(a.v_pool + (off < 0 ? 0 : off) + dc * 8);
-        }
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = tid + i * kGroupThreads;
-      const int key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(sK(buf) + key * kLdK + ch * 8) = (absent >> i) & 1u ? zero4 : kreg[i];
-    }
-    if constexpr (PV) {
-#pragma unroll
-      for (int it = 0; it < 2; ++it) {
-        const int item = tid + it * kGroupThreads;
-        const int kg = item & 15, dc = item >> 4;
-        const bf16x8 v0 = __builtin_bit_cast(bf16x8, (absent >> 8) & 1u ? zero4 : vreg[it * 4 + 0]);
-        const bf16x8 v1 = __builtin_bit_cast(bf16x8, (absent >> 9) & 1u ? zero4 : vreg[it * 4 + 1]);
-        const bf16x8 v2 = __builtin_bit_cast(bf16x8, (absent >> 10) & 1u ? zero4 : vreg[it * 4 + 2]);
-        const bf16x8 v3 = __builtin_bit_cast(bf16x8, (absent >> 11) & 1u ? zero4 : vreg[it * 4 + 3]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          bf16x4 w;
-          w[0] = v0[e]; w[1] = v1[e]; w[2] = v2[e]; w[3] = v3[e];
-          *reinterpret_cast<bf16x4*>(sV(buf) + (dc * 8 + e) * kLdV + kg * 4) = w;
-        }
-      }
-    }
-  };
-
-  f32x16 o_acc[PV ? 4 : 1];
-  if constexpr (PV) {
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o_acc[d][r] = 0.f;
-  }
-  float m_run = -INFINITY, l_part = 0.f;
-  const float scale = kLog2e * rsqrtf((float)kDh);
-  const int n_tiles = (S + kTileK - 1) / kTileK;
-  const int krow = key_perm(lane & 31);
-
-  // key group gk owns tiles [t_lo, t_hi); every group runs n_it iterations
-  // so the barriers line up, idle in the ones past its range
-  const int t_lo = gk * n_tiles / KS, t_hi = (gk + 1) * n_tiles / KS;
-  const int n_it = (n_tiles + KS - 1) / KS;
-  if (t_lo < t_hi) {
-    load_slots(t_lo);
-    load_tile();
-    if (t_lo + 1 < t_hi) load_slots(t_lo + 1);
-    store_tile(0);
-  }
-  __syncthreads();
-  for (int it = 0; it < n_it; ++it) {
-    const int t = t_lo + it;
-    const int buf = it & 1;
-    if (t < t_hi) {
-    if (t + 1 < t_hi) load_tile();
-    if (t + 2 < t_hi) load_slots(t + 2);
-    const bf16* ks = sK(buf);
-    f32x16 st[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      // all 8 K fragments of this 32-key block are read before its MFMAs
-      bf16x8 kf[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-        kf[s] = *reinterpret_cast<const bf16x8*>(ks + (kb * 32 + krow) * kLdK + s * 16 + hl * 8);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) st[kb][r] = 0.f;
-#pragma unroll
-      for (int s = 0; s < 8; ++s) st[kb] = mfma32x32x16(kf[s], qf[s], st[kb]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // register r of block kb holds key kb*32 + 16(r/8) + 8 hl + r%8
-    const int kt0 = t * kTileK;
-    float mx = -INFINITY;
-    if (kt0 + kTileK <= S) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kb][r]);
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt0 + kb * 32 + 16 * (r >> 3) + 8 * hl + (r & 7);
-          st[kb][r] = key < S ? st[kb][r] : -INFINITY;
-          mx = fmaxf(mx, st[kb][r]);
-        }
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale;
-    // The running max moves only when a tile's max exceeds it by more than
-    // 2^8; exp2(u - m) then stays <= 256 (exact in fp32 and bf16), and the
-    // final normalisation uses the same m, so the result is unchanged.
-    const bool bump = mx > m_run + 8.f;
-    float alpha = 1.f;
-    if (__builtin_amdgcn_ballot_w64(bump)) {
-      const float m_new = bump ? mx : m_run;
-      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_part *= alpha;
-      if constexpr (PV) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o_acc[d][r] *= alpha;
-      }
-    }
-    float psum = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(st[kb][r], scale, -m_run));
-        st[kb][r] = e;
-        psum += e;
-      }
-    l_part += psum;
-    if constexpr (PV) {
-      const bf16* vs = sV(buf);
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int g2 = 0; g2 < 2; ++g2) {
-          bf16x8 pb;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) pb[j] = (bf16)st[kb][8 * g2 + j];
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-                vs + (d * 32 + (lane & 31)) * kLdV + kb * 32 + 16 * g2 + 8 * hl);
-            o_acc[d] = mfma32x32x16(vf, pb, o_acc[d]);
-          }
-        }
-    }
-    if (t + 1 < t_hi) store_tile(buf ^ 1);
-    }
-    __syncthreads();
-  }
-
-  if constexpr (KS > 1) {
-    // groups 1.. hand (max, partial sum, O) to group 0 through LDS, per lane
-    float* xch = reinterpret_cast<float*>(smem);
-    constexpr int kVals = 2 + (PV ? 64 : 0);
-    if (gk > 0) {
-      float* dst = xch + ((gk - 1) * 2 + wq) * kVals * 64 + lane;
-      dst[0] = m_run;
-      dst[64] = l_part;
-      if constexpr (PV) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) dst[(2 + d * 16 + r) * 64] = o_acc[d][r];
-      }
-    }
-    __syncthreads();
-    if (gk > 0) return;
-#pragma unroll
-    for (int o = 1; o < KS; ++o) {
-      const float* src = xch + ((o - 1) * 2 + wq) * kVals * 64 + lane;
-      const float m_o = src[0];
-      const float m_new = fmaxf(m_run, m_o);
-      // a group that saw no key has m = -inf and contributes nothing
-      const float a_self = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-      const float a_o = m_o == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_o - m_new);
-      l_part = l_part * a_self + src[64] * a_o;
-      if constexpr (PV) {
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o_acc[d][r] = o_acc[d][r] * a_self + src[(2 + d * 16 + r) * 64] * a_o;
-      }
-      m_run = m_new;
-    }
-  }
-
-  const float l_tot = l_part + __shfl_xor(l_part, 32);
-  if (!q_ok) return;
-  const int64_t row = a.row_start[b] + qi;
-  if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run + __log2f(l_tot)) * kLn2;
-  if constexpr (PV) {
-    const float inv = 1.f / l_tot;
-    bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        bf16x4 w;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) w[j] = (bf16)(o_acc[d][4 * gq + j] * inv);
-        *reinterpret_cast<bf16x4*>(op + d * 32 + 8 * gq + 4 * hl) = w;
-      }
-  }
-}
-
-// Key groups per workgroup: with V, two groups (2 x 70 KB of LDS, one
-// 4-wave workgroup per CU, one wave per SIMD at this register count); the
-// log-sum-exp-only variant has no V tiles and takes four.  Requests with
-// fewer key tiles than groups leave the extra groups idle, which is
-// harmless.
-template <bool PV>
-hipError_t launch(AttnArgs& a, hipStream_t s) {
-  int tiles = 0;
-  for (int b = 0; b < a.batch; ++b) {
-    a.tile_start[b] = tiles;
-    tiles += (a.row_start[b + 1] - a.row_start[b] + kTileQ - 1) / kTileQ;
-  }
-  a.tile_start[a.batch] = tiles;
-  if (tiles == 0) return hipSuccess;
-  constexpr int KS = PV ? 2 : 4;
-  hipLaunchKernelGGL((attention_kernel<PV, KS>), dim3(tiles * a.H), dim3(kGroupThreads * KS), 0, s, a);
-  return hipGetLastError();
-}
-
 
 // ============================================================================
 // Read-slot attention with the K/V tiles loaded straight into LDS.
@@ -1131,8 +781,6 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 
 }  // namespace
 
-int attention_tile_rows() { return kTileQ; }
-
 
 // Key splits for the read-slot attention.  Cost in 64-key tiles of one
 // 128-query workgroup (about 1 us each): rounds of `slots` resident
@@ -1340,32 +988,5 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
   return hipGetLastError();
 }
 
-hipError_t launch_score_lse_bf16(int batch, const int* cu_q, int H, int Hkv, const void* q,
-                                 int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows,
-                                 const void* k_pool, int64_t pool_ld, int64_t n_slots,
-                                 const int32_t* affix_slots, int L, float* lse_out,
-                                 hipStream_t s) {
-  AttnArgs a = {};
-  a.q = (const bf16*)q;
-  a.q_ld = q_ld;
-  a.q_n_rows = q_n_rows;
-  a.q_idx = q_rows;
-  a.slots = affix_slots;
-  a.k_pool = (const bf16*)k_pool;
-  a.v_pool = nullptr;
-  a.pool_ld = pool_ld;
-  a.n_slots = n_slots;
-  a.out = nullptr;
-  a.lse = lse_out;
-  a.H = H;
-  a.Hkv = Hkv;
-  a.batch = batch;
-  for (int b = 0; b <= batch; ++b) a.row_start[b] = cu_q[b];
-  for (int b = 0; b < batch; ++b) {
-    a.key_start[b] = 0;
-    a.key_len[b] = L;
-  }
-  return launch<false>(a, s);
-}
 
 }  // namespace acache

@@ -316,18 +316,33 @@ __global__ __launch_bounds__(256) void reduce_residual_kernel(bf16* __restrict__
 }
 
 // ---------------------------------------------------------------- probe-score head reduction (Eq. 5)
-__global__ __launch_bounds__(64) void head_reduce_kernel(const float* __restrict__ part, int batch, int H,
+// scores[b][j] (+)= sum over the request's R partial rows part[b][r][j], in
+// a fixed order: 8 chunks of consecutive rows summed by 8 threads (rows in
+// ascending order), then the 8 chunk sums in chunk order.  Workgroup: 32
+// keys x 8 chunks.
+__global__ __launch_bounds__(256) void head_reduce_kernel(const float* __restrict__ part, int batch, int R,
                                                           int L, float* __restrict__ scores, int init) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)batch * L) return;
-  const int b = (int)(t / L);
-  const int j = (int)(t - (int64_t)b * L);
-  const float* p = part + (int64_t)b * H * L + j;
+  __shared__ float cs[8][33];
+  const int kx = threadIdx.x & 31, c = threadIdx.x >> 5;
+  const int64_t t = (int64_t)blockIdx.x * 32 + kx;
+  const bool ok = t < (int64_t)batch * L;
+  const int b = ok ? (int)(t / L) : 0;
+  const int j = ok ? (int)(t - (int64_t)b * L) : 0;
+  const int r0 = c * R / 8, r1 = (c + 1) * R / 8;
+  const float* p = part + (int64_t)b * R * L + j;
   float s = 0.f;
-  // fixed order over heads; unrolled so that the loads are in flight together
-#pragma unroll 8
-  for (int h = 0; h < H; ++h) s += p[(int64_t)h * L];
-  scores[t] = init ? s : scores[t] + s;
+  if (ok) {
+#pragma unroll 4
+    for (int r = r0; r < r1; ++r) s += p[(int64_t)r * L];
+  }
+  cs[c][kx] = s;
+  __syncthreads();
+  if (c == 0 && ok) {
+    float tot = cs[0][kx];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) tot += cs[i][kx];
+    scores[t] = init ? tot : scores[t] + tot;
+  }
 }
 
 inline int grid_for(int64_t work, int per_block = 256, int cap = 65535) {
@@ -706,8 +721,7 @@ hipError_t launch_threshold_commit(int batch, int block, const int32_t* pick, co
 hipError_t launch_head_reduce(const float* part, int batch, int H, int L, float* scores, int init,
                               hipStream_t s) {
   const int64_t work = (int64_t)batch * L;
-  // 64-thread workgroups: a request's keys spread over more CUs
-  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 63) / 64)), dim3(64), 0, s, part,
+  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((work + 31) / 32)), dim3(256), 0, s, part,
                      batch, H, L, scores, init);
   return hipGetLastError();
 }
