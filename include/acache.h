@@ -470,8 +470,8 @@ typedef enum {
   ACACHE_K_GEMM_GATE_UP = 2, /* gate/up projection + SwiGLU */
   ACACHE_K_GEMM_DOWN = 3,    /* down projection (split-K partials) */
   ACACHE_K_ATTENTION = 4,    /* read-slot attention */
-  ACACHE_K_SCORE_LSE = 5,    /* probe: affix-only log-sum-exp */
-  ACACHE_K_SCORE_COLSUM = 6, /* probe: per-head column sums */
+  ACACHE_K_SCORE_LSE = 5,    /* probe: affix-only log-sum-exp (fp32 path; bf16 does it in SCORE_COLSUM) */
+  ACACHE_K_SCORE_COLSUM = 6, /* probe: per-head column sums (bf16: with the log-sum-exp sweep) */
   ACACHE_K_SCORE_REDUCE = 7, /* probe: fixed-order head reduction */
   ACACHE_K_RMSNORM = 8,      /* RMSNorm before attention */
   ACACHE_K_RESIDUAL = 9,     /* split-K reduction + residual (+ RMSNorm) */

@@ -38,9 +38,9 @@ OPERATIONS = {
     "gemm_qkv": ([r"gemm_bf16_kernel<3,", r"gemm_bf16_fixup<3,"], r"gemm_bf16_kernel<3,"),
     "gemm_accum": ([r"gemm_bf16_kernel<1,", r"gemm_bf16_fixup<1,"], r"gemm_bf16_kernel<1,"),
     "gemm_partial": ([r"gemm_bf16_kernel<2,"], r"gemm_bf16_kernel<2,"),
-    "attention": ([r"attention_pv_kernel", r"attention_merge_kernel"], r"attention_pv_kernel"),
-    "score_lse": ([r"attention_kernel<false"], r"attention_kernel<false"),
-    "score_colsum": ([r"colsum_kernel"], r"colsum_kernel"),
+    "attention": ([r"attention_(pv|wide)_kernel", r"attention_merge_kernel"], r"attention_(pv|wide)_kernel"),
+    "score": ([r"score_fused_kernel"], r"score_fused_kernel"),
+    "score_reduce": ([r"head_reduce_kernel"], r"head_reduce_kernel"),
     "rmsnorm": ([r"rmsnorm_vec_kernel", r"rmsnorm_rows_kernel"], r"rmsnorm_(vec|rows)_kernel"),
     "residual": ([r"reduce_residual_kernel", r"q_rotary_reduce_kernel"], r"(reduce_residual|q_rotary_reduce)_kernel"),
     "gather": ([r"gather_rows_kernel"], r"gather_rows_kernel"),
