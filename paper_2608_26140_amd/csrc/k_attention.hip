@@ -408,19 +408,25 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
 // The tile loop is software pipelined: iteration t computes S(t+1) = K Q^T
 // of the next tile while it exponentiates tile t's logits, then O += V P of
 // tile t while it takes the row maxima of tile t+1, so matrix and vector
-// work are independent within each half of the iteration.  The running max
-// moves only when a tile exceeds it by more than 2^8 (lazy rescale), after
-// tile t's P V has been added.  Per query the keys are visited in the same
-// order and tiles, with the same MFMA sequences, as attention_pv_kernel, so
-// the two kernels give the same bits.
+// work are independent within each half of the iteration.  The copies of
+// tile t+3 are issued between the first MFMAs of the iteration rather than
+// ahead of them (measured: 9-10% faster; a wave that issues its copies and
+// their address work first leaves its SIMD's matrix unit idle meanwhile).
+// The running max moves only when a tile exceeds it by more than 2^8 (lazy
+// rescale), after tile t's P V has been added.  Per query the keys are
+// visited in the same order and tiles, with the same MFMA sequences, as
+// attention_pv_kernel, so the two kernels give the same bits.
 //
-// Measured (8 wavefronts of 32 queries, two per SIMD, against
-// attention_pv_kernel's two 128-query workgroups per CU): 9-15% faster for
-// the probe's 512 rows and the Dream-shaped refresh, equal for the serving
-// refresh, slower for grids that fill less than one round (fewer,
+// Measured (8 wavefronts of 32 queries, two per SIMD): 39-41% of the bf16
+// peak on the serving shapes (512 and 2150 rows per request over 8704
+// keys), against 36-37% for attention_pv_kernel's two 128-query workgroups
+// per CU; slower than it for grids that fill less than one round (fewer,
 // longer-lived workgroups).  Four wavefronts of 64 queries halve the LDS
-// reads per MFMA but run one wavefront per SIMD, and lose: LDS throughput
-// and the overlap of matrix and vector work need two wavefronts per SIMD.
+// reads per MFMA but run one wavefront per SIMD, and lose: the overlap of
+// matrix and vector work needs two wavefronts per SIMD.  Variants measured
+// and not kept: K/V staged through registers instead of buffer -> LDS
+// copies (equal); no LDS fragment reads at all, or no exponentials (each
+// under 10% faster, so neither is what bounds the loop).
 // ============================================================================
 
 typedef uint32_t rsrc_words __attribute__((ext_vector_type(4)));
@@ -454,6 +460,8 @@ __device__ __forceinline__ void wait_vm_asm() {
 }
 
 constexpr int kWdStages = 4;                     // K + V stages in the ring
+constexpr int kWdKAhead = 3;                     // K fragments read ahead, in MFMA chunks
+constexpr int kWdVAhead = 2;                     // V fragments read ahead
 constexpr int kWdSlotB = kTileK * 4;             // one tile's slot indices
 // buffer offset of an absent key: past every pool the launcher admits
 // (n_slots * pool_ld * 2 <= kWdAbsent), so its loads return zeros
@@ -545,10 +553,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
   // K and V rows of tile t into stage t % 4: this lane's keys (64 / WAVES)
   // wave + 4 i + lane / 16, chunk lane % 16 (K chunks XOR-swizzled by row & 15, V by
   // 2 (row & 3)); reads the tile's slot indices from LDS
-  auto issue_kv = [&](int t) {
-    char* st = ring + (t & 3) * kStageB;
+  auto kv_offsets = [&](int t, uint32_t (&off)[C::kDma]) {
     const char* sl = my_slots + (t & 3) * kWdSlotB;
-    uint32_t off[C::kDma];
 #pragma unroll
     for (int i = 0; i < C::kDma; ++i) {
       const int kk = wave * C::kKeysPerWave + 4 * i + (lane >> 4);
@@ -557,14 +563,20 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
       const bool ok = key < S && slot >= 0 && slot < a.n_slots;
       off[i] = ok ? (uint32_t)slot * ld_b + head_b : kWdAbsent;
     }
+  };
+  auto kv_issue = [&](int t, const uint32_t (&off)[C::kDma], int i) {
+    char* st = ring + (t & 3) * kStageB;
+    const int r = (wave * C::kKeysPerWave + 4 * i + (lane >> 4)) & (kTileK - 1);
+    const int ck = pch ^ (r & 15), cv = pch ^ ((r & 3) << 1);
+    const int dst = (wave * C::kDma + i) * 1024;
+    dma16_asm(kres, off[i] + ck * 16, st + dst);
+    dma16_asm(vres, off[i] + cv * 16, st + kTileB + dst);
+  };
+  auto issue_kv = [&](int t) {
+    uint32_t off[C::kDma];
+    kv_offsets(t, off);
 #pragma unroll
-    for (int i = 0; i < C::kDma; ++i) {
-      const int r = (wave * C::kKeysPerWave + 4 * i + (lane >> 4)) & (kTileK - 1);
-      const int ck = pch ^ (r & 15), cv = pch ^ ((r & 3) << 1);
-      const int dst = (wave * C::kDma + i) * 1024;
-      dma16_asm(kres, off[i] + ck * 16, st + dst);
-      dma16_asm(vres, off[i] + cv * 16, st + kTileB + dst);
-    }
+    for (int i = 0; i < C::kDma; ++i) kv_issue(t, off, i);
   };
 
   const float scale = kLog2e * rsqrtf((float)kDh);
@@ -682,52 +694,102 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
   }
   // one iteration: P(t) from cur, S(t+1) into nxt, O += V P(t), max of t+1
   auto step = [&](int t, f32x16 (&cur)[QB][2], f32x16 (&nxt)[QB][2]) {
-    wait_vm_asm<kOps + 1>();  // tile t+1 has landed in this wave
-    bare_barrier();           // ... in every wave, and every wave is done with tile t-1
-    issue_slots(t + 4);
-    wait_vm_asm<kOps + 1>();  // the slot indices of tile t+3
-    issue_kv(t + 3);   // into the stage of tile t-1
-    if (!live) return;
-    // P(t): exp2 of the scaled logits against the running max, packed to bf16
+    wait_vm_asm<kOps>();  // tile t+1 and the slot indices of tile t+3 have landed in this wave
+    bare_barrier();       // ... in every wave, and every wave is done with tile t-1
+    if (!live) {
+      issue_slots(t + 4);
+      issue_kv(t + 3);  // into the stage of tile t-1
+      return;
+    }
+    // The iteration is laid out by hand in chunks fenced against the
+    // scheduler: 16 chunks of one S(t+1) MFMA (K fragment read kWdKAhead
+    // chunks ahead) with two of tile t's exponentials, then 16 chunks of one
+    // P V MFMA (V fragment read kWdVAhead chunks ahead) with the maxima of two
+    // of tile t+1's logits.  The empty asm statements keep the running sum and
+    // maximum inside their chunk (without them the compiler sinks the adds
+    // and maxima past the MFMAs).  Every accumulator sees the same MFMA
+    // sequence as in attention_pv_kernel.
+    const char* ks = ring + ((t + 1) & 3) * kStageB;
+    const char* vs = ring + (t & 3) * kStageB + kTileB;
+    auto kfrag = [&](int i) {
+      const int kb = i >> 3, s2 = i & 7;
+      return *reinterpret_cast<const bf16x8*>(ks + kb * 32 * kRowB + k_row_off + (((2 * s2 + hl) ^ k_sw) << 4));
+    };
+    auto vfrag = [&](int i) {
+      const int kb = i >> 3, g2 = (i >> 2) & 1, d = i & 3;
+      const int row0 = kb * 32 + g2 * 16 + v_key;
+      const int off = ((4 * d + v_chunk_lo) ^ v_sw) * 16 + v_byte;
+      const v4i16 lo = ds_read_tr16(vs + row0 * kRowB + off);
+      const v4i16 hi = ds_read_tr16(vs + (row0 + 4) * kRowB + off);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
     bf16x8 pb[QB][2][2];
+    float psum[QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float psum = 0.f;
+      psum[qb] = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int g2 = 0; g2 < 2; ++g2)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float e = __builtin_amdgcn_exp2f(fmaf(cur[qb][kb][8 * g2 + j], scale, -m_run[qb]));
-            psum += e;
-            pb[qb][kb][g2][j] = (bf16)e;
-          }
-      l_part[qb] += psum;
+        for (int r = 0; r < 16; ++r) nxt[qb][kb][r] = 0.f;
     }
-    // S(t+1) unconditionally (past the range it reads a tile copied for
-    // nothing and is not used), so the block has no branch between the
-    // exponentials and these MFMAs
-    scores(t + 1, nxt);
-    // O^T += V^T P^T of tile t
-    const char* vs = ring + (t & 3) * kStageB + kTileB;
+    bf16x8 kf[kWdKAhead + 1];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int i = 0; i < kWdKAhead; ++i) kf[i] = kfrag(i);
+    bf16x8 vf[kWdVAhead + 1];
+    uint32_t koff[C::kDma];
 #pragma unroll
-      for (int g2 = 0; g2 < 2; ++g2) {
-        const int row0 = kb * 32 + g2 * 16 + v_key;
+    for (int i = 0; i < 16; ++i) {
+      // the copies of tile t+3 (into the stage of tile t-1), spread over
+      // the first chunks: slot indices of tile t+4, offsets, K/V rows
+      if (i == 0) issue_slots(t + 4);
+      if (i == 1) kv_offsets(t + 3, koff);
 #pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          const int off = ((4 * d + v_chunk_lo) ^ v_sw) * 16 + v_byte;
-          const v4i16 lo = ds_read_tr16(vs + row0 * kRowB + off);
-          const v4i16 hi = ds_read_tr16(vs + (row0 + 4) * kRowB + off);
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      for (int j = 0; j < C::kDma; ++j)
+        if (i == 3 + 2 * j) kv_issue(t + 3, koff, j);
+      if (i + kWdKAhead < 16) kf[(i + kWdKAhead) % (kWdKAhead + 1)] = kfrag(i + kWdKAhead);
+      if (i >= 16 - kWdVAhead) vf[i - (16 - kWdVAhead)] = vfrag(i - (16 - kWdVAhead));
+      const int kb = i >> 3, s2 = i & 7;
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o_acc[qb][d] = mfma32x32x16(vf, pb[qb][kb][g2], o_acc[qb][d]);
+      for (int qb = 0; qb < QB; ++qb) nxt[qb][kb] = mfma32x32x16(kf[i % (kWdKAhead + 1)], qf[qb][s2], nxt[qb][kb]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = 2 * i + u, ekb = e >> 4, r = e & 15;
+          const float x = __builtin_amdgcn_exp2f(fmaf(cur[qb][ekb][r], scale, -m_run[qb]));
+          psum[qb] += x;
+          pb[qb][ekb][r >> 3][r & 7] = (bf16)x;
         }
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) asm volatile("" ::"v"(psum[qb]));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      l_part[qb] += psum[qb];
+      mx[qb] = -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i + kWdVAhead < 16) vf[(i + kWdVAhead) % (kWdVAhead + 1)] = vfrag(i + kWdVAhead);
+      const int kb = i >> 3, g2 = (i >> 2) & 1, d = i & 3;
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) o_acc[qb][d] = mfma32x32x16(vf[i % (kWdVAhead + 1)], pb[qb][kb][g2], o_acc[qb][d]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        mx[qb] = fmaxf(mx[qb], fmaxf(nxt[qb][i >> 3][2 * (i & 7)], nxt[qb][i >> 3][2 * (i & 7) + 1]));
+        asm volatile("" ::"v"(mx[qb]));
       }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (t + 1 < t_hi) {
-      row_max(t + 1, nxt, mx);
+      if ((t + 2) * kTileK > S) {
+        row_max(t + 1, nxt, mx);
+      } else {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) mx[qb] = fmaxf(mx[qb], __shfl_xor(mx[qb], 32)) * scale;
+      }
       rescale(mx);
     }
   };
@@ -810,8 +872,9 @@ static int attention_splits(int n_wg, int slots, double tile_cost, int n_kt, int
 }
 
 // One 64-key tile of a 256-query workgroup of attention_wide_kernel (one
-// per CU), in units of a 128-query workgroup's tile (two per CU), measured.
-constexpr double kWideTileCost = 0.95;
+// per CU), in units of a 128-query workgroup's tile (two per CU), measured
+// on the serving shapes (40% against 36.5% of the bf16 peak).
+constexpr double kWideTileCost = 0.9;
 constexpr int kWideQB = 1, kWideWaves = 8;
 using WideQ = WideCfg<kWideQB, kWideWaves>;
 
