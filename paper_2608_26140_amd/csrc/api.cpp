@@ -115,7 +115,7 @@ acache_status check_cu(const int32_t* cu, int batch) {
 
 // Workspace plan for `rows` rows (layer_recompute / score / linear).
 struct WsPlan {
-  size_t y, q, o, h, part, qkv, gu, lse, lse_aff, colsum, colsum_bytes, total;
+  size_t y, q, o, h, part, qkv, gu, rope, lse, lse_aff, colsum, colsum_bytes, total;
   size_t part_bytes;  // size of the part region (split-K / stream-K / attention key-split partials)
 };
 
@@ -151,10 +151,13 @@ WsPlan plan_ws(const acache_dims* d, int rows, int batch, int L) {
     w.part_bytes = std::max(part_elems * sizeof(float), gemm_bf16_sk_ws_bytes());
     w.part = take(w.part_bytes);
     w.qkv = w.gu = 0;
+    // the rotary table of the QKV projection: (cos, sin) of 64 pairs per row
+    w.rope = take(M * 64 * 2 * sizeof(float));
   } else {
     w.qkv = take(M * (size_t)(d->n_heads + 2 * d->n_kv_heads) * d->head_dim * es);
     w.gu = take(M * 2 * (size_t)d->d_ff * es);
     w.part = 0;
+    w.rope = 0;
   }
   w.lse = take(M * d->n_heads * sizeof(float));
   w.lse_aff = take(M * d->n_heads * sizeof(float));
@@ -594,8 +597,10 @@ acache_status acache_layer_schedule(const acache_dims* dims, int32_t rows, int32
 // fresh K/V to their pool slots.
 static acache_status run_qkv_bf16(const acache_dims* dims, const acache_layer_weights* w, int M, const void* y,
                                   void* q, const int32_t* pos, const int32_t* write_slots, void* k_pool,
-                                  void* v_pool, int64_t pool_ld, int64_t n_slots, float* part, hipStream_t stream) {
+                                  void* v_pool, int64_t pool_ld, int64_t n_slots, float* part, float* rope,
+                                  hipStream_t stream) {
   const int d = dims->d_model, H = dims->n_heads, Hkv = dims->n_kv_heads, dh = dims->head_dim;
+  LAUNCH(launch_rope_table(pos, M, dims->rope_base, rope, stream));
   GemmParams g = {};
   g.X = y;
   g.W = w->w_qkv;
@@ -609,10 +614,9 @@ static acache_status run_qkv_bf16(const acache_dims* dims, const acache_layer_we
   g.pool_ld = pool_ld;
   g.n_slots = n_slots;
   g.write_slots = write_slots;
-  g.pos = pos;
+  g.rope_cs = rope;
   g.hq_cols = H * dh;
   g.hkv_cols = Hkv * dh;
-  g.rope_base = dims->rope_base;
   g.sk_ws = part;
   LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_bf16(EPI_QKV, g, stream));
   return ACACHE_OK;
@@ -726,7 +730,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
 
   LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
   if (dims->dtype == ACACHE_BF16) {
-    st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, at<float>(ws, p.part), stream);
+    st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, at<float>(ws, p.part),
+                      at<float>(ws, p.rope), stream);
     if (st != ACACHE_OK) return st;
     // the part region is idle between the QKV fixup and the O projection
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse,
@@ -830,7 +835,7 @@ acache_status acache_layer_score(const acache_dims* dims, const acache_layer_wei
     LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
     if (dims->dtype == ACACHE_BF16) {
       st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, at<float>(ws, p.part),
-                        stream);
+                        at<float>(ws, p.rope), stream);
       if (st != ACACHE_OK) return st;
       LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld,
                                                                   n_slots, at<char>(ws, p.o), lse,
@@ -897,7 +902,8 @@ acache_status acache_layer_decode(const acache_dims* dims, const acache_layer_we
   float* part = at<float>(ws, p.part);
 
   LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(ACACHE_BF16, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
-  st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, part, stream);
+  st = run_qkv_bf16(dims, w, M, y, q, pos, write_slots, k_pool, v_pool, pool_ld, n_slots, part, at<float>(ws, p.rope),
+                    stream);
   if (st != ACACHE_OK) return st;
   LAUNCH_T(ACACHE_K_ATTENTION, stream,
            launch_attention_decode_bf16(batch, rows_per_request, H, Hkv, q, affix_slots, affix_len, anchors, k,

@@ -46,6 +46,9 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
 bool rmsnorm_rows_ok(const void* x, const void* g, const void* y, int d);
 hipError_t launch_rmsnorm_rows(const void* x, int64_t n_src, const int32_t* src_rows, const void* g, void* y,
                                int rows, int d, float eps, hipStream_t s);
+// cos and sin of pos[m] * theta_d for every row m < M and rotary pair d < 64
+// (head_dim 128): table[(m * 64 + d) * 2 + {0, 1}].
+hipError_t launch_rope_table(const int32_t* pos, int M, float rope_base, float* table, hipStream_t s);
 hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
                                   const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s);
 // scores[b, j] (+)= sum over the request's H partial rows of part[b][r][j], in
@@ -71,9 +74,8 @@ struct GemmParams {
   int64_t pool_ld;
   int64_t n_slots;
   const int32_t* write_slots;
-  const int32_t* pos;
+  const float* rope_cs;  // [M][64][2]: cos, sin of row m's rotary angle for pair d (launch_rope_table)
   int hq_cols, hkv_cols;
-  float rope_base;
 };
 hipError_t launch_gemm_bf16(GemmEpi epi, const GemmParams& p, hipStream_t s);
 int gemm_bf16_splits(int M, int N, int K);  // split-K choice for EPI_PARTIAL

@@ -8,11 +8,14 @@
 // and puts both halves of every rotary pair (columns d and d + 64 of one
 // head) in the same lane.
 //
-// Workgroup tile: 256 weight rows x 256 (or 128) activation rows, 8 waves
-// (2 along N x 4 along M, two per SIMD), each wave 128 x 64 (or 128 x 32)
-// = 4 x 2 (4 x 1) MFMA 32x32x16 tiles.  The main loop is a ping-pong
-// schedule over 32-wide K units, fed by buffer -> LDS copies into a ring of
-// units (see the kernel).  Workgroups are
+// Workgroup tiles: 256 weight rows x 256 activation rows, 4 waves (one per
+// SIMD) of 128 x 128 on MFMA 16x16x32 with the accumulators in AGPRs, two
+// LDS stages of a 64-wide K step (gemm_bf16_w4_kernel); or, where it
+// leaves fewer CUs idle, 256 x 128 with 8 waves (two per SIMD) of 128 x 32
+// on MFMA 32x32x16 and a ping-pong schedule over 32-wide K units
+// (gemm_bf16_kernel).  Both are fed by buffer -> LDS copies (no staging
+// registers).  The rotary epilogue reads each row's (cos, sin) table,
+// computed once per projection by launch_rope_table.  Workgroups are
 // renumbered so that each XCD (8 per chip, own L2) receives a contiguous
 // run of tiles with the M index fastest: the tiles sharing one weight tile
 // run on the same L2.
@@ -30,6 +33,7 @@
 // rotary embedding and the K/V store to pool slots, and SwiGLU.
 #include <algorithm>
 #include <atomic>
+#include <type_traits>
 
 #include "device.h"
 #include "internal.h"
@@ -165,7 +169,7 @@ __device__ __forceinline__ void add_partial(const float* base, f32x16 (&acc)[4][
 // acc[a][b][r] = C[m = mbase + 32b + lane%32][n = nbase + 32a + 8(r/4) + 4(lane/32) + r%4]
 template <int EPI, class C>
 __device__ __forceinline__ void epilogue(const GemmParams& p, const f32x16 (&acc)[4][C::FM], int nt, int mt,
-                                         int sp, int wn, int wm, int lane, const double* inv_freq) {
+                                         int sp, int wn, int wm, int lane) {
   constexpr int BN = C::BN, BM = C::BM, FM = C::FM;
   const int hl = lane >> 5;
   const int mbase = mt * BM + wm * C::WAVE_M + (lane & 31);
@@ -224,18 +228,20 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const f32x16 (&acc
       if (!is_v) {
         // rotate the pairs (d, d + 64): both halves sit in this lane, in
         // fragments a and a + 2
-        const double ang_pos = (double)p.pos[m];
+        const float* rt = p.rope_cs + (int64_t)m * 128;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             float lo[4], hi[4];
+            const int d0 = a * 32 + 8 * g + 4 * hl;
+            const f32x4 t0 = *reinterpret_cast<const f32x4*>(rt + 2 * d0);
+            const f32x4 t1 = *reinterpret_cast<const f32x4*>(rt + 2 * d0 + 4);
+            const float cs4[4] = {t0[0], t0[2], t1[0], t1[2]}, sn4[4] = {t0[1], t0[3], t1[1], t1[3]};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
               const int r = 4 * g + j;
-              const int d = a * 32 + 8 * g + 4 * hl + j;
-              float sn, cs;
-              rotary_sincos(ang_pos * inv_freq[d], &sn, &cs);
+              const float cs = cs4[j], sn = sn4[j];
               const float x1 = acc[a][b][r], x2 = acc[a + 2][b][r];
               lo[j] = x1 * cs - x2 * sn;
               hi[j] = x2 * cs + x1 * sn;
@@ -256,9 +262,6 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, const f32x16 (&acc
   }
 }
 
-__device__ __forceinline__ void init_inv_freq(double* inv_freq, const GemmParams& p, int tid) {
-  if (tid < 64) inv_freq[tid] = exp2(-(2.0 * tid / 128.0) * log2((double)p.rope_base));
-}
 
 // Main loop: a ping-pong schedule.  The K range is cut into 32-wide units.
 // The waves form two groups, waves 0-3 and 4-7, one wave of each on every
@@ -303,9 +306,6 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
   constexpr int kStages = 4;
   constexpr int kAhead = kStages - 1;
   __shared__ __attribute__((aligned(1024))) char ring[kStages * kStageB];
-  // the rotary frequencies live in the ring, written once the main loop of
-  // an item is over
-  double* inv_freq = reinterpret_cast<double*>(ring);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: LDS addresses in SGPRs
@@ -443,11 +443,6 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
       bare_barrier();
     }
     if (grp == 0) bare_barrier();  // the phase in which group 1 computes the last unit
-    // every wave is past its last read of the ring, and every copy has landed
-    if constexpr (EPI == EPI_QKV) {
-      init_inv_freq(inv_freq, p, tid);
-      lds_barrier();
-    }
 
     if (sk && kn < nk_tile) {
       float* slot = tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * C::ACC4 * 4);
@@ -455,9 +450,377 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
       ++piece;
     } else {
       if (sk) ++piece;
-      epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane, inv_freq);
+      epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// 16x16x32 MFMA tiles (gfx950 issues them at a higher rate than 32x32x16:
+// measured 86% against 69% of the bf16 peak for back-to-back independent
+// MFMAs from one wave per SIMD).  Lane l supplies A[l % 16][8 (l / 16) + j]
+// and B[8 (l / 16) + j][l % 16], j = 0..7, and receives
+// D[4 (l / 16) + r][l % 16] in accumulator register r = 0..3.  With the
+// weights as A, lane l holds activation row l % 16 and output columns
+// 4 (l / 16) .. + 3 of each 16 x 16 tile.
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// The same MFMA with the accumulator held in AGPRs by the asm constraint
+// (the compiler otherwise moves a 256-register accumulator set between
+// AGPRs and VGPRs on every loop iteration).  The hazard recognizer does not
+// look into inline asm: callers pad with s_nop where the accumulators pass
+// between VALU and MFMA (mfma_agpr_fence).
+__device__ __forceinline__ void mfma16x16x32_agpr(f32x4& c, bf16x8 a, bf16x8 b) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+// Wait states between MFMA results in AGPRs and their VALU readers (or
+// VALU-written AGPRs and a following MFMA), more than any gfx950 MFMA needs.
+__device__ __forceinline__ void mfma_agpr_fence() { asm volatile("s_nop 7\n s_nop 7\n s_nop 7" ::: "memory"); }
+
+// One wave's 128 x 128 accumulators: acc[a][b][r] = C[m = mbase + 16 b + lane % 16]
+// [n = nbase + 16 a + 4 (lane / 16) + r].
+typedef f32x4 Acc16[8][8];
+
+// Partial accumulators: float4 chunk i = a * 8 + b of lane l at (i * 64 + l) * 4.
+__device__ __forceinline__ void store_partial16(float* base, const Acc16& acc, int lane) {
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 8; ++b) *reinterpret_cast<f32x4*>(base + ((a * 8 + b) * 64 + lane) * 4) = acc[a][b];
+}
+__device__ __forceinline__ void add_partial16(const float* base, Acc16& acc, int lane) {
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(base + ((a * 8 + b) * 64 + lane) * 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[a][b][j] += v[j];
+    }
+}
+
+// Writes one wave's accumulators (wave (wn, wm) of 256 x 256 tile (nt, mt),
+// split sp): the same epilogues as the 32x32 layout.
+template <int EPI>
+__device__ __forceinline__ void epilogue16(const GemmParams& p, const Acc16& acc, int nt, int mt, int sp, int wn,
+                                           int wm, int lane) {
+  const int q4 = 4 * (lane >> 4);
+  const int mbase = mt * 256 + wm * 128 + (lane & 15);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const int m = mbase + b * 16;
+    if (m >= p.M) continue;
+    if constexpr (EPI == EPI_STORE || EPI == EPI_ACCUM || EPI == EPI_PARTIAL) {
+      const int nbase = nt * 256 + wn * 128 + q4;
+#pragma unroll
+      for (int a = 0; a < 8; ++a) {
+        const int n = nbase + a * 16;
+        float v[4] = {acc[a][b][0], acc[a][b][1], acc[a][b][2], acc[a][b][3]};
+        if constexpr (EPI == EPI_PARTIAL) {
+          *reinterpret_cast<f32x4*>(p.P + ((int64_t)sp * p.M + m) * p.N + n) = acc[a][b];
+        } else {
+          bf16* dst = (bf16*)p.C + (int64_t)m * p.ldc + n;
+          if constexpr (EPI == EPI_ACCUM) {
+            const bf16x4 old = *reinterpret_cast<const bf16x4*>(dst);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] += (float)old[j];
+          }
+          store4(dst, v);
+        }
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      // tiles 0..3 of the wave are gate rows, 4..7 the matching up rows
+      const int cbase = nt * 128 + wn * 64 + q4;
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float gt = acc[a][b][j], up = acc[a + 4][b][j];
+          v[j] = gt / (1.f + __expf(-gt)) * up;
+        }
+        store4((bf16*)p.C + (int64_t)m * p.ldc + cbase + a * 16, v);
+      }
+    } else if constexpr (EPI == EPI_QKV) {
+      const int col0 = nt * 256 + wn * 128;  // first weight row of this wave = one head
+      const bool is_v = col0 >= p.hq_cols + p.hkv_cols;
+      bf16* dst;
+      if (col0 < p.hq_cols) {
+        dst = (bf16*)p.q_out + (int64_t)m * p.hq_cols + col0;
+      } else {
+        const int64_t slot = p.write_slots[m];
+        if (slot < 0 || slot >= p.n_slots) continue;
+        const int c = is_v ? col0 - p.hq_cols - p.hkv_cols : col0 - p.hq_cols;
+        dst = (bf16*)(is_v ? p.v_pool : p.k_pool) + slot * p.pool_ld + c;
+      }
+      if (!is_v) {
+        // rotate the pairs (d, d + 64): both halves sit in this lane, in
+        // tiles a and a + 4
+        const float* rt = p.rope_cs + (int64_t)m * 128;
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          float lo[4], hi[4];
+          const int d0 = a * 16 + q4;
+          const f32x4 t0 = *reinterpret_cast<const f32x4*>(rt + 2 * d0);
+          const f32x4 t1 = *reinterpret_cast<const f32x4*>(rt + 2 * d0 + 4);
+          const float cs4[4] = {t0[0], t0[2], t1[0], t1[2]}, sn4[4] = {t0[1], t0[3], t1[1], t1[3]};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const float cs = cs4[j], sn = sn4[j];
+            const float x1 = acc[a][b][j], x2 = acc[a + 4][b][j];
+            lo[j] = x1 * cs - x2 * sn;
+            hi[j] = x2 * cs + x1 * sn;
+          }
+          store4(dst + a * 16 + q4, lo);
+          store4(dst + (a + 4) * 16 + q4, hi);
+        }
+      } else {
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+          const float v[4] = {acc[a][b][0], acc[a][b][1], acc[a][b][2], acc[a][b][3]};
+          store4(dst + a * 16 + q4, v);
+        }
+      }
+    }
+  }
+}
+
+// Main loop with one wave per SIMD: 4 waves (2 along N x 2 along M), each a
+// 128 x 128 wave tile = 8 x 8 MFMA 16x16x32 tiles, 256 fp32 accumulators
+// per lane (0.5 KB of LDS fragment reads per 32 x 32 x 16 of work).
+//
+// LDS holds two stages of one 64-wide K step: 256 weight rows and 256
+// activation rows of 128 bytes.  Each copy instruction moves 8 whole rows
+// (a 128-byte line per row, so every L2 request is a full line), buffer ->
+// LDS with no staging registers.  16-byte chunk c of row r sits at
+// c ^ ((r >> 1) & 7): the 16 rows read by one 16-lane pass of a fragment
+// read hit 16 distinct bank groups.  The MFMAs run in 32-wide units, two per
+// stage.  Before unit u each wave waits for its fragment reads of unit u and
+// meets the others at a barrier; it then reads unit u + 1's 16 fragments
+// into the other register set, one read after every fourth of unit u's 64
+// MFMAs.  At the second unit of step j (after its barrier every wave holds
+// step j in registers or is done with it) the copies of step j + 2 go into
+// step j's stage, and the wait before that barrier makes step j + 1
+// complete: copies have two units (2048 MFMA cycles) to land.
+constexpr int kW4RowB = 128;
+
+template <int EPI, class C>
+__global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams p, TileMap tm) {
+  static_assert(C::BN == 256 && C::BM == 256 && C::WN == 2 && C::WM == 2 && C::BK == 64, "4-wave tile");
+  constexpr int kStageB = 512 * kW4RowB;
+  __shared__ __attribute__((aligned(1024))) char ring[2 * kStageB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave & 1, wm = wave >> 1;
+  const int F = p.N >> 1;
+  const int K = p.K;
+  const int nk_tile = tm.nk;
+  const int w = logical_block();
+
+  // copies: instruction i of a wave covers rows 64 wave + 8 i + lane / 8;
+  // the lane fills physical chunk lane % 8 with logical chunk
+  // (lane % 8) ^ ((row >> 1) & 7)
+  const int crow = lane >> 3;
+  // fragment reads: row lane % 16 of each 16-row fragment, chunk 4 h + lane / 16
+  const int fsw = ((lane & 15) >> 1) & 7;
+  const int arow = wn * 128 + (lane & 15);
+  const int brow = 256 + wm * 128 + (lane & 15);
+  const int cofs0 = ((0 + (lane >> 4)) ^ fsw) * 16;
+  const int cofs1 = ((4 + (lane >> 4)) ^ fsw) * 16;
+  const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(p.W, (uint32_t)p.N * (uint32_t)K * 2u);
+  const __amdgpu_buffer_rsrc_t xres = buffer_rsrc(p.X, (uint32_t)p.M * (uint32_t)K * 2u);
+
+  Acc16 acc;
+  int item = 0;
+  int u = 0, u_end = 0;
+  if (tm.sk_groups > 0 && w < tm.sk_groups) {
+    u = sk_start(tm, w);
+    u_end = sk_start(tm, w + 1);
+  }
+  int piece = 0;
+  while (true) {
+    int t, kb, kn;
+    bool sk = false;
+    if (item < tm.dp_rounds) {
+      t = item * tm.dp_stride + w;
+      kb = -1;
+      kn = 0;
+      ++item;
+    } else if (u < u_end) {
+      const int tl = u / nk_tile;
+      kb = u - tl * nk_tile;
+      kn = min(nk_tile - kb, u_end - u);
+      t = tm.sk_first + tl;
+      u += kn;
+      sk = true;
+    } else {
+      break;
+    }
+    int nt, mt, sp;
+    tile_coords(tm, t, nt, mt, sp);
+    if (kb < 0) {
+      kb = sp * nk_tile / tm.splits;
+      kn = (sp + 1) * nk_tile / tm.splits - kb;
+    }
+    const int k0 = kb * C::BK;
+
+    uint32_t wsrc[8], xsrc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = wave * 64 + i * 8 + crow;
+      const int c = (lane & 7) ^ ((4 * i + (lane >> 4)) & 7);
+      wsrc[i] = (uint32_t)(weight_row<EPI, 256>(nt, r, F) * K + k0 + c * 8) * 2u;
+      xsrc[i] = (uint32_t)(min(mt * C::BM + r, p.M - 1) * K + k0 + c * 8) * 2u;
+    }
+    // copies of K step j of the item into stage j % 2
+    auto issue = [&](int j) {
+      char* st = ring + (j & 1) * kStageB;
+      const uint32_t ko = (uint32_t)j * 128u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dma16_buf(wres, wsrc[i], ko, st + (wave * 64 + i * 8) * kW4RowB);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) dma16_buf(xres, xsrc[i], ko, st + (256 + wave * 64 + i * 8) * kW4RowB);
+    };
+    // fragment f of unit h (0 / 1) of step j: f < 8 weight tile f, else
+    // activation tile f - 8
+    auto frag = [&](int j, int h, int f) {
+      const char* st = ring + (j & 1) * kStageB;
+      const int row = f < 8 ? arow + f * 16 : brow + (f - 8) * 16;
+      return *reinterpret_cast<const bf16x8*>(st + row * kW4RowB + (h ? cofs1 : cofs0));
+    };
+
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int b = 0; b < 8; ++b)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[a][b][r] = 0.f;
+
+    // the previous item's stores and copies are complete, and every wave is
+    // past its last LDS read of the previous item
+    wait_vmcnt<0>();
+    lds_barrier();
+    issue(0);
+    if (kn > 1) {
+      issue(1);
+      wait_vmcnt<16>();  // step 0 (this wave's part)
+    } else {
+      wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    bare_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    bf16x8 fx[16], fy[16];
+#pragma unroll
+    for (int f = 0; f < 16; ++f) fx[f] = frag(0, 0, f);
+    mfma_agpr_fence();  // the zeroed accumulators before the first MFMA
+
+    // copy i (0..15) of K step j: 8 weight rows then 8 activation rows per wave
+    auto copy_one = [&](int j, int i) {
+      char* st = ring + (j & 1) * kStageB;
+      const uint32_t ko = (uint32_t)j * 128u;
+      if (i < 8) dma16_buf(wres, wsrc[i], ko, st + (wave * 64 + i * 8) * kW4RowB);
+      else dma16_buf(xres, xsrc[i - 8], ko, st + (256 + wave * 64 + (i - 8) * 8) * kW4RowB);
+    };
+    // 64 MFMAs from cur, the 16 reads of the next unit into nxt among them,
+    // and (cj >= 0) the 16 copies of K step cj, one after every fourth MFMA
+    // (a burst of copies stalls the wave's MFMA issue while the memory
+    // pipeline takes them)
+    auto unit = [&](bf16x8 (&cur)[16], bf16x8 (&nxt)[16], int nj, int nh, int cj, auto copies) {
+#pragma unroll
+      for (int i = 0; i < 64; ++i) {
+        const int a = i >> 3, b = i & 7;
+        if constexpr (decltype(copies)::value) {
+          if ((i & 3) == 1) copy_one(cj, i >> 2);
+        }
+        if ((i & 3) == 0) nxt[i >> 2] = frag(nj, nh, i >> 2);
+        mfma16x16x32_agpr(acc[a][b], cur[a], cur[8 + b]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    auto step = [&](int j, auto copies) {
+      // unit 0 of step j
+      wait_lgkmcnt<0>();
+      __builtin_amdgcn_sched_barrier(0);
+      bare_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      unit(fx, fy, j, 1, 0, std::false_type());
+      // unit 1 of step j: step j + 1 complete in every wave, step j's stage
+      // free for the copies of step j + 2
+      wait_vmcnt<0>();
+      wait_lgkmcnt<0>();
+      __builtin_amdgcn_sched_barrier(0);
+      bare_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      // after the last step this reads step j's own stage (complete, not
+      // written any more); the values are not used
+      unit(fy, fx, j + 1 < kn ? j + 1 : j, 0, j + 2, copies);
+    };
+    int j = 0;
+    for (; j + 2 < kn; ++j) step(j, std::true_type());
+    for (; j < kn; ++j) step(j, std::false_type());
+    mfma_agpr_fence();  // the last MFMAs' results before the epilogue reads them
+    // every wave is past its last read of the ring, and every copy has landed
+    wait_vmcnt<0>();
+    lds_barrier();
+
+    if (sk && kn < nk_tile) {
+      float* slot = tm.sk_part + ((size_t)(w * 2 + piece) * C::WAVES + wave) * (64 * 256);
+      store_partial16(slot, acc, lane);
+      ++piece;
+    } else {
+      if (sk) ++piece;
+      epilogue16<EPI>(p, acc, nt, mt, sp, wn, wm, lane);
+    }
+  }
+}
+
+// Stream-K fixup of the 16x16 tiles: as gemm_bf16_fixup, two pieces staged
+// per round.
+template <int EPI, class C>
+__global__ __launch_bounds__(256) void gemm_bf16_fixup16(GemmParams p, TileMap tm) {
+  constexpr int kPieceF = 64 * 256;  // floats per wave piece
+  constexpr int kDepth = 2;
+  __shared__ __attribute__((aligned(16))) float stage[kDepth][kPieceF];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int q = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
+  const int wn = wave & 1, wm = wave >> 1;
+  const int nk_tile = tm.nk;
+  const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
+  if (first == last) return;  // the tile was finished by one workgroup
+  auto piece = [&](int w) {
+    const int pc = sk_start(tm, w) / nk_tile == s ? 0 : 1;
+    return tm.sk_part + ((size_t)(w * 2 + pc) * C::WAVES + wave) * kPieceF;
+  };
+  Acc16 acc;
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b < 8; ++b)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[a][b][r] = 0.f;
+  for (int w0 = first; w0 <= last; w0 += kDepth + 1) {
+    if (q > 0 && q <= kDepth && w0 + q <= last) {
+      const float* src = piece(w0 + q);
+      float* dst = stage[q - 1];
+#pragma unroll 8
+      for (int i = 0; i < 64; ++i)
+        *reinterpret_cast<f32x4*>(dst + (i * 64 + lane) * 4) = *reinterpret_cast<const f32x4*>(src + (i * 64 + lane) * 4);
+    }
+    if (q == 0) add_partial16(piece(w0), acc, lane);
+    __syncthreads();
+    if (q == 0) {
+      for (int j = 1; j <= kDepth && w0 + j <= last; ++j) add_partial16(stage[j - 1], acc, lane);
+    }
+    __syncthreads();
+  }
+  if (q != 0) return;
+  int nt, mt, sp;
+  tile_coords(tm, tm.sk_first + s, nt, mt, sp);
+  epilogue16<EPI>(p, acc, nt, mt, sp, wn, wm, lane);
 }
 
 // Stream-K fixup: block = one wave-tile of one split tile of the stream-K
@@ -468,8 +831,9 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
 template <int EPI, class C>
 __global__ __launch_bounds__(256) void gemm_bf16_fixup(GemmParams p, TileMap tm) {
   constexpr int kPieceF = 64 * C::ACC4 * 4;  // floats per wave piece
-  __shared__ double inv_freq[64];
-  __shared__ __attribute__((aligned(16))) float stage[3][kPieceF];
+  // pieces staged per round: three of a 128 x 64 wave tile, two of a 128 x 128 one
+  constexpr int kDepth = 3 * kPieceF * 4 <= 128 * 1024 ? 3 : 2;
+  __shared__ __attribute__((aligned(16))) float stage[kDepth][kPieceF];
   const int tid = threadIdx.x, lane = tid & 63;
   const int q = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
@@ -477,7 +841,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_fixup(GemmParams p, TileMap tm)
   const int nk_tile = tm.nk;
   const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
   if (first == last) return;  // the tile was finished by one workgroup
-  if constexpr (EPI == EPI_QKV) init_inv_freq(inv_freq, p, tid);
   // piece 0 of w if w's range starts in this tile, else its piece 1
   auto piece = [&](int w) {
     const int pc = sk_start(tm, w) / nk_tile == s ? 0 : 1;
@@ -490,8 +853,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_fixup(GemmParams p, TileMap tm)
     for (int b = 0; b < C::FM; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-  for (int w0 = first; w0 <= last; w0 += 4) {
-    if (q > 0 && w0 + q <= last) {
+  for (int w0 = first; w0 <= last; w0 += kDepth + 1) {
+    if (q > 0 && q <= kDepth && w0 + q <= last) {
       const float* src = piece(w0 + q);
       float* dst = stage[q - 1];
 #pragma unroll 8
@@ -502,23 +865,23 @@ __global__ __launch_bounds__(256) void gemm_bf16_fixup(GemmParams p, TileMap tm)
     if (q == 0) add_partial<C>(piece(w0), acc, lane);
     __syncthreads();
     if (q == 0) {
-      for (int j = 1; j < 4 && w0 + j <= last; ++j) add_partial<C>(stage[j - 1], acc, lane);
+      for (int j = 1; j <= kDepth && w0 + j <= last; ++j) add_partial<C>(stage[j - 1], acc, lane);
     }
     __syncthreads();
   }
   if (q != 0) return;
   int nt, mt, sp;
   tile_coords(tm, tm.sk_first + s, nt, mt, sp);
-  epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane, inv_freq);
+  epilogue<EPI, C>(p, acc, nt, mt, sp, wn, wm, lane);
 }
 
 }  // namespace
 
-// 8 waves (2 per SIMD), each wave 128 weight rows x BM / 4 activation rows;
-// BK 64.  The 256 x 256 tile reads 0.75 KB of LDS per MFMA; the 256 x 128
-// tile (1.25 KB per MFMA) doubles the tile count for row counts that would
-// leave CUs idle.
-using GemmCfg = Cfg<256, 256, 2, 4, 64>;
+// The 256 x 128 tile (8 waves, 1.25 KB of LDS reads per 32x32x16 MFMA)
+// doubles the tile count for row counts that would leave CUs idle.
+// 256 x 256 tiles: 4 waves of 128 x 128 on 16x16x32 MFMAs (gemm_bf16_w4_kernel);
+// 256 x 128 tiles: the 8-wave ping-pong kernel on 32x32x16 MFMAs
+using GemmCfg = Cfg<256, 256, 2, 2, 64>;
 using GemmCfgH = Cfg<256, 128, 2, 4, 64>;
 
 namespace {
@@ -639,15 +1002,35 @@ template <class C>
 hipError_t launch_plan(GemmEpi epi, const GemmParams& p, const Plan& pl, hipStream_t s) {
   const TileMap& tm = pl.tm;
   const dim3 grid(pl.grid), block(C::THREADS);
-  switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
-    case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
-    case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
+  if constexpr (C::WAVES == 4) {
+    switch (epi) {
+      case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_w4_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
+      case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_w4_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
+      case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_w4_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
+      case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_w4_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_w4_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
+    }
+  } else {
+    switch (epi) {
+      case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_STORE, C>), grid, block, 0, s, p, tm); break;
+      case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_ACCUM, C>), grid, block, 0, s, p, tm); break;
+      case EPI_PARTIAL: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_PARTIAL, C>), grid, block, 0, s, p, tm); break;
+      case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_QKV, C>), grid, block, 0, s, p, tm); break;
+      case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_kernel<EPI_SWIGLU, C>), grid, block, 0, s, p, tm); break;
+    }
   }
   if (pl.sk_tiles > 0) {
     const dim3 fgrid(pl.sk_tiles * C::WAVES), fblock(256);
+    if constexpr (C::WAVES == 4) {
+      switch (epi) {
+        case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup16<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup16<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_fixup16<EPI_QKV, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_fixup16<EPI_SWIGLU, C>), fgrid, fblock, 0, s, p, tm); break;
+        default: break;
+      }
+      return hipGetLastError();
+    }
     switch (epi) {
       case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
       case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;

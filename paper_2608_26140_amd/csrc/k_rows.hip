@@ -663,6 +663,29 @@ hipError_t launch_reduce_residual(void* x, const float* part, int splits, int M,
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- rotary table
+// One thread per (row, pair): the angle pos * theta_d in fp64 (theta_d =
+// base^(-2d/128)), reduced and evaluated by rotary_sincos as everywhere else
+// on the path; the QKV projection's epilogue reads it for all its heads.
+__global__ __launch_bounds__(256) void rope_table_kernel(const int32_t* __restrict__ pos, int M, double l2b,
+                                                         float* __restrict__ table) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)M * 64) return;
+  const int m = (int)(i >> 6), d = (int)(i & 63);
+  float sn, cs;
+  rotary_sincos((double)pos[m] * exp2(-(2.0 * d / 128.0) * l2b), &sn, &cs);
+  const float2 v = {cs, sn};
+  reinterpret_cast<float2*>(table)[i] = v;
+}
+
+hipError_t launch_rope_table(const int32_t* pos, int M, float rope_base, float* table, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  const int64_t n = (int64_t)M * 64;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pos, M,
+                     log2((double)rope_base), table);
+  return hipGetLastError();
+}
+
 hipError_t launch_q_rotary_reduce(const float* part, int splits, int n, int H, const int32_t* rows,
                                   const int32_t* pos, float rope_base, void* q, int64_t q_n_rows, hipStream_t s) {
   if (n <= 0) return hipSuccess;
