@@ -80,7 +80,7 @@ struct TileMap {
   float* sk_part;  // [sk_groups][2][THREADS * ACC4 * 4] partial accumulators
 };
 
-constexpr int kGroupM = 8;       // M tiles per raster group
+constexpr int kGroupM = 4;       // M tiles per raster group
 constexpr int kMaxSkGroups = 256;
 constexpr int kMinSkSteps = 4;   // K steps per tile for stream-K, and per split, at least
 constexpr int kMaxSplits = 16;
@@ -463,10 +463,7 @@ __global__ __launch_bounds__(C::THREADS) void gemm_bf16_kernel(GemmParams p, Til
 // D[4 (l / 16) + r][l % 16] in accumulator register r = 0..3.  With the
 // weights as A, lane l holds activation row l % 16 and output columns
 // 4 (l / 16) .. + 3 of each 16 x 16 tile.
-__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-// The same MFMA with the accumulator held in AGPRs by the asm constraint
+// The accumulator is held in AGPRs by the asm constraint
 // (the compiler otherwise moves a 256-register accumulator set between
 // AGPRs and VGPRs on every loop iteration).  The hazard recognizer does not
 // look into inline asm: callers pad with s_nop where the accumulators pass
@@ -489,27 +486,18 @@ __device__ __forceinline__ void store_partial16(float* base, const Acc16& acc, i
 #pragma unroll
     for (int b = 0; b < 8; ++b) *reinterpret_cast<f32x4*>(base + ((a * 8 + b) * 64 + lane) * 4) = acc[a][b];
 }
-__device__ __forceinline__ void add_partial16(const float* base, Acc16& acc, int lane) {
-#pragma unroll
-  for (int a = 0; a < 8; ++a)
-#pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(base + ((a * 8 + b) * 64 + lane) * 4);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[a][b][j] += v[j];
-    }
-}
 
 // Writes one wave's accumulators (wave (wn, wm) of 256 x 256 tile (nt, mt),
-// split sp): the same epilogues as the 32x32 layout.
-template <int EPI>
-__device__ __forceinline__ void epilogue16(const GemmParams& p, const Acc16& acc, int nt, int mt, int sp, int wn,
-                                           int wm, int lane) {
+// split sp): the same epilogues as the 32x32 layout.  acc[a][bb] holds the
+// 16-row block b = B0 + bb (NB of the wave's 8).
+template <int EPI, int B0 = 0, int NB = 8>
+__device__ __forceinline__ void epilogue16(const GemmParams& p, const f32x4 (&acc)[8][NB], int nt, int mt, int sp,
+                                           int wn, int wm, int lane) {
   const int q4 = 4 * (lane >> 4);
   const int mbase = mt * 256 + wm * 128 + (lane & 15);
 #pragma unroll
-  for (int b = 0; b < 8; ++b) {
-    const int m = mbase + b * 16;
+  for (int b = 0; b < NB; ++b) {
+    const int m = mbase + (B0 + b) * 16;
     if (m >= p.M) continue;
     if constexpr (EPI == EPI_STORE || EPI == EPI_ACCUM || EPI == EPI_PARTIAL) {
       const int nbase = nt * 256 + wn * 128 + q4;
@@ -777,13 +765,12 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
   }
 }
 
-// Stream-K fixup of the 16x16 tiles: as gemm_bf16_fixup, two pieces staged
-// per round.
+// Stream-K fixup of the 16x16 tiles: block = one wave-tile of one split
+// tile of the stream-K region; its wave q sums the rows 32 q .. 32 q + 31 of
+// the tile's pieces in workgroup order and runs their epilogue.
 template <int EPI, class C>
 __global__ __launch_bounds__(256) void gemm_bf16_fixup16(GemmParams p, TileMap tm) {
   constexpr int kPieceF = 64 * 256;  // floats per wave piece
-  constexpr int kDepth = 2;
-  __shared__ __attribute__((aligned(16))) float stage[kDepth][kPieceF];
   const int tid = threadIdx.x, lane = tid & 63;
   const int q = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int s = blockIdx.x / C::WAVES, wave = blockIdx.x % C::WAVES;
@@ -791,36 +778,43 @@ __global__ __launch_bounds__(256) void gemm_bf16_fixup16(GemmParams p, TileMap t
   const int nk_tile = tm.nk;
   const int first = sk_owner(tm, s * nk_tile), last = sk_owner(tm, (s + 1) * nk_tile - 1);
   if (first == last) return;  // the tile was finished by one workgroup
-  auto piece = [&](int w) {
-    const int pc = sk_start(tm, w) / nk_tile == s ? 0 : 1;
-    return tm.sk_part + ((size_t)(w * 2 + pc) * C::WAVES + wave) * kPieceF;
-  };
-  Acc16 acc;
-#pragma unroll
-  for (int a = 0; a < 8; ++a)
-#pragma unroll
-    for (int b = 0; b < 8; ++b)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) acc[a][b][r] = 0.f;
-  for (int w0 = first; w0 <= last; w0 += kDepth + 1) {
-    if (q > 0 && q <= kDepth && w0 + q <= last) {
-      const float* src = piece(w0 + q);
-      float* dst = stage[q - 1];
-#pragma unroll 8
-      for (int i = 0; i < 64; ++i)
-        *reinterpret_cast<f32x4*>(dst + (i * 64 + lane) * 4) = *reinterpret_cast<const f32x4*>(src + (i * 64 + lane) * 4);
-    }
-    if (q == 0) add_partial16(piece(w0), acc, lane);
-    __syncthreads();
-    if (q == 0) {
-      for (int j = 1; j <= kDepth && w0 + j <= last; ++j) add_partial16(stage[j - 1], acc, lane);
-    }
-    __syncthreads();
-  }
-  if (q != 0) return;
   int nt, mt, sp;
   tile_coords(tm, tm.sk_first + s, nt, mt, sp);
-  epilogue16<EPI>(p, acc, nt, mt, sp, wn, wm, lane);
+  auto run = [&](auto qc) {
+    constexpr int Q = decltype(qc)::value;
+    f32x4 acc[8][2];
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[a][bb][r] = 0.f;
+#pragma unroll 2
+    for (int w = first; w <= last; ++w) {
+      // piece 0 of w if w's range starts in this tile, else its piece 1
+      const int pc = sk_start(tm, w) / nk_tile == s ? 0 : 1;
+      const float* src = tm.sk_part + ((size_t)(w * 2 + pc) * C::WAVES + wave) * kPieceF;
+      f32x4 v[8][2];
+#pragma unroll
+      for (int a = 0; a < 8; ++a)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+          v[a][bb] = *reinterpret_cast<const f32x4*>(src + ((a * 8 + 2 * Q + bb) * 64 + lane) * 4);
+#pragma unroll
+      for (int a = 0; a < 8; ++a)
+#pragma unroll
+        for (int bb = 0; bb < 2; ++bb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[a][bb][r] += v[a][bb][r];
+    }
+    epilogue16<EPI, 2 * Q, 2>(p, acc, nt, mt, sp, wn, wm, lane);
+  };
+  switch (q) {
+    case 0: run(std::integral_constant<int, 0>()); break;
+    case 1: run(std::integral_constant<int, 1>()); break;
+    case 2: run(std::integral_constant<int, 2>()); break;
+    default: run(std::integral_constant<int, 3>()); break;
+  }
 }
 
 // Stream-K fixup: block = one wave-tile of one split tile of the stream-K

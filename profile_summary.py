@@ -34,10 +34,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 
 # operation -> (kernel-name patterns summed per launch unit, pattern that counts units)
 OPERATIONS = {
-    "gemm_gate_up": ([r"gemm_bf16_kernel<4,", r"gemm_bf16_fixup<4,"], r"gemm_bf16_kernel<4,"),
-    "gemm_qkv": ([r"gemm_bf16_kernel<3,", r"gemm_bf16_fixup<3,"], r"gemm_bf16_kernel<3,"),
-    "gemm_accum": ([r"gemm_bf16_kernel<1,", r"gemm_bf16_fixup<1,"], r"gemm_bf16_kernel<1,"),
-    "gemm_partial": ([r"gemm_bf16_kernel<2,"], r"gemm_bf16_kernel<2,"),
+    # 256 x 256 tiles run gemm_bf16_w4_kernel (+ gemm_bf16_fixup16), 256 x 128 tiles gemm_bf16_kernel
+    "gemm_gate_up": ([r"gemm_bf16_(w4_)?kernel<4,", r"gemm_bf16_fixup(16)?<4,"], r"gemm_bf16_(w4_)?kernel<4,"),
+    "gemm_qkv": ([r"gemm_bf16_(w4_)?kernel<3,", r"gemm_bf16_fixup(16)?<3,"], r"gemm_bf16_(w4_)?kernel<3,"),
+    "gemm_accum": ([r"gemm_bf16_(w4_)?kernel<1,", r"gemm_bf16_fixup(16)?<1,"], r"gemm_bf16_(w4_)?kernel<1,"),
+    "gemm_partial": ([r"gemm_bf16_(w4_)?kernel<2,"], r"gemm_bf16_(w4_)?kernel<2,"),
     "attention": ([r"attention_(pv|wide)_kernel", r"attention_merge_kernel"], r"attention_(pv|wide)_kernel"),
     "score": ([r"score_fused_kernel"], r"score_fused_kernel"),
     "score_reduce": ([r"head_reduce_kernel"], r"head_reduce_kernel"),
