@@ -45,6 +45,10 @@ struct AttnArgs {
   int H, Hkv;
   int batch;
   int row_start[kMaxBatch + 1];
+  // the rows of request b this launch takes: row_start[b] + row_lo[b] ..
+  // + row_n[b] - 1 (a launch may take a part of each request's rows)
+  int row_lo[kMaxBatch];
+  int row_n[kMaxBatch];
   int key_start[kMaxBatch + 1];
   int key_len[kMaxBatch + 1];
   int tile_start[kMaxBatch + 1];
@@ -139,7 +143,8 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   }
   const int g = h / (a.H / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, hl = lane >> 5;
-  const int n_rows = a.row_start[b + 1] - a.row_start[b];
+  const int n_rows = a.row_n[b];
+  const int64_t r0 = (int64_t)a.row_start[b] + a.row_lo[b];  // global row of query 0
   const int qi = (tile - a.tile_start[b]) * kPvTileQ + wave * 32 + (lane & 31);
   const bool q_ok = qi < n_rows;
   // a wavefront without a valid query only copies and synchronises
@@ -151,7 +156,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 
   bf16x8 qf[8];
   {
-    int64_t qrow = q_ok ? (int64_t)a.row_start[b] + qi : -1;
+    int64_t qrow = q_ok ? r0 + qi : -1;
     const bf16* qp = a.q + (qrow < 0 ? 0 : qrow) * a.q_ld + h * kDh + hl * 8;
 #pragma unroll
     for (int s2 = 0; s2 < 8; ++s2) {
@@ -163,7 +168,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 
   const uint64_t* mrow = nullptr;  // this query row's key mask (MASK)
   if constexpr (MASK) {
-    if (q_ok) mrow = pa.key_mask + (int64_t)((a.row_start[b] + qi) / pa.mask_rows) * pa.mask_tiles;
+    if (q_ok) mrow = pa.key_mask + (int64_t)((r0 + qi) / pa.mask_rows) * pa.mask_tiles;
   }
 
   // this lane's 4 keys of a tile (one per load): key 16 wave + 4 i + lane / 16,
@@ -326,7 +331,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 
   const float l_tot = l_part + __shfl_xor(l_part, 32);
   if (!q_ok) return;
-  const int64_t row = a.row_start[b] + qi;
+  const int64_t row = r0 + qi;
   if (splits > 1 || pa.partial) {
     // unnormalised partial: O^T register r of block d holds dims 32 d + 8 (r / 4) + 4 hl + r % 4
     const int64_t prow = pa.partial ? pa.part_rows : (int64_t)a.row_start[a.batch];
@@ -512,7 +517,8 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
   const int g = h / (a.H / a.Hkv);
   const int tid = threadIdx.x, lane = tid & 63, hl = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n_rows = a.row_start[b + 1] - a.row_start[b];
+  const int n_rows = a.row_n[b];
+  const int64_t r0 = (int64_t)a.row_start[b] + a.row_lo[b];  // global row of query 0
   const int q0 = (tile - a.tile_start[b]) * C::kTileQ + wave * 32 * QB;
   int qi[QB];
 #pragma unroll
@@ -527,7 +533,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const bool ok = qi[qb] < n_rows;
-    const int64_t qrow = ok ? (int64_t)a.row_start[b] + qi[qb] : 0;
+    const int64_t qrow = ok ? r0 + qi[qb] : 0;
     const bf16* qp = a.q + qrow * a.q_ld + h * kDh + hl * 8;
 #pragma unroll
     for (int s2 = 0; s2 < 8; ++s2) {
@@ -807,7 +813,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
   for (int qb = 0; qb < QB; ++qb) {
     const float l_tot = l_part[qb] + __shfl_xor(l_part[qb], 32);
     if (qi[qb] >= n_rows) continue;
-    const int64_t row = a.row_start[b] + qi[qb];
+    const int64_t row = r0 + qi[qb];
     if (splits > 1) {
       const int64_t prow = (int64_t)a.row_start[a.batch];
       float* po = pa.part_o + (((int64_t)split * prow + row) * a.H + h) * kDh;
@@ -904,12 +910,16 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   }
   const int64_t rows = rg.cu_rows[rg.batch];
   if (rows == 0) return hipSuccess;
-  int tiles = 0, tiles_w = 0, max_kt = 0;
+  int tiles = 0, tiles_w = 0, max_kt = 0, full_w = 0, rem_n = 0;
   for (int b = 0; b < rg.batch; ++b) {
     a.key_len[b] = rg.cu_keys[b + 1] - rg.cu_keys[b];
     const int nr = a.row_start[b + 1] - a.row_start[b];
+    a.row_lo[b] = 0;
+    a.row_n[b] = nr;
     tiles += (nr + kPvTileQ - 1) / kPvTileQ;
     tiles_w += (nr + WideQ::kTileQ - 1) / WideQ::kTileQ;
+    full_w += nr / WideQ::kTileQ;
+    rem_n += (nr % WideQ::kTileQ + kPvTileQ - 1) / kPvTileQ;
     max_kt = std::max(max_kt, (a.key_len[b] + kTileK - 1) / kTileK);
   }
   if (tiles == 0) return hipSuccess;
@@ -917,9 +927,37 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   double cost_n = 0.0, cost_w = 0.0;
   const int splits_n = attention_splits(tiles * H, 512, 1.0, max_kt, rows, H, pbytes, &cost_n);
   const int splits_w = attention_splits(tiles_w * H, 256, kWideTileCost, max_kt, rows, H, pbytes, &cost_w);
+  const bool wide_ok = (uint64_t)n_slots * (uint64_t)pool_ld * 2u <= (uint64_t)kWdAbsent;
   // the wide kernel only where its workgroups fill at least one round of CUs
-  const bool wide = cost_w < cost_n && tiles_w * H * splits_w >= 256 &&
-                    (uint64_t)n_slots * (uint64_t)pool_ld * 2u <= (uint64_t)kWdAbsent;
+  const bool wide = wide_ok && cost_w < cost_n && tiles_w * H * splits_w >= 256;
+  // split: each request's whole 256-row tiles on the wide kernel and its
+  // last partial tile (in 128-row tiles) on the two-per-CU kernel, one launch
+  // each, no key splits (the merge kernel would cover every row)
+  const double cost_split = (double)((full_w * H + 255) / 256) * max_kt * kWideTileCost +
+                            (double)((rem_n * H + 511) / 512) * max_kt;
+  if (wide_ok && full_w * H >= 256 && rem_n > 0 && cost_split < std::min(cost_w, cost_n)) {
+    pa.splits = 1;
+    int acc = 0;
+    for (int b = 0; b < rg.batch; ++b) {
+      const int nr = a.row_start[b + 1] - a.row_start[b];
+      a.row_n[b] = nr - nr % WideQ::kTileQ;
+      a.tile_start[b] = acc;
+      acc += a.row_n[b] / WideQ::kTileQ;
+    }
+    a.tile_start[rg.batch] = acc;
+    hipLaunchKernelGGL((attention_wide_kernel<kWideQB, kWideWaves>), dim3(acc * H), dim3(WideQ::kThreads), 0, s, pa);
+    acc = 0;
+    for (int b = 0; b < rg.batch; ++b) {
+      const int nr = a.row_start[b + 1] - a.row_start[b];
+      a.row_lo[b] = nr - nr % WideQ::kTileQ;
+      a.row_n[b] = nr % WideQ::kTileQ;
+      a.tile_start[b] = acc;
+      acc += (a.row_n[b] + kPvTileQ - 1) / kPvTileQ;
+    }
+    a.tile_start[rg.batch] = acc;
+    hipLaunchKernelGGL(attention_pv_kernel<false>, dim3(acc * H), dim3(kPvThreads), 0, s, pa);
+    return hipGetLastError();
+  }
   const int tq = wide ? WideQ::kTileQ : kPvTileQ;
   const int splits = wide ? splits_w : splits_n;
   int acc_tiles = 0;
@@ -1016,6 +1054,8 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
     a.batch = 1;
     a.row_start[0] = 0;
     a.row_start[1] = (int)rows;
+    a.row_lo[0] = 0;
+    a.row_n[0] = (int)rows;
     a.key_start[0] = 0;
     a.key_start[1] = L;
     a.key_len[0] = L;
@@ -1036,6 +1076,10 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
     a.batch = batch;
     for (int b = 0; b <= batch; ++b) {
       a.row_start[b] = b * rows_per_req;
+      if (b < batch) {
+        a.row_lo[b] = 0;
+        a.row_n[b] = rows_per_req;
+      }
       a.key_start[b] = b * private_len;
       a.tile_start[b] = b * q_tiles_req;
     }

@@ -236,6 +236,38 @@ def test_attention_wide_tiles_and_absent_slots(A, H, Hkv, rows, keys):
     assert_close(down(lse), lse_ref, dtype, "attention lse")
 
 
+def test_attention_whole_tiles_and_remainders(A):
+    """Serving-like launch (16 requests of 2150 rows, 32 heads): the launcher
+    runs each request's whole 256-row tiles on the wide kernel and its last
+    102 rows, in a second launch, on the 128-row kernel.  Sampled rows of
+    both launches (first and last rows of each part) are checked against the
+    oracle; every output row must be written (finite)."""
+    torch = _torch()
+    dtype, H, Hkv, dh = "bf16", 32, 32, 128
+    B, R, S = 16, 2150, 160
+    rows, keys = [R] * B, [S + 7 * b for b in range(B)]
+    q, kp, vp, slots, cu_rows, cu_keys, n_slots = _attn_case(dtype, H, Hkv, dh, rows, keys, seed=2150)
+    dims = A.make_dims(4096, H, Hkv, dh, 128, dtype)
+    lse = torch.full((sum(rows), H), float("nan"), dtype=torch.float32, device="cuda")
+    out = torch.full((sum(rows), H * dh), float("nan"), dtype=torch.bfloat16, device="cuda")
+    A.acache_attention(dims, cu_rows, cu_keys, up(q, dtype), up_i32(slots), up(kp, dtype), up(vp, dtype),
+                       out=out, lse=lse)
+    g_out, g_lse = down(out), down(lse)
+    assert np.all(np.isfinite(g_out)) and np.all(np.isfinite(g_lse)), "a row was not written"
+    f = lambda a: O.from_bits(a, dtype)
+    pick = [0, 1, 255, 1023, 2047, 2048, 2049, 2100, R - 2, R - 1]
+    sel, sub_rows = [], []
+    for b in range(B):
+        sel += [cu_rows[b] + i for i in pick]
+        sub_rows.append(len(pick))
+    sel = np.array(sel)
+    sub_cu = np.concatenate([[0], np.cumsum(sub_rows)]).astype(int).tolist()
+    o_ref, lse_ref = O.attention_via_slots(f(q)[sel].reshape(-1, H, dh), f(kp).reshape(-1, Hkv, dh),
+                                           f(vp).reshape(-1, Hkv, dh), slots, sub_cu, cu_keys)
+    assert_close(g_out[sel], o_ref.reshape(len(sel), H * dh), dtype, "attention out (sampled rows)")
+    assert_close(g_lse[sel], lse_ref, dtype, "attention lse (sampled rows)")
+
+
 def test_attention_rows_sum_to_one(A):
     """V = 1 gives O = 1 exactly up to rounding: attention rows sum to one."""
     torch = _torch()
