@@ -32,7 +32,9 @@ import sys
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
-# operation -> (kernel-name patterns summed per launch unit, pattern that counts units)
+# operation -> (kernel-name patterns summed per launch unit, pattern that starts a unit); launches of
+# one operation that follow each other directly are one unit (attention's whole-tile and remainder
+# kernels, a GEMM and its stream-K fixup)
 OPERATIONS = {
     # 256 x 256 tiles run gemm_bf16_w4_kernel (+ gemm_bf16_fixup16), 256 x 128 tiles gemm_bf16_kernel
     "gemm_gate_up": ([r"gemm_bf16_(w4_)?kernel<4,", r"gemm_bf16_fixup(16)?<4,"], r"gemm_bf16_(w4_)?kernel<4,"),
@@ -56,7 +58,11 @@ def short(name: str) -> str:
 
 
 def _rows(path):
-    return list(csv.DictReader(open(path)))
+    """CSV rows in launch order (the trace lists kernels as they complete)."""
+    rows = list(csv.DictReader(open(path)))
+    if rows and "Dispatch_Id" in rows[0]:
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+    return rows
 
 
 def _col(row, *names):
@@ -94,16 +100,18 @@ def stats(argv):
     if os.path.exists(trace) and op:
         seg = _segment(_rows(trace), steps)
         pats, unit = OPERATIONS[op]
-        durs, n_units = [], 0
+        durs, n_units, prev = [], 0, False
         for r in seg:
             k = _col(r, "Kernel_Name", "Name")
-            if any(re.search(p, k) for p in pats):
+            hit = any(re.search(p, k) for p in pats)
+            if hit:
                 d = int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))
-                if re.search(unit, k):
+                if re.search(unit, k) and not prev:
                     durs.append(d)
                     n_units += 1
                 else:
                     durs[-1] += d
+            prev = hit
         mean = sum(durs) / max(n_units, 1) / 1e3
         lines += ["", f"Dominant kernel ({roof['kernel']}): {n_units} launches in the last {steps} steps of the trace "
                   f"({n_units / steps:g} per step), mean {mean:.2f} us per launch (a stream-K launch counts its fixup);",
@@ -132,12 +140,14 @@ def traffic(argv):
 
     def per_unit(path, pats, unit):
         seg = _segment(_rows(path), steps)
-        tot, units = 0.0, 0
+        tot, units, prev = 0.0, 0, False
         for r in seg:
             k = _col(r, "Kernel_Name")
-            if any(re.search(p, k) for p in pats):
+            hit = any(re.search(p, k) for p in pats)
+            if hit:
                 tot += float(_col(r, "Counter_Value"))
-                units += bool(re.search(unit, k))
+                units += bool(re.search(unit, k)) and not prev
+            prev = hit
         return tot / max(units, 1), units / steps
 
     lines = [f"# HBM traffic per launch: {workload} step (rocprofv3 FETCH_SIZE / WRITE_SIZE)", "",
@@ -147,7 +157,7 @@ def traffic(argv):
              f"  FETCH_SIZE reads {copy_mean(cfetch):.0f} KiB -> read scale {rs:.4f}; "
              f"WRITE_SIZE {copy_mean(cwrite):.0f} KiB -> write scale {ws:.4f}", "",
              f"Launches of the last {steps} step(s); a stream-K GEMM launch counts its fixup kernel, attention its",
-             "key-split merge kernel.", "",
+             "remainder-tile and key-split merge kernels.", "",
              f"{'operation':14s} {'per step':>8s} {'fetch_KiB':>11s} {'write_KiB':>11s} {'MB/launch':>10s}"]
     tfile = os.path.join(ROOT, "profiles", "traffic.json")
     rec = json.load(open(tfile)) if os.path.exists(tfile) else {}
