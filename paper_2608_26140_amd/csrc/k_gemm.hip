@@ -654,11 +654,16 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
     }
     const int k0 = kb * C::BK;
 
+    // the lane's copy offsets are recomputed per item from a lane index the
+    // compiler cannot see through: hoisted out of the item loop they are
+    // held through the K loop, spilled, and reloaded one wait at a time
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
     uint32_t wsrc[8], xsrc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const int r = wave * 64 + i * 8 + crow;
-      const int c = (lane & 7) ^ ((4 * i + (lane >> 4)) & 7);
+      const int r = wave * 64 + i * 8 + (ln >> 3);
+      const int c = (ln & 7) ^ ((4 * i + (ln >> 4)) & 7);
       wsrc[i] = (uint32_t)(weight_row<EPI, 256>(nt, r, F) * K + k0 + c * 8) * 2u;
       xsrc[i] = (uint32_t)(min(mt * C::BM + r, p.M - 1) * K + k0 + c * 8) * 2u;
     }
