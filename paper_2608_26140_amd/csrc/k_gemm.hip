@@ -493,6 +493,9 @@ __device__ __forceinline__ void store_partial16(float* base, const Acc16& acc, i
 template <int EPI, int B0 = 0, int NB = 8>
 __device__ __forceinline__ void epilogue16(const GemmParams& p, const f32x4 (&acc)[8][NB], int nt, int mt, int sp,
                                            int wn, int wm, int lane) {
+  // lane-dependent addresses are computed here, per item: hoisted out of the
+  // item loop they would be held through the K loop and spilled
+  asm volatile("" : "+v"(lane));
   const int q4 = 4 * (lane >> 4);
   const int mbase = mt * 256 + wm * 128 + (lane & 15);
 #pragma unroll
