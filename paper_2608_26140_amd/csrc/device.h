@@ -61,6 +61,15 @@ __device__ __forceinline__ void wait_lgkmcnt() {
   __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
 }
 
+// This lane's index in its wavefront, computed where it is called: the
+// compiler cannot hoist the asm out of a loop, so nothing derived from the
+// lane index has to stay live (or be spilled) across the loop's body.
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n v_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // Workgroup barrier that orders LDS only.  __syncthreads() also waits for
 // every outstanding global load, which would include loads in flight to
 // LDS for later stages; those are tracked with explicit vmcnt waits.

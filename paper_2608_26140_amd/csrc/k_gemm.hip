@@ -495,7 +495,7 @@ __device__ __forceinline__ void epilogue16(const GemmParams& p, const f32x4 (&ac
                                            int wn, int wm, int lane) {
   // lane-dependent addresses are computed here, per item: hoisted out of the
   // item loop they would be held through the K loop and spilled
-  asm volatile("" : "+v"(lane));
+  lane = lane_id_here();
   const int q4 = 4 * (lane >> 4);
   const int mbase = mt * 256 + wm * 128 + (lane & 15);
 #pragma unroll
@@ -658,10 +658,9 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
     const int k0 = kb * C::BK;
 
     // the lane's copy offsets are recomputed per item from a lane index the
-    // compiler cannot see through: hoisted out of the item loop they are
-    // held through the K loop, spilled, and reloaded one wait at a time
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
+    // compiler cannot hoist: hoisted out of the item loop they are held
+    // through the K loop, spilled, and reloaded one wait at a time
+    const int ln = lane_id_here();
     uint32_t wsrc[8], xsrc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -694,9 +693,11 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[a][b][r] = 0.f;
 
-    // the previous item's stores and copies are complete, and every wave is
-    // past its last LDS read of the previous item
-    wait_vmcnt<0>();
+    // every wave is past its last LDS read of the previous item (the copies
+    // of the previous item have landed before its epilogue).  Its stores need
+    // not drain before these copies go out: loads complete in issue order, so
+    // the wait for step 0 below holds however the stores complete, and the
+    // copies' latency overlaps the stores' drain.
     lds_barrier();
     issue(0);
     if (kn > 1) {
