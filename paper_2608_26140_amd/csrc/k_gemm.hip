@@ -1037,14 +1037,14 @@ hipError_t launch_plan(GemmEpi epi, const GemmParams& p, const Plan& pl, hipStre
         case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_fixup16<EPI_SWIGLU, C>), fgrid, fblock, 0, s, p, tm); break;
         default: break;
       }
-      return hipGetLastError();
-    }
-    switch (epi) {
-      case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
-      case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
-      case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_QKV, C>), fgrid, fblock, 0, s, p, tm); break;
-      case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_SWIGLU, C>), fgrid, fblock, 0, s, p, tm); break;
-      default: break;
+    } else {
+      switch (epi) {
+        case EPI_STORE: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_STORE, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_ACCUM: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_ACCUM, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_QKV, C>), fgrid, fblock, 0, s, p, tm); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL((gemm_bf16_fixup<EPI_SWIGLU, C>), fgrid, fblock, 0, s, p, tm); break;
+        default: break;
+      }
     }
   }
   return hipGetLastError();
