@@ -136,11 +136,14 @@ def test_rmsnorm(A, dtype, d):
 # 256 x 256 tiles (T tiles, nk K steps of 64): (256, 3072, 4096) T = 12,
 # stream-K only; (520, 24576, 2048) T = 288, one data-parallel round +
 # stream-K over 32 tiles; (512, 32768, 256) T = 256, data-parallel;
-# (300, 4096, 128) nk = 2, too short for stream-K; the rest run data-parallel
-# by the cost model.
+# (300, 4096, 128) nk = 2, too short for stream-K; (1280, 16384, 64) T = 320
+# and (2304, 8192, 128) T = 288, two data-parallel rounds of one or two K
+# steps, so a workgroup's second tile starts right behind its first tile's
+# stores; the rest run data-parallel by the cost model.
 @pytest.mark.parametrize("schedule", ["dp", "sk"])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (77, 512, 256), (128, 256, 4096), (717, 768, 1024), (300, 4096, 128),
-                                   (256, 3072, 4096), (520, 24576, 2048), (512, 32768, 256)])
+                                   (256, 3072, 4096), (520, 24576, 2048), (512, 32768, 256), (1280, 16384, 64),
+                                   (2304, 8192, 128)])
 def test_linear_bf16(A, M, N, K, schedule):
     a = W.draw_tensor((M, K), "bf16", seed=M)
     w = W.draw_tensor((N, K), "bf16", std=0.05, seed=N + K)
