@@ -581,26 +581,30 @@ __device__ __forceinline__ void epilogue16(const GemmParams& p, const f32x4 (&ac
 // 128 x 128 wave tile = 8 x 8 MFMA 16x16x32 tiles, 256 fp32 accumulators
 // per lane (0.5 KB of LDS fragment reads per 32 x 32 x 16 of work).
 //
-// LDS holds two stages of one 64-wide K step: 256 weight rows and 256
-// activation rows of 128 bytes.  Each copy instruction moves 8 whole rows
-// (a 128-byte line per row, so every L2 request is a full line), buffer ->
-// LDS with no staging registers.  16-byte chunk c of row r sits at
-// c ^ ((r >> 1) & 7): the 16 rows read by one 16-lane pass of a fragment
-// read hit 16 distinct bank groups.  The MFMAs run in 32-wide units, two per
-// stage.  Before unit u each wave waits for its fragment reads of unit u and
-// meets the others at a barrier; it then reads unit u + 1's 16 fragments
-// into the other register set, one read after every fourth of unit u's 64
-// MFMAs.  At the second unit of step j (after its barrier every wave holds
-// step j in registers or is done with it) the copies of step j + 2 go into
-// step j's stage, and the wait before that barrier makes step j + 1
-// complete: copies have two units (2048 MFMA cycles) to land.
+// LDS holds the 256 weight rows of three 64-wide K steps and the 256
+// activation rows of two, rows of 128 bytes (160 KB in all).  Each copy
+// instruction moves 8 whole rows (a 128-byte line per row, so every L2
+// request is a full line), buffer -> LDS with no staging registers.  16-byte
+// chunk c of row r sits at c ^ ((r >> 1) & 7): the 16 rows read by one
+// 16-lane pass of a fragment read hit 16 distinct bank groups.  The MFMAs
+// run in 32-wide units, two per step.  Before unit u each wave waits for its
+// fragment reads of unit u and meets the others at a barrier; it then reads
+// unit u + 1's 16 fragments into the other register set, one read after
+// every fourth of unit u's 64 MFMAs.  Unit 0 of step j sends step j + 2's
+// weight rows into the weight stage of step j - 1 (every wave was done with
+// it at the barrier before unit 1 of step j - 1), unit 1 its activation rows
+// into step j's activation stage, one copy after every eighth MFMA: the L2 ->
+// LDS path carries the same load in both units, and step j + 1 is complete
+// once no more than step j + 2's weight copies are in flight.
 constexpr int kW4RowB = 128;
+constexpr int kW4StageB = 256 * kW4RowB;  // one operand's rows of one K step
 
 template <int EPI, class C>
 __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams p, TileMap tm) {
   static_assert(C::BN == 256 && C::BM == 256 && C::WN == 2 && C::WM == 2 && C::BK == 64, "4-wave tile");
-  constexpr int kStageB = 512 * kW4RowB;
-  __shared__ __attribute__((aligned(1024))) char ring[2 * kStageB];
+  // weight stages 0..2, then activation stages 0..1
+  __shared__ __attribute__((aligned(1024))) char ring[5 * kW4StageB];
+  char* const xring = ring + 3 * kW4StageB;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -617,7 +621,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
   // fragment reads: row lane % 16 of each 16-row fragment, chunk 4 h + lane / 16
   const int fsw = ((lane & 15) >> 1) & 7;
   const int arow = wn * 128 + (lane & 15);
-  const int brow = 256 + wm * 128 + (lane & 15);
+  const int brow = wm * 128 + (lane & 15);
   const int cofs0 = ((0 + (lane >> 4)) ^ fsw) * 16;
   const int cofs1 = ((4 + (lane >> 4)) ^ fsw) * 16;
   const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(p.W, (uint32_t)p.N * (uint32_t)K * 2u);
@@ -669,19 +673,24 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
       wsrc[i] = (uint32_t)(weight_row<EPI, 256>(nt, r, F) * K + k0 + c * 8) * 2u;
       xsrc[i] = (uint32_t)(min(mt * C::BM + r, p.M - 1) * K + k0 + c * 8) * 2u;
     }
-    // copies of K step j of the item into stage j % 2
+    // copy i (0..7) of K step j: 8 weight rows into weight stage j % 3, or
+    // 8 activation rows into activation stage j % 2
+    auto copy_w = [&](int j, int i) {
+      dma16_buf(wres, wsrc[i], (uint32_t)j * 128u, ring + (j % 3) * kW4StageB + (wave * 64 + i * 8) * kW4RowB);
+    };
+    auto copy_x = [&](int j, int i) {
+      dma16_buf(xres, xsrc[i], (uint32_t)j * 128u, xring + (j & 1) * kW4StageB + (wave * 64 + i * 8) * kW4RowB);
+    };
     auto issue = [&](int j) {
-      char* st = ring + (j & 1) * kStageB;
-      const uint32_t ko = (uint32_t)j * 128u;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) dma16_buf(wres, wsrc[i], ko, st + (wave * 64 + i * 8) * kW4RowB);
+      for (int i = 0; i < 8; ++i) copy_w(j, i);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) dma16_buf(xres, xsrc[i], ko, st + (256 + wave * 64 + i * 8) * kW4RowB);
+      for (int i = 0; i < 8; ++i) copy_x(j, i);
     };
     // fragment f of unit h (0 / 1) of step j: f < 8 weight tile f, else
     // activation tile f - 8
     auto frag = [&](int j, int h, int f) {
-      const char* st = ring + (j & 1) * kStageB;
+      const char* st = f < 8 ? ring + (j % 3) * kW4StageB : xring + (j & 1) * kW4StageB;
       const int row = f < 8 ? arow + f * 16 : brow + (f - 8) * 16;
       return *reinterpret_cast<const bf16x8*>(st + row * kW4RowB + (h ? cofs1 : cofs0));
     };
@@ -714,46 +723,46 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
     for (int f = 0; f < 16; ++f) fx[f] = frag(0, 0, f);
     mfma_agpr_fence();  // the zeroed accumulators before the first MFMA
 
-    // copy i (0..15) of K step j: 8 weight rows then 8 activation rows per wave
-    auto copy_one = [&](int j, int i) {
-      char* st = ring + (j & 1) * kStageB;
-      const uint32_t ko = (uint32_t)j * 128u;
-      if (i < 8) dma16_buf(wres, wsrc[i], ko, st + (wave * 64 + i * 8) * kW4RowB);
-      else dma16_buf(xres, xsrc[i - 8], ko, st + (256 + wave * 64 + (i - 8) * 8) * kW4RowB);
-    };
     // 64 MFMAs from cur, the 16 reads of the next unit into nxt among them,
-    // and (cj >= 0) the 16 copies of K step cj, one after every fourth MFMA
-    // (a burst of copies stalls the wave's MFMA issue while the memory
-    // pipeline takes them)
-    auto unit = [&](bf16x8 (&cur)[16], bf16x8 (&nxt)[16], int nj, int nh, int cj, auto copies) {
+    // and (copies) the 8 weight (CX false) or activation (CX true) copies of
+    // K step cj, one after every eighth MFMA (a burst of copies stalls the
+    // wave's MFMA issue while the memory pipeline takes them)
+    auto unit = [&](bf16x8 (&cur)[16], bf16x8 (&nxt)[16], int nj, int nh, int cj, auto cx, auto copies) {
 #pragma unroll
       for (int i = 0; i < 64; ++i) {
         const int a = i >> 3, b = i & 7;
         if constexpr (decltype(copies)::value) {
-          if ((i & 3) == 1) copy_one(cj, i >> 2);
+          if ((i & 7) == 3) {
+            if constexpr (decltype(cx)::value) copy_x(cj, i >> 3);
+            else copy_w(cj, i >> 3);
+          }
         }
         if ((i & 3) == 0) nxt[i >> 2] = frag(nj, nh, i >> 2);
         mfma16x16x32_agpr(acc[a][b], cur[a], cur[8 + b]);
         __builtin_amdgcn_sched_barrier(0);
       }
     };
+    // K step j with (copies) the copies of step j + 2
     auto step = [&](int j, auto copies) {
-      // unit 0 of step j
+      constexpr bool CP = decltype(copies)::value;
+      // unit 0 of step j: the weight stage of step j - 1 is free (every wave
+      // passed the barrier before unit 1 of step j - 1 after its last read)
       wait_lgkmcnt<0>();
       __builtin_amdgcn_sched_barrier(0);
       bare_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      unit(fx, fy, j, 1, 0, std::false_type());
-      // unit 1 of step j: step j + 1 complete in every wave, step j's stage
-      // free for the copies of step j + 2
-      wait_vmcnt<0>();
+      unit(fx, fy, j, 1, j + 2, std::false_type(), copies);
+      // unit 1 of step j: step j + 1 complete in every wave (copies complete
+      // in issue order: in flight after it only step j + 2's weight rows),
+      // step j's activation stage free for step j + 2's
+      wait_vmcnt<CP ? 8 : 0>();
       wait_lgkmcnt<0>();
       __builtin_amdgcn_sched_barrier(0);
       bare_barrier();
       __builtin_amdgcn_sched_barrier(0);
       // after the last step this reads step j's own stage (complete, not
       // written any more); the values are not used
-      unit(fy, fx, j + 1 < kn ? j + 1 : j, 0, j + 2, copies);
+      unit(fy, fx, j + 1 < kn ? j + 1 : j, 0, j + 2, std::true_type(), copies);
       // every step ends with the MFMA results landed: the compiler may place
       // register copies or spill code of the accumulators on any loop edge
       // (the exit of the first loop below among them), and inline asm
