@@ -590,7 +590,8 @@ __device__ __forceinline__ void epilogue16(const GemmParams& p, const f32x4 (&ac
 // run in 32-wide units, two per step.  Before unit u each wave waits for its
 // fragment reads of unit u and meets the others at a barrier; it then reads
 // unit u + 1's 16 fragments into the other register set, one read after
-// every fourth of unit u's 64 MFMAs.  Unit 0 of step j sends step j + 2's
+// every third of unit u's first 46 MFMAs (the last read then has 18 MFMAs
+// to land before the unit's wait).  Unit 0 of step j sends step j + 2's
 // weight rows into the weight stage of step j - 1 (every wave was done with
 // it at the barrier before unit 1 of step j - 1), unit 1 its activation rows
 // into step j's activation stage, one copy after every eighth MFMA: the L2 ->
@@ -723,7 +724,8 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
     for (int f = 0; f < 16; ++f) fx[f] = frag(0, 0, f);
     mfma_agpr_fence();  // the zeroed accumulators before the first MFMA
 
-    // 64 MFMAs from cur, the 16 reads of the next unit into nxt among them,
+    // 64 MFMAs from cur, the 16 reads of the next unit into nxt among the
+    // first 46,
     // and (copies) the 8 weight (CX false) or activation (CX true) copies of
     // K step cj, one after every eighth MFMA (a burst of copies stalls the
     // wave's MFMA issue while the memory pipeline takes them)
@@ -737,7 +739,7 @@ __global__ __launch_bounds__(C::THREADS, 1) void gemm_bf16_w4_kernel(GemmParams 
             else copy_w(cj, i >> 3);
           }
         }
-        if ((i & 3) == 0) nxt[i >> 2] = frag(nj, nh, i >> 2);
+        if (i % 3 == 0 && i / 3 < 16) nxt[i / 3] = frag(nj, nh, i / 3);
         mfma16x16x32_agpr(acc[a][b], cur[a], cur[8 + b]);
         __builtin_amdgcn_sched_barrier(0);
       }
