@@ -9,8 +9,9 @@
 // head) in the same lane.
 //
 // Workgroup tiles: 256 weight rows x 256 activation rows, 4 waves (one per
-// SIMD) of 128 x 128 on MFMA 16x16x32 with the accumulators in AGPRs, two
-// LDS stages of a 64-wide K step (gemm_bf16_w4_kernel); or, where it
+// SIMD) of 128 x 128 on MFMA 16x16x32 with the accumulators in AGPRs, the
+// weight rows of three 64-wide K steps and the activation rows of two in
+// LDS (gemm_bf16_w4_kernel); or, where it
 // leaves fewer CUs idle, 256 x 128 with 8 waves (two per SIMD) of 128 x 32
 // on MFMA 32x32x16 and a ping-pong schedule over 32-wide K units
 // (gemm_bf16_kernel).  Both are fed by buffer -> LDS copies (no staging
