@@ -112,6 +112,18 @@ typedef struct {
                                  layer, so the caller need not clear scores).  Applies only to a call
                                  that scores (L > 0 and some masked rows); otherwise scores is left
                                  unchanged, as with init == 0 */
+  int32_t affix_keys_known;   /* acache_layer_recompute only; nonzero: every request's read slots hold
+                                 the affix keys in affix-local order from key index affix_key_begin,
+                                 read_slots[cu_keys[b] + affix_key_begin + j] == affix_slots[j] for
+                                 j < L.  Under ACACHE_NORM_AFFIX on the bf16 path the attention pass
+                                 then also takes each row's log-sum-exp over those keys and the score
+                                 uses it instead of its own pass over the affix keys (when
+                                 affix_key_begin is 0, L is a multiple of 64 and the attention needs
+                                 no key split; otherwise the score makes that pass itself).  Zero: no
+                                 such promise (any caller that leaves the field zeroed) */
+  int32_t affix_key_begin;    /* with affix_keys_known: key index of the first affix key, >= 0, the same
+                                 in every request; each request has at least affix_key_begin + L keys,
+                                 or the promise is ignored */
 } acache_score_args;
 
 /* Logical layout shared by every request of a batch, and its slot plan. */

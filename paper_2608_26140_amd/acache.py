@@ -45,7 +45,8 @@ class Ragged(ctypes.Structure):
 class ScoreArgs(ctypes.Structure):
     _fields_ = [("q_rows", ctypes.c_void_p), ("cu_q", ctypes.POINTER(ctypes.c_int32)),
                 ("affix_slots", ctypes.c_void_p), ("affix_len", ctypes.c_int32), ("norm", ctypes.c_int32),
-                ("scores", ctypes.c_void_p), ("init", ctypes.c_int32)]
+                ("scores", ctypes.c_void_p), ("init", ctypes.c_int32), ("affix_keys_known", ctypes.c_int32),
+                ("affix_key_begin", ctypes.c_int32)]
 
 
 class Layout(ctypes.Structure):
@@ -344,7 +345,9 @@ def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tenso
                            write_slots: torch.Tensor, read_slots: torch.Tensor, k_pool: torch.Tensor,
                            v_pool: torch.Tensor, ws: torch.Tensor, score: Optional[dict] = None, stream=None):
     """One block in place on x.  weights: LayerWeights or dict of tensors.
-    score: dict(q_rows, cu_q, affix_slots, scores, norm) for the probe."""
+    score: dict(q_rows, cu_q, affix_slots, scores, norm, init, and optionally
+    affix_key_begin: the key index at which every request's read slots hold
+    the affix slots in order) for the probe."""
     for t, n in ((pos, "pos"), (write_slots, "write_slots"), (read_slots, "read_slots")):
         _dev_i32(t, n)
     lw = weights if isinstance(weights, LayerWeights) else layer_weights(weights)
@@ -353,9 +356,11 @@ def acache_layer_recompute(dims: Dims, weights, cu_rows, cu_keys, x: torch.Tenso
     cq = None
     if score is not None:
         cq = _i32(score["cu_q"])
+        akb = score.get("affix_key_begin")
         sa = ScoreArgs(score["q_rows"].data_ptr(), cq, score["affix_slots"].data_ptr(),
                        score["affix_slots"].numel(), score.get("norm", ACACHE_NORM_AFFIX),
-                       score["scores"].data_ptr(), int(score.get("init", 0)))
+                       score["scores"].data_ptr(), int(score.get("init", 0)), int(akb is not None),
+                       int(akb or 0))
     _check("acache_layer_recompute", lib.acache_layer_recompute(
         ctypes.byref(dims), ctypes.byref(lw), ctypes.byref(rg), _ptr(x), _ptr(pos), _ptr(write_slots),
         _ptr(read_slots), _ptr(k_pool), _ptr(v_pool), k_pool.stride(0), k_pool.shape[0],

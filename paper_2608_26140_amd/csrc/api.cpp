@@ -177,18 +177,21 @@ T* at(void* ws, size_t off) {
 // Eq. 4-5 for one layer (shared by acache_score and the probe mode of
 // acache_layer_recompute).  lse_full: [q_n_rows, H] natural log, or NULL.
 // colsum: colsum_bytes of scratch for the per-head (and per-split) column
-// sums; lse_aff: [q_n_rows, H] scratch of the fp32 path.
+// sums; lse_aff: [q_n_rows, H] scratch of the fp32 path.  aff_given
+// (nullable, bf16): the rows' log-sum-exp over the affix keys already taken
+// (by the layer's attention), used instead of the score's own pass.
 acache_status run_score(const acache_dims* d, int batch, const int32_t* cu_q, const void* q,
                         int64_t q_ld, int64_t q_n_rows, const int32_t* q_rows, const void* k_pool,
                         int64_t pool_ld, int64_t n_slots, const int32_t* affix_slots, int L,
                         acache_norm norm, const float* lse_full, float* scores, float* lse_aff,
-                        float* colsum, size_t colsum_bytes, int init, hipStream_t s) {
+                        float* colsum, size_t colsum_bytes, int init, hipStream_t s,
+                        const float* aff_given = nullptr) {
   const int H = d->n_heads, Hkv = d->n_kv_heads, dh = d->head_dim;
   if (d->dtype == ACACHE_BF16) {
     int rows = H;
     LAUNCH_T(ACACHE_K_SCORE_COLSUM, s,
              launch_score_fused_bf16(batch, cu_q, H, Hkv, q, q_ld, q_n_rows, q_rows, k_pool, pool_ld, n_slots,
-                                     affix_slots, L, norm == ACACHE_NORM_FULL ? lse_full : nullptr, colsum,
+                                     affix_slots, L, norm == ACACHE_NORM_FULL ? lse_full : aff_given, colsum,
                                      colsum_bytes, &rows, s));
     LAUNCH_T(ACACHE_K_SCORE_REDUCE, s, launch_head_reduce(colsum, batch, rows, L, scores, init, s));
     return ACACHE_OK;
@@ -727,6 +730,18 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   void* hb = at<char>(ws, p.h);
   const bool probe = score && L > 0 && score->cu_q[r.batch] > 0;
   float* lse = (probe && score->norm == ACACHE_NORM_FULL) ? at<float>(ws, p.lse) : nullptr;
+  // under the affix normaliser the attention may take the rows' log-sum-exp
+  // over the affix keys for the score, where the caller promises every
+  // request reads them in order from key index affix_key_begin
+  float* lse_aff = nullptr;
+  if (probe && score->norm == ACACHE_NORM_AFFIX && dims->dtype == ACACHE_BF16 && score->affix_keys_known &&
+      score->affix_key_begin >= 0) {
+    bool fits = true;
+    for (int b = 0; b < r.batch; ++b)
+      fits = fits && (int64_t)r.cu_keys[b + 1] - r.cu_keys[b] >= (int64_t)score->affix_key_begin + L;
+    if (fits) lse_aff = at<float>(ws, p.lse_aff);
+  }
+  bool aff_done = false;
 
   LAUNCH_T(ACACHE_K_RMSNORM, stream, launch_rmsnorm(dims->dtype, x, w->attn_norm, y, M, d, dims->rms_eps, stream));
   if (dims->dtype == ACACHE_BF16) {
@@ -735,7 +750,8 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
     if (st != ACACHE_OK) return st;
     // the part region is idle between the QKV fixup and the O projection
     LAUNCH_T(ACACHE_K_ATTENTION, stream, launch_attention_bf16(r, H, Hkv, q, read_slots, k_pool, v_pool, pool_ld, n_slots, o, lse,
-                                                                at<float>(ws, p.part), p.part_bytes, stream));
+                                                                at<float>(ws, p.part), p.part_bytes, stream, lse_aff,
+                                                                lse_aff ? score->affix_key_begin : 0, L, &aff_done));
   } else {
     float* qkv = at<float>(ws, p.qkv);
     LAUNCH_T(ACACHE_K_GEMM_QKV, stream, launch_gemm_f32((const float*)y, (const float*)w->w_qkv, qkv, nqkv, M, nqkv, d, 0, stream));
@@ -747,7 +763,7 @@ acache_status acache_layer_recompute(const acache_dims* dims, const acache_layer
   if (probe) {
     st = run_score(dims, r.batch, score->cu_q, q, hq, M, score->q_rows, k_pool, pool_ld, n_slots,
                    score->affix_slots, L, score->norm, lse, score->scores, at<float>(ws, p.lse_aff),
-                   at<float>(ws, p.colsum), p.colsum_bytes, score->init, stream);
+                   at<float>(ws, p.colsum), p.colsum_bytes, score->init, stream, aff_done ? lse_aff : nullptr);
     if (st != ACACHE_OK) return st;
   }
   if (dims->dtype == ACACHE_BF16) {

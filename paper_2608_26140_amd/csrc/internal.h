@@ -97,10 +97,16 @@ hipError_t launch_kv_deviation(acache_dtype dt, const void* kp, const void* vp, 
 
 // ---- bf16 attention and scoring (k_attention.hip, k_score.hip)
 // part / part_bytes: optional fp32 space for key splits (null: one split)
+// lse_aff (nullable): also the natural-log log-sum-exp over each request's
+// keys [aff_begin, aff_begin + aff_len), written only where aff_begin is 0
+// (the running softmax's state once those keys are in), aff_len a multiple
+// of 64 and the launch takes one key split; *aff_done (nullable) tells
+// whether it was written.
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,
-                                 float* part, size_t part_bytes, hipStream_t s);
+                                 float* part, size_t part_bytes, hipStream_t s, float* lse_aff = nullptr,
+                                 int aff_begin = 0, int aff_len = 0, bool* aff_done = nullptr);
 // Decode-step attention: the queries of all requests against the shared
 // affix slots (each request's anchors masked out), then each request's
 // queries against its private slots, merged.  mask: [batch][ceil(L / 64)]

@@ -42,6 +42,11 @@ struct AttnArgs {
   int64_t n_slots;
   bf16* out;             // [rows, H * 128] (PV only)
   float* lse;            // [.., H] natural log; nullable for PV
+  // nullable (one key split only): [.., H] natural-log log-sum-exp over key
+  // tiles 0 .. aff_t1 - 1 of each request, the state of the running softmax
+  // once those tiles are in (the keys are visited in order)
+  float* lse_aff;
+  int aff_t1;
   int H, Hkv;
   int batch;
   int row_start[kMaxBatch + 1];
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   for (int d = 0; d < 4; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o_acc[d][r] = 0.f;
-  float m_run = -INFINITY, l_part = 0.f;
+  float m_run = -INFINITY, l_part = 0.f, lse_aff2 = 0.f;
   const float scale = kLog2e * rsqrtf((float)kDh);
   const int krow = key_perm(lane & 31);
   // K fragment byte offsets inside a tile for key block 0 (block 1: + 32 rows)
@@ -310,6 +315,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
         psum += e;
       }
     l_part += psum;
+    if (t + 1 == a.aff_t1) lse_aff2 = m_run + __log2f(l_part + __shfl_xor(l_part, 32));
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -352,6 +358,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
     return;
   }
   if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run + __log2f(l_tot)) * kLn2;
+  if (a.lse_aff && hl == 0) a.lse_aff[row * a.H + h] = lse_aff2 * kLn2;
   const float inv = 1.f / l_tot;
   bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
 #pragma unroll
@@ -647,11 +654,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
     for (int d = 0; d < 4; ++d)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o_acc[qb][d][r] = 0.f;
-  float m_run[QB], l_part[QB];
+  float m_run[QB], l_part[QB], lse_aff2[QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     m_run[qb] = -INFINITY;
     l_part[qb] = 0.f;
+    lse_aff2[qb] = 0.f;
   }
   // moves the running max of a block whose tile maximum exceeds it by more
   // than 2^8, rescaling what has been accumulated
@@ -774,6 +782,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       l_part[qb] += psum[qb];
+      if (t + 1 == a.aff_t1) lse_aff2[qb] = m_run[qb] + __log2f(l_part[qb] + __shfl_xor(l_part[qb], 32));
       mx[qb] = -INFINITY;
     }
 #pragma unroll
@@ -833,6 +842,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
       continue;
     }
     if (a.lse && hl == 0) a.lse[row * a.H + h] = (m_run[qb] + __log2f(l_tot)) * kLn2;
+    if (a.lse_aff && hl == 0) a.lse_aff[row * a.H + h] = lse_aff2[qb] * kLn2;
     const float inv = 1.f / l_tot;
     bf16* op = a.out + row * (int64_t)a.H * kDh + (int64_t)h * kDh;
 #pragma unroll
@@ -887,7 +897,12 @@ using WideQ = WideCfg<kWideQB, kWideWaves>;
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,
-                                 float* part, size_t part_bytes, hipStream_t s) {
+                                 float* part, size_t part_bytes, hipStream_t s, float* lse_aff, int aff_begin,
+                                 int aff_len, bool* aff_done) {
+  if (aff_done) *aff_done = false;
+  // the affix log-sum-exp rides along where the affix keys come first, in
+  // whole key tiles, and the launch takes one key split
+  const bool want_aff = lse_aff && aff_len > 0 && aff_begin == 0 && aff_len % kTileK == 0;
   PvArgs pa = {};
   AttnArgs& a = pa.a;
   a.q = (const bf16*)q;
@@ -935,8 +950,15 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   // each, no key splits (the merge kernel would cover every row)
   const double cost_split = (double)((full_w * H + 255) / 256) * max_kt * kWideTileCost +
                             (double)((rem_n * H + 511) / 512) * max_kt;
+  auto take_aff = [&]() {
+    if (!want_aff) return;
+    a.lse_aff = lse_aff;
+    a.aff_t1 = aff_len / kTileK;
+    if (aff_done) *aff_done = true;
+  };
   if (wide_ok && full_w * H >= 256 && rem_n > 0 && cost_split < std::min(cost_w, cost_n)) {
     pa.splits = 1;
+    take_aff();
     int acc = 0;
     for (int b = 0; b < rg.batch; ++b) {
       const int nr = a.row_start[b + 1] - a.row_start[b];
@@ -967,6 +989,7 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   }
   a.tile_start[rg.batch] = acc_tiles;
   pa.splits = splits;
+  if (splits == 1) take_aff();
   pa.part_o = part;
   pa.part_ml = part ? part + (size_t)splits * rows * H * kDh : nullptr;
   if (wide)

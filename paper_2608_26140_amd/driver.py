@@ -218,13 +218,16 @@ class AffixBatch:
         for k in self.k_pools:
             A.acache_rerotate_k(self.model.dims, k, slots, k, slots, d, stream=stream)
 
-    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None, outputs: bool = True, layer_hook=None):
+    def probe(self, norm: int = A.ACACHE_NORM_AFFIX, stream=None, outputs: bool = True, layer_hook=None,
+              attention_lse: bool = True):
         """One-shot probe (Section 3.2): forward the non-affix rows against the
         fixed shared affix cache and accumulate Eq. 5 over layers.  Returns
         (scores [B, L] fp32, x rows, maps).  outputs=False: the last layer
         computes only what its score reads (acache_layer_score), and the
         returned x is None.  layer_hook(n, x, scores): as run_layers', with
-        the score buffer (its sum over the layers before n)."""
+        the score buffer (its sum over the layers before n).  attention_lse:
+        let a layer's attention take the affix log-sum-exp for its score
+        (False: the score always makes its own pass over the affix keys)."""
         m = self.maps(None, 0, stream)
         x = self.gather_inputs(m, stream)
         # the first layer writes the scores (init) and the others add to them;
@@ -233,8 +236,13 @@ class AffixBatch:
             scores = torch.empty((self.B, self.L), dtype=torch.float32, device=self.device)
         else:
             scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
+        # with no anchors every request reads its affix keys, in order, through
+        # the shared slots from key index ab on: the attention may take their
+        # log-sum-exp for the score
         score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
                      affix_slots=self.affix_slots, scores=scores, norm=norm, init=int(self.G > 0))
+        if attention_lse:
+            score["affix_key_begin"] = self.ab
         hook = None if layer_hook is None else (lambda n, xx: layer_hook(n, xx, scores))
         self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream, layer_hook=hook)
         return scores, (x if outputs else None), m

@@ -157,6 +157,24 @@ def test_score_only_last_layer(case, norm):
         check_anchors(anchors[b], res.scores, K, e["max_abs"], f"{w.name} score-only request {b} ({norm})")
 
 
+def test_probe_affix_lse_from_attention(case):
+    """Affix-normalised probe scores whether the attention hands the score
+    each row's log-sum-exp over the affix keys (taken where the affix comes
+    first, in whole 64-key tiles: the LLaDA layer here) or the score makes
+    its own pass over them: both against the oracle and close to each other."""
+    from paper_2608_26140_amd import acache as A
+    w, s, layers, sk, sv, oc = case
+    dt = w.dims.dtype
+    with_lse, _, _ = s.batch.probe(A.ACACHE_NORM_AFFIX, attention_lse=True)
+    own, _, _ = s.batch.probe(A.ACACHE_NORM_AFFIX, attention_lse=False)
+    g, h = down(with_lse), down(own)
+    assert_close(g, h, dt, "attention log-sum-exp against the score's own")
+    for b in range(w.batch):
+        res = oc.probe(b, "affix")
+        assert_close(g[b], res.scores, dt, f"scores request {b} (attention log-sum-exp)")
+        assert_close(h[b], res.scores, dt, f"scores request {b} (score's own pass)")
+
+
 def test_score_init_writes(case):
     """init on the probe's first layer writes the scores instead of adding:
     a buffer full of NaN ends with the same bits as the accumulating path on
