@@ -68,8 +68,10 @@ def parse():
 def flops_model(w, K):
     """Algorithmic FLOPs of one step, by kernel (see the design notes):
     linear 2 * params / layer / row, attention 4 * S * H * d_h / row / layer,
-    probe scoring 2 sweeps * 2 * G * L * H * d_h / request / layer (timed as
-    score_colsum on the bf16 path, where both sweeps are one kernel)."""
+    probe scoring 2 * G * L * H * d_h / request / layer per sweep over the
+    affix keys: the column sums, and the log-sum-exp where the layer's
+    attention does not hand it over (timed as score_colsum on the bf16 path,
+    where both sweeps are one kernel)."""
     d = w.dims
     lay = w.layout
     B, S, L, G, N = w.batch, lay.seq_len, lay.affix_len, lay.mask_len, d.n_layers
@@ -91,13 +93,16 @@ def flops_model(w, K):
     # rows' queries (acache_layer_score under the affix-only normalisation)
     out["probe"] = {k: v * B * P * (N - 1) for k, v in per_row.items()}
     out["probe"]["gemm_qkv"] += 2 * d.d_model * hq * B * G
-    score = 2 * 2 * G * L * hq * B * N
+    sweep = 2 * G * L * hq * B
     if d.dtype == "bf16":
-        # one kernel: the log-sum-exp sweep and the column-sum sweep
-        out["probe"]["score_colsum"] = score
+        # one kernel: the column-sum sweep, and the log-sum-exp sweep except
+        # where the attention takes it (affix first in whole 64-key tiles:
+        # every probe layer but the last, which runs no attention)
+        lse_sweeps = 1 if lay.affix_begin == 0 and L % 64 == 0 else N
+        out["probe"]["score_colsum"] = sweep * (N + lse_sweeps)
     else:
-        out["probe"]["score_lse"] = score / 2
-        out["probe"]["score_colsum"] = score / 2
+        out["probe"]["score_lse"] = sweep * N
+        out["probe"]["score_colsum"] = sweep * N
     return out, rows
 
 

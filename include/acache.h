@@ -118,9 +118,9 @@ typedef struct {
                                  j < L.  Under ACACHE_NORM_AFFIX on the bf16 path the attention pass
                                  then also takes each row's log-sum-exp over those keys and the score
                                  uses it instead of its own pass over the affix keys (when
-                                 affix_key_begin is 0, L is a multiple of 64 and the attention needs
-                                 no key split; otherwise the score makes that pass itself).  Zero: no
-                                 such promise (any caller that leaves the field zeroed) */
+                                 affix_key_begin is 0 and L is a multiple of 64; otherwise the score
+                                 makes that pass itself).  Zero: no such promise (any caller that
+                                 leaves the field zeroed) */
   int32_t affix_key_begin;    /* with affix_keys_known: key index of the first affix key, >= 0, the same
                                  in every request; each request has at least affix_key_begin + L keys,
                                  or the promise is ignored */

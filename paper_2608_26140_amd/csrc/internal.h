@@ -99,9 +99,9 @@ hipError_t launch_kv_deviation(acache_dtype dt, const void* kp, const void* vp, 
 // part / part_bytes: optional fp32 space for key splits (null: one split)
 // lse_aff (nullable): also the natural-log log-sum-exp over each request's
 // keys [aff_begin, aff_begin + aff_len), written only where aff_begin is 0
-// (the running softmax's state once those keys are in), aff_len a multiple
-// of 64 and the launch takes one key split; *aff_done (nullable) tells
-// whether it was written.
+// (the running softmax's state once those keys are in) and aff_len is a
+// multiple of 64 (under key splits the merge kernel combines the splits'
+// shares); *aff_done (nullable) tells whether it was written.
 hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q,
                                  const int32_t* read_slots, const void* k_pool, const void* v_pool,
                                  int64_t pool_ld, int64_t n_slots, void* out, float* lse,

@@ -42,9 +42,10 @@ struct AttnArgs {
   int64_t n_slots;
   bf16* out;             // [rows, H * 128] (PV only)
   float* lse;            // [.., H] natural log; nullable for PV
-  // nullable (one key split only): [.., H] natural-log log-sum-exp over key
-  // tiles 0 .. aff_t1 - 1 of each request, the state of the running softmax
-  // once those tiles are in (the keys are visited in order)
+  // nullable: [.., H] natural-log log-sum-exp over key tiles 0 .. aff_t1 - 1
+  // of each request, the state of the running softmax once those tiles are
+  // in (the keys are visited in order).  Under key splits each split leaves
+  // its share in PvArgs::part_aff and the merge kernel combines them
   float* lse_aff;
   int aff_t1;
   int H, Hkv;
@@ -103,6 +104,9 @@ struct PvArgs {
   int splits;
   float* part_o;   // [splits][rows][H][128] unnormalised O (splits > 1)
   float* part_ml;  // [splits][rows][H][2] (running max in log2 units, sum)
+  // with lse_aff and splits > 1: [splits][rows][H], each split's log-sum-exp
+  // (log2 units) over its tiles below aff_t1, -inf for a split past them
+  float* part_aff;
   // decode passes: both write partials into one buffer of part_rows rows,
   // this launch's splits at indices split_base ..
   int partial;
@@ -226,7 +230,9 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
   for (int d = 0; d < 4; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o_acc[d][r] = 0.f;
-  float m_run = -INFINITY, l_part = 0.f, lse_aff2 = 0.f;
+  float m_run = -INFINITY, l_part = 0.f, lse_aff2 = -INFINITY;
+  // the affix tiles of this split end before tile aff_end (none if past them)
+  const int aff_end = min(a.aff_t1, t_hi);
   const float scale = kLog2e * rsqrtf((float)kDh);
   const int krow = key_perm(lane & 31);
   // K fragment byte offsets inside a tile for key block 0 (block 1: + 32 rows)
@@ -315,7 +321,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
         psum += e;
       }
     l_part += psum;
-    if (t + 1 == a.aff_t1) lse_aff2 = m_run + __log2f(l_part + __shfl_xor(l_part, 32));
+    if (t + 1 == aff_end) lse_aff2 = m_run + __log2f(l_part + __shfl_xor(l_part, 32));
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -354,6 +360,7 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
       float* pm = pa.part_ml + (((int64_t)psplit * prow + row) * a.H + h) * 2;
       pm[0] = m_run;
       pm[1] = l_tot;
+      if (pa.part_aff) pa.part_aff[((int64_t)psplit * prow + row) * a.H + h] = lse_aff2;
     }
     return;
   }
@@ -374,11 +381,14 @@ __global__ __launch_bounds__(kPvThreads, 2) void attention_pv_kernel(PvArgs pa) 
 
 // Combines the key splits of each (row, head): m = max_s m_s,
 // O = sum_s 2^(m_s - m) O_s / sum_s 2^(m_s - m) l_s.  32 threads per
-// (row, head), 4 dimensions each.
+// (row, head), 4 dimensions each.  With part_aff also the affix
+// log-sum-exp, log sum_s 2^(a_s) over the splits' shares a_s.
 __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __restrict__ part_o,
                                                               const float* __restrict__ part_ml, int splits,
                                                               int64_t rows, int H, bf16* __restrict__ out,
-                                                              float* __restrict__ lse) {
+                                                              float* __restrict__ lse,
+                                                              const float* __restrict__ part_aff,
+                                                              float* __restrict__ lse_aff) {
   const int64_t pair = (int64_t)blockIdx.x * 8 + (threadIdx.x >> 5);
   if (pair >= rows * H) return;
   const int c = (threadIdx.x & 31) * 4;
@@ -400,6 +410,16 @@ __global__ __launch_bounds__(256) void attention_merge_kernel(const float* __res
   for (int j = 0; j < 4; ++j) w[j] = (bf16)(o[j] * inv);
   *reinterpret_cast<bf16x4*>(out + pair * kDh + c) = w;
   if (lse && c == 0) lse[pair] = (m + __log2f(l)) * kLn2;
+  if (part_aff && c == 0) {
+    float ma = -INFINITY;
+    for (int s2 = 0; s2 < splits; ++s2) ma = fmaxf(ma, part_aff[(int64_t)s2 * rows * H + pair]);
+    float la = 0.f;
+    for (int s2 = 0; s2 < splits; ++s2) {
+      const float v = part_aff[(int64_t)s2 * rows * H + pair];
+      la += v == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(v - ma);
+    }
+    lse_aff[pair] = (ma + __log2f(la)) * kLn2;
+  }
 }
 
 
@@ -659,8 +679,9 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
   for (int qb = 0; qb < QB; ++qb) {
     m_run[qb] = -INFINITY;
     l_part[qb] = 0.f;
-    lse_aff2[qb] = 0.f;
+    lse_aff2[qb] = -INFINITY;
   }
+  const int aff_end = min(a.aff_t1, t_hi);
   // moves the running max of a block whose tile maximum exceeds it by more
   // than 2^8, rescaling what has been accumulated
   auto rescale = [&](const float (&mx)[QB]) {
@@ -782,7 +803,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       l_part[qb] += psum[qb];
-      if (t + 1 == a.aff_t1) lse_aff2[qb] = m_run[qb] + __log2f(l_part[qb] + __shfl_xor(l_part[qb], 32));
+      if (t + 1 == aff_end) lse_aff2[qb] = m_run[qb] + __log2f(l_part[qb] + __shfl_xor(l_part[qb], 32));
       mx[qb] = -INFINITY;
     }
 #pragma unroll
@@ -838,6 +859,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
         float* pm = pa.part_ml + (((int64_t)split * prow + row) * a.H + h) * 2;
         pm[0] = m_run[qb];
         pm[1] = l_tot;
+        if (pa.part_aff) pa.part_aff[((int64_t)split * prow + row) * a.H + h] = lse_aff2[qb];
       }
       continue;
     }
@@ -863,12 +885,12 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 // Key splits for the read-slot attention.  Cost in 64-key tiles of one
 // 128-query workgroup (about 1 us each): rounds of `slots` resident
 // workgroups times the tiles per split times the cost of one tile, plus the
-// merge traffic (each split's fp32 O and (m, l) written and read back at
-// about 4 TB/s).  The partials must fit in part_bytes.  Returns the splits;
-// *cost receives the estimate.
+// merge traffic (each split's fp32 O and (m, l), and extra_b more bytes per
+// (row, head), written and read back at about 4 TB/s).  The partials must
+// fit in part_bytes.  Returns the splits; *cost receives the estimate.
 static int attention_splits(int n_wg, int slots, double tile_cost, int n_kt, int64_t rows, int H,
-                            size_t part_bytes, double* cost) {
-  const int64_t per_split = rows * H * (kDh * 4 + 8);
+                            size_t part_bytes, int extra_b, double* cost) {
+  const int64_t per_split = rows * H * (kDh * 4 + 8 + extra_b);
   int best = 1;
   double best_cost = 1e30;
   for (int s = 1; s <= 8 && s <= n_kt; ++s) {
@@ -901,7 +923,8 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
                                  int aff_len, bool* aff_done) {
   if (aff_done) *aff_done = false;
   // the affix log-sum-exp rides along where the affix keys come first, in
-  // whole key tiles, and the launch takes one key split
+  // whole key tiles (under key splits through one more fp32 partial per
+  // split, row and head)
   const bool want_aff = lse_aff && aff_len > 0 && aff_begin == 0 && aff_len % kTileK == 0;
   PvArgs pa = {};
   AttnArgs& a = pa.a;
@@ -940,8 +963,9 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   if (tiles == 0) return hipSuccess;
   const size_t pbytes = part ? part_bytes : 0;
   double cost_n = 0.0, cost_w = 0.0;
-  const int splits_n = attention_splits(tiles * H, 512, 1.0, max_kt, rows, H, pbytes, &cost_n);
-  const int splits_w = attention_splits(tiles_w * H, 256, kWideTileCost, max_kt, rows, H, pbytes, &cost_w);
+  const int aff_b = want_aff ? 4 : 0;
+  const int splits_n = attention_splits(tiles * H, 512, 1.0, max_kt, rows, H, pbytes, aff_b, &cost_n);
+  const int splits_w = attention_splits(tiles_w * H, 256, kWideTileCost, max_kt, rows, H, pbytes, aff_b, &cost_w);
   const bool wide_ok = (uint64_t)n_slots * (uint64_t)pool_ld * 2u <= (uint64_t)kWdAbsent;
   // the wide kernel only where its workgroups fill at least one round of CUs
   const bool wide = wide_ok && cost_w < cost_n && tiles_w * H * splits_w >= 256;
@@ -989,9 +1013,10 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   }
   a.tile_start[rg.batch] = acc_tiles;
   pa.splits = splits;
-  if (splits == 1) take_aff();
+  take_aff();
   pa.part_o = part;
   pa.part_ml = part ? part + (size_t)splits * rows * H * kDh : nullptr;
+  if (splits > 1 && a.lse_aff) pa.part_aff = pa.part_ml + (size_t)splits * rows * H * 2;
   if (wide)
     hipLaunchKernelGGL((attention_wide_kernel<kWideQB, kWideWaves>), dim3(acc_tiles * H * splits),
                        dim3(WideQ::kThreads), 0, s, pa);
@@ -1000,7 +1025,8 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   if (splits > 1) {
     const int64_t pairs = rows * H;
     hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s,
-                       (const float*)pa.part_o, (const float*)pa.part_ml, splits, rows, H, (bf16*)out, lse);
+                       (const float*)pa.part_o, (const float*)pa.part_ml, splits, rows, H, (bf16*)out, lse,
+                       (const float*)pa.part_aff, pa.part_aff ? lse_aff : nullptr);
   }
   return hipGetLastError();
 }
@@ -1045,7 +1071,7 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
   const int sp_priv = 1;
   double cost_unused = 0.0;
   const int sp_shared = shared ? attention_splits(q_tiles_all * H, 512, 1.0, n_kt_shared, rows, H,
-                                                  part_bytes - (size_t)per_split * sp_priv, &cost_unused)
+                                                  part_bytes - (size_t)per_split * sp_priv, 0, &cost_unused)
                                : 0;
   const int total = sp_shared + sp_priv;
 
@@ -1114,7 +1140,8 @@ hipError_t launch_attention_decode_bf16(int batch, int rows_per_req, int H, int 
   }
   const int64_t pairs = rows * H;
   hipLaunchKernelGGL(attention_merge_kernel, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s, (const float*)part,
-                     (const float*)(part + (size_t)total * rows * H * kDh), total, rows, H, (bf16*)out, nullptr);
+                     (const float*)(part + (size_t)total * rows * H * kDh), total, rows, H, (bf16*)out, nullptr,
+                     nullptr, nullptr);
   return hipGetLastError();
 }
 

@@ -16,7 +16,7 @@ from tests.oracle_side import anchor_count, rows_selective, check_anchors, oracl
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["tiny-f32", "llada-layer", "mini-stack", "mini-gqa-infix", "mini-f32-stack"]
+NAMES = ["tiny-f32", "llada-layer", "mini-stack", "mini-affix64", "mini-gqa-infix", "mini-f32-stack"]
 
 
 def storage_round(a: np.ndarray, dtype: str) -> np.ndarray:
@@ -160,8 +160,10 @@ def test_score_only_last_layer(case, norm):
 def test_probe_affix_lse_from_attention(case):
     """Affix-normalised probe scores whether the attention hands the score
     each row's log-sum-exp over the affix keys (taken where the affix comes
-    first, in whole 64-key tiles: the LLaDA layer here) or the score makes
-    its own pass over them: both against the oracle and close to each other."""
+    first, in whole 64-key tiles: the LLaDA layer and mini-affix64, whose
+    small probe grids split the attention's keys, so the splits' shares go
+    through the merge) or the score makes its own pass over them: both
+    against the oracle and close to each other."""
     from paper_2608_26140_amd import acache as A
     w, s, layers, sk, sv, oc = case
     dt = w.dims.dtype

@@ -136,6 +136,14 @@ TEST_CONFIGS: Dict[str, Workload] = {
                        dtype="bf16", vocab=1000),
         layout=SeqLayout(seq_len=330, affix_begin=0, affix_len=250, mask_begin=298, mask_len=32),
         batch=3, ratio=0.2, stale="donor"),
+    # prefix affix of whole 64-key tiles (the probe's attention hands the
+    # score its affix log-sum-exp, here under key splits)
+    "mini-affix64": Workload(
+        name="mini-affix64", seed_id=15,
+        dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=2, head_dim=128, d_ff=1024, n_layers=3,
+                       dtype="bf16", vocab=1000),
+        layout=SeqLayout(seq_len=336, affix_begin=0, affix_len=256, mask_begin=304, mask_len=32),
+        batch=3, ratio=0.2, stale="donor"),
     "mini-gqa-infix": Workload(
         name="mini-gqa-infix", seed_id=12,
         dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ff=768, n_layers=2,
