@@ -3,6 +3,7 @@
     python profile_summary.py stats   RUN_DIR NAME BENCH_JSON OUT_TXT "COMMAND" [--steps N]
     python profile_summary.py traffic FETCH_CSV WRITE_CSV COPY_FETCH_CSV COPY_WRITE_CSV WORKLOAD OUT_TXT \
                                       "STEP_COMMAND" "COPY_COMMAND" [--steps N] [--copy-mib M]
+    python profile_summary.py mfma    PMC_CSV WORKLOAD OUT_TXT "COMMAND" [--steps N]
 
 stats: the kernel statistics of a `rocprofv3 --kernel-trace --stats` run
 (RUN_DIR/NAME_kernel_stats.csv), and, from its kernel trace, the mean
@@ -15,6 +16,11 @@ counters read for the row-gather kernel copying M MiB (bench.py
 --copy-calibration M); written to profiles/traffic.json (keyed by workload
 and operation, with the digest of the kernel sources they were taken on)
 and OUT_TXT.
+
+mfma: the matrix units' activity per kernel over the last N steps from one
+`--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_INSTS_VALU_MFMA_MOPS_BF16`
+pass: the share of cycles in which a SIMD's matrix unit is busy, the clock
+the dispatch ran at, and the hardware-counted MFMA work.
 
 A step holds one top-K launch, between its probe and its refresh.  The
 run's last N steps are taken as the span from the launch after the
@@ -52,8 +58,24 @@ OPERATIONS = {
 BENCH_KERNEL = {"gemm_gate_up": "gemm_gate_up", "gemm_qkv": "gemm_qkv", "attention": "attention"}
 
 
+def _unmangled(name: str) -> str:
+    """The last component of a mangled nested name (_ZN <len><id>... E), for
+    the few rows the profiler leaves mangled."""
+    if not name.startswith("_ZN"):
+        return name
+    i, last = 3, name
+    while i < len(name) and name[i].isdigit():
+        j = i
+        while name[j].isdigit():
+            j += 1
+        n = int(name[i:j])
+        last, i = name[j:j + n], j + n
+    return last
+
+
 def short(name: str) -> str:
-    n = name.replace("acache::(anonymous namespace)::", "").replace("acache::", "").replace("void ", "")
+    n = _unmangled(name)
+    n = n.replace("acache::(anonymous namespace)::", "").replace("acache::", "").replace("void ", "")
     return re.sub(r"\(.*\)$", "", n)[:90]
 
 
@@ -122,6 +144,53 @@ def stats(argv):
     print("\n".join(lines[:40]))
 
 
+SIMDS = 1024  # 256 CUs x 4 SIMDs
+XCDS = 8
+
+
+def mfma(argv):
+    csv_path, workload, out, cmd = argv[:4]
+    steps = int(argv[argv.index("--steps") + 1]) if "--steps" in argv else 1
+    per = {}  # dispatch -> (kernel, duration ns, {counter: value})
+    for r in _rows(csv_path):
+        d = int(r["Dispatch_Id"])
+        if d not in per:
+            per[d] = (r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]), {})
+        per[d][2][r["Counter_Name"]] = per[d][2].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    order = [{"Kernel_Name": per[d][0], "d": d} for d in sorted(per)]
+    seg = _segment(order, steps)
+    agg, names = {}, []
+    for r in seg:
+        k = short(r["Kernel_Name"])
+        _, dur, c = per[r["d"]]
+        if k not in agg:
+            agg[k] = [0, 0.0, 0.0, 0.0, 0.0]
+            names.append(k)
+        a = agg[k]
+        a[0] += 1
+        a[1] += dur
+        a[2] += c.get("GRBM_GUI_ACTIVE", 0.0)
+        a[3] += c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        a[4] += c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0)
+    lines = [f"# MFMA activity per kernel: {workload} step (rocprofv3 SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE,",
+             "# SQ_INSTS_VALU_MFMA_MOPS_BF16)", "", "command (from the repository root on the GPU box):", f"  {cmd}", "",
+             f"Dispatches of the last {steps} step(s).  GRBM_GUI_ACTIVE per dispatch is summed over the {XCDS} XCDs:",
+             f"divided by {XCDS} and by the dispatch's duration it gives the clock.  MFMA busy =",
+             f"SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / {XCDS} x {SIMDS} SIMDs): the share of cycles in which a",
+             "SIMD's matrix unit is busy.  MFMA GFLOP = MOPS x 512 (hardware-counted, padded rows included).", "",
+             f"{'kernel':60s} {'calls':>6s} {'avg_us':>9s} {'clock GHz':>9s} {'MFMA busy':>9s} {'MFMA GFLOP':>10s} "
+             f"{'TFLOP/s':>8s}"]
+    for k in sorted(names, key=lambda n: -agg[n][1]):
+        n, dur, grbm, busy, mops = agg[k]
+        cyc = grbm / XCDS
+        lines.append(f"{k[:60]:60s} {n:6d} {dur / n / 1e3:9.1f} {cyc / dur if dur else 0:9.2f} "
+                     f"{100 * busy / (cyc * SIMDS) if cyc else 0:8.1f}% {mops * 512 / 1e9 / n:10.1f} "
+                     f"{mops * 512 / dur / 1e3 if dur else 0:8.0f}")
+    lines += ["", "Short launches read a higher clock: the counting window is longer than the kernel."]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def traffic(argv):
     fetch, write, cfetch, cwrite, workload, out, step_cmd, copy_cmd = argv[:8]
     steps = int(argv[argv.index("--steps") + 1]) if "--steps" in argv else 1
@@ -179,4 +248,4 @@ def traffic(argv):
 
 
 if __name__ == "__main__":
-    {"stats": stats, "traffic": traffic}[sys.argv[1]](sys.argv[2:])
+    {"stats": stats, "traffic": traffic, "mfma": mfma}[sys.argv[1]](sys.argv[2:])
