@@ -138,8 +138,10 @@ def test_rmsnorm(A, dtype, d):
 # stream-K over 32 tiles; (512, 32768, 256) T = 256, data-parallel;
 # (300, 4096, 128) nk = 2, too short for stream-K; (1280, 16384, 64) T = 320
 # and (2304, 8192, 128) T = 288, two data-parallel rounds of one or two K
-# steps, so a workgroup's second tile starts right behind its first tile's
-# stores; the rest run data-parallel by the cost model.
+# steps, the second partial, on 256 persistent workgroups, so a workgroup's
+# second tile starts right behind its first tile's stores (so does
+# (520, 24576, 2048) without a workspace); the rest run data-parallel by the
+# cost model.
 @pytest.mark.parametrize("schedule", ["dp", "sk"])
 @pytest.mark.parametrize("M,N,K", [(1, 256, 64), (77, 512, 256), (128, 256, 4096), (717, 768, 1024), (300, 4096, 128),
                                    (256, 3072, 4096), (520, 24576, 2048), (512, 32768, 256), (1280, 16384, 64),
