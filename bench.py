@@ -96,9 +96,10 @@ def flops_model(w, K):
     sweep = 2 * G * L * hq * B
     if d.dtype == "bf16":
         # one kernel: the column-sum sweep, and the log-sum-exp sweep except
-        # where the attention takes it (affix first in whole 64-key tiles:
-        # every probe layer but the last, which runs no attention)
-        lse_sweeps = 1 if lay.affix_begin == 0 and L % 64 == 0 else N
+        # where the attention takes it (the probe reads the affix keys first;
+        # whole 64-key tiles: every probe layer but the last, which runs no
+        # attention)
+        lse_sweeps = 1 if L % 64 == 0 else N
         out["probe"]["score_colsum"] = sweep * (N + lse_sweeps)
     else:
         out["probe"]["score_lse"] = sweep * N

@@ -136,6 +136,11 @@ typedef struct {
   int32_t shared_base;    /* pool slot of affix-local index 0 (shared region) */
   int32_t private_base;   /* first private slot */
   int32_t private_stride; /* request b's private slots start at private_base + b * private_stride */
+  int32_t key_order;      /* order of a request's keys in read_slots: 0, logical positions 0 .. S-1;
+                             1, the L affix positions first (affix-local order), then the others in
+                             logical order.  Attention over a request's keys does not depend on their
+                             order; the probe reads the affix first so that its attention pass can
+                             take the affix log-sum-exp of Eq. 4 (acache_score_args) */
 } acache_layout;
 
 /* ---------------------------------------------------------------------------
@@ -229,8 +234,9 @@ acache_status acache_kv_scatter(const void* k_src, const void* v_src, int64_t sr
  *   row_pos     [B*R]  logical position of each recomputed row
  *   row_src     [B*R]  b*S + position (index into per-position inputs)
  *   write_slots [B*R]  private slot of each recomputed row
- *   read_slots  [B*S]  slot each logical position is read from: its
- *                      private slot if recomputed, else shared_base + (p - affix_begin)
+ *   read_slots  [B*S]  slot each key is read from, keys in the layout's key_order
+ *                      (key_order 0: key p is logical position p): its private slot
+ *                      if recomputed, else shared_base + (p - affix_begin)
  *   q_rows      [B*G]  (nullable) row of each masked position
  * anchors [B, k] affix-local indices, ascending per request (NULL iff k == 0).
  * k == 0 gives the probe / direct-reuse maps, k == L the full-recompute maps.

@@ -51,7 +51,7 @@ class ScoreArgs(ctypes.Structure):
 
 class Layout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("seq_len", "affix_begin", "affix_len", "mask_begin", "mask_len",
-                                              "shared_base", "private_base", "private_stride")]
+                                              "shared_base", "private_base", "private_stride", "key_order")]
 
 
 class Paging(ctypes.Structure):

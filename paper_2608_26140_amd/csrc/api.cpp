@@ -394,6 +394,7 @@ static acache_status check_layout(const acache_layout* lay, int32_t batch, int32
   CHECK(lay->mask_len == 0 || lay->mask_begin + lay->mask_len <= ab || lay->mask_begin >= ab + L,
         ACACHE_ERR_SHAPE);  // the masked span is not part of the affix
   CHECK((int64_t)batch * S < (int64_t)1 << 31, ACACHE_ERR_SHAPE);
+  CHECK(lay->key_order == 0 || lay->key_order == 1, ACACHE_ERR_UNSUPPORTED);
   return ACACHE_OK;
 }
 
@@ -421,14 +422,9 @@ acache_status acache_build_maps(const acache_layout* lay, int32_t batch, const i
                                 int32_t k, int32_t* row_pos, int32_t* row_src,
                                 int32_t* write_slots, int32_t* read_slots, int32_t* q_rows,
                                 hipStream_t stream) {
-  CHECK(lay, ACACHE_ERR_NULL);
-  const int S = lay->seq_len, ab = lay->affix_begin, L = lay->affix_len;
-  CHECK(batch >= 0 && S >= 0 && L >= 0 && ab >= 0 && ab + L <= S, ACACHE_ERR_SHAPE);
-  CHECK(k >= 0 && k <= L, ACACHE_ERR_SHAPE);
-  CHECK(lay->mask_len >= 0 && lay->mask_begin >= 0 && lay->mask_begin + lay->mask_len <= S,
-        ACACHE_ERR_SHAPE);
-  CHECK(lay->mask_len == 0 || lay->mask_begin + lay->mask_len <= ab || lay->mask_begin >= ab + L,
-        ACACHE_ERR_SHAPE);  // the masked span is not part of the affix
+  acache_status st = check_layout(lay, batch, k);
+  if (st != ACACHE_OK) return st;
+  const int S = lay->seq_len, L = lay->affix_len;
   const int R = k + S - L;
   CHECK(lay->private_stride >= R && lay->private_base >= 0 && lay->shared_base >= 0, ACACHE_ERR_SHAPE);
   CHECK((int64_t)lay->private_base + (int64_t)batch * lay->private_stride < (int64_t)1 << 31,

@@ -111,7 +111,10 @@ __global__ __launch_bounds__(256) void build_maps_kernel(acache_layout lay, acac
   } else {
     slot = pg.block_size > 0 ? paged_slot(pg.shared_blocks, pg.block_size, p - ab) : lay.shared_base + (p - ab);
   }
-  rslots[t] = slot;
+  // key index of position p: p, or with the affix first p - ab inside the
+  // affix, L + p before it and p after it
+  const int key = lay.key_order == 0 ? p : (p >= ab && p < ae) ? p - ab : p < ab ? L + p : p;
+  rslots[(int64_t)b * S + key] = slot;
 }
 
 // ---------------------------------------------------------------- RMSNorm

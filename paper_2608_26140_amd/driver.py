@@ -140,11 +140,17 @@ class AffixBatch:
     def rows_per_request(self, k: int) -> int:
         return k + self.S - self.L
 
-    def maps(self, anchors: Optional[torch.Tensor], k: int, stream=None) -> dict:
+    def maps(self, anchors: Optional[torch.Tensor], k: int, stream=None, key_order: int = 0) -> dict:
+        """key_order 1: each request's read slots list the affix keys first
+        (the probe's order; see acache_layout.key_order)."""
+        lay = self.layout
+        if key_order:
+            lay = A.Layout(*[getattr(lay, n) for n, _ in A.Layout._fields_])
+            lay.key_order = key_order
         if self.pages is None:
-            return A.acache_build_maps(self.layout, self.B, anchors, k, self.device, stream)
+            return A.acache_build_maps(lay, self.B, anchors, k, self.device, stream)
         tbl, nb = self.private_table(self.rows_per_request(k))
-        return A.acache_build_maps_paged(self.layout, self.B, anchors, k, self.bs, self.shared_blocks, tbl, nb,
+        return A.acache_build_maps_paged(lay, self.B, anchors, k, self.bs, self.shared_blocks, tbl, nb,
                                          self.device, stream)
 
     def gather_inputs(self, m: dict, stream=None) -> torch.Tensor:
@@ -226,9 +232,10 @@ class AffixBatch:
         computes only what its score reads (acache_layer_score), and the
         returned x is None.  layer_hook(n, x, scores): as run_layers', with
         the score buffer (its sum over the layers before n).  attention_lse:
-        let a layer's attention take the affix log-sum-exp for its score
-        (False: the score always makes its own pass over the affix keys)."""
-        m = self.maps(None, 0, stream)
+        the keys are read affix first, so that a layer's attention takes the
+        affix log-sum-exp for its score (False: keys in logical order, and
+        the score makes its own pass over the affix keys)."""
+        m = self.maps(None, 0, stream, key_order=1 if attention_lse else 0)
         x = self.gather_inputs(m, stream)
         # the first layer writes the scores (init) and the others add to them;
         # with no masked rows no layer scores, and they stay zero
@@ -236,13 +243,13 @@ class AffixBatch:
             scores = torch.empty((self.B, self.L), dtype=torch.float32, device=self.device)
         else:
             scores = torch.zeros((self.B, self.L), dtype=torch.float32, device=self.device)
-        # with no anchors every request reads its affix keys, in order, through
-        # the shared slots from key index ab on: the attention may take their
-        # log-sum-exp for the score
+        # with no anchors and the affix first, every request reads its affix
+        # keys, in order, through the shared slots from key index 0: the
+        # attention may take their log-sum-exp for the score
         score = dict(q_rows=m["q_rows"], cu_q=[b * self.G for b in range(self.B + 1)],
                      affix_slots=self.affix_slots, scores=scores, norm=norm, init=int(self.G > 0))
         if attention_lse:
-            score["affix_key_begin"] = self.ab
+            score["affix_key_begin"] = 0
         hook = None if layer_hook is None else (lambda n, xx: layer_hook(n, xx, scores))
         self.run_layers(x, m, 0, score=score, score_last_only=not outputs, stream=stream, layer_hook=hook)
         return scores, (x if outputs else None), m

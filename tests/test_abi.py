@@ -84,6 +84,10 @@ def test_host_validation_enqueues_nothing(A):
     lay_ovl = A.Layout(100, 0, 60, 50, 20, 0, 60, 100)
     assert lib.acache_build_maps(ctypes.byref(lay_ovl), 1, None, 0, ctypes.c_void_p(16), ctypes.c_void_p(16),
                                  ctypes.c_void_p(16), ctypes.c_void_p(16), None, None) == 2
+    # maps: unknown key order
+    lay_ord = A.Layout(100, 0, 60, 80, 20, 0, 60, 100, 2)
+    assert lib.acache_build_maps(ctypes.byref(lay_ord), 1, None, 0, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                                 ctypes.c_void_p(16), ctypes.c_void_p(16), None, None) == 4
 
 
 def test_layer_recompute_validation(A):

@@ -89,16 +89,25 @@ def test_kv_scatter(A, dtype):
 
 # ----------------------------------------------------------------------------- maps (Section 4.1)
 
+def affix_first(read_slots, B, S, ab, L):
+    """Read slots in logical order -> the affix keys first (key_order 1)."""
+    order = np.concatenate([np.arange(ab, ab + L), np.arange(ab), np.arange(ab + L, S)])
+    return np.asarray(read_slots).reshape(B, S)[:, order].reshape(-1)
+
+
 @pytest.mark.parametrize("layout,B,k", [((1536, 0, 1024, 1280, 256), 1, 205), ((192, 0, 128, 160, 32), 1, 26),
                                         ((5120, 512, 4096, 4864, 256), 4, 819), ((2432, 0, 2048, 2176, 256), 8, 0),
                                         ((2432, 0, 2048, 2176, 256), 3, 2048)])
-def test_build_maps(A, layout, B, k):
+@pytest.mark.parametrize("key_order", [0, 1])
+def test_build_maps(A, layout, B, k, key_order):
     S, ab, L, mb, G = layout
     anchors = np.stack([np.sort(W.draw_permutation(L, seed=b)[:k]) for b in range(B)]).astype(np.int32)
     R = k + S - L
-    lay = A.Layout(S, ab, L, mb, G, 0, L, S)
+    lay = A.Layout(S, ab, L, mb, G, 0, L, S, key_order)
     got = A.acache_build_maps(lay, B, up_i32(anchors) if k else None, k)
-    ref = O.build_maps(S, ab, L, mb, G, anchors, 0, L, S)
+    ref = list(O.build_maps(S, ab, L, mb, G, anchors, 0, L, S))
+    if key_order:
+        ref[3] = affix_first(ref[3], B, S, ab, L)
     for name, r in zip(["row_pos", "row_src", "write_slots", "read_slots", "q_rows"], ref):
         np.testing.assert_array_equal(got[name].cpu().numpy(), r, err_msg=name)
     assert got["row_pos"].numel() == B * R
@@ -106,16 +115,19 @@ def test_build_maps(A, layout, B, k):
 
 @pytest.mark.parametrize("layout,B,k,bs", [((192, 0, 128, 160, 32), 3, 26, 16), ((5120, 512, 4096, 4864, 256), 4, 819, 256),
                                            ((2432, 0, 2048, 2176, 256), 2, 0, 100), ((300, 40, 200, 260, 40), 2, 200, 1)])
-def test_build_maps_paged(A, layout, B, k, bs):
+@pytest.mark.parametrize("key_order", [0, 1])
+def test_build_maps_paged(A, layout, B, k, bs, key_order):
     S, ab, L, mb, G = layout
     anchors = np.stack([np.sort(W.draw_permutation(L, seed=b)[:k]) for b in range(B)]).astype(np.int32)
     R = k + S - L
     n_sh, nb = -(-L // bs), -(-R // bs) + 1          # one spare block per request
     ids = W.draw_permutation(n_sh + B * nb, seed=30 + bs)
     shared, private = ids[:n_sh], ids[n_sh:]
-    lay = A.Layout(S, ab, L, mb, G, 0, 0, 0)
+    lay = A.Layout(S, ab, L, mb, G, 0, 0, 0, key_order)
     got = A.acache_build_maps_paged(lay, B, up_i32(anchors) if k else None, k, bs, up_i32(shared), up_i32(private), nb)
-    ref = O.build_maps_paged(S, ab, L, mb, G, anchors, bs, shared, private, nb)
+    ref = list(O.build_maps_paged(S, ab, L, mb, G, anchors, bs, shared, private, nb))
+    if key_order:
+        ref[3] = affix_first(ref[3], B, S, ab, L)
     for name, r in zip(["row_pos", "row_src", "write_slots", "read_slots", "q_rows"], ref):
         np.testing.assert_array_equal(got[name].cpu().numpy(), r, err_msg=name)
 

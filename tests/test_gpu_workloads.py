@@ -16,7 +16,7 @@ from tests.oracle_side import anchor_count, rows_selective, check_anchors, oracl
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["tiny-f32", "llada-layer", "mini-stack", "mini-affix64", "mini-gqa-infix", "mini-f32-stack"]
+NAMES = ["tiny-f32", "llada-layer", "mini-stack", "mini-affix64", "mini-infix64", "mini-gqa-infix", "mini-f32-stack"]
 
 
 def storage_round(a: np.ndarray, dtype: str) -> np.ndarray:
@@ -159,11 +159,12 @@ def test_score_only_last_layer(case, norm):
 
 def test_probe_affix_lse_from_attention(case):
     """Affix-normalised probe scores whether the attention hands the score
-    each row's log-sum-exp over the affix keys (taken where the affix comes
-    first, in whole 64-key tiles: the LLaDA layer and mini-affix64, whose
-    small probe grids split the attention's keys, so the splits' shares go
-    through the merge) or the score makes its own pass over them: both
-    against the oracle and close to each other."""
+    each row's log-sum-exp over the affix keys (the probe reads the affix
+    keys first; taken where the affix is whole 64-key tiles: the LLaDA layer,
+    mini-affix64 and the infix mini-infix64, whose small probe grids split
+    the attention's keys, so the splits' shares go through the merge) or the
+    score makes its own pass over them, keys in logical order: both against
+    the oracle and close to each other."""
     from paper_2608_26140_amd import acache as A
     w, s, layers, sk, sv, oc = case
     dt = w.dims.dtype
@@ -271,12 +272,19 @@ def test_ratio_one_equals_full_and_ignores_stale(case):
 
 def test_ratio_zero_equals_direct_reuse(case):
     """Anchor ratio 0 is direct reuse: the rows and outputs of the probe
-    forward (scoring does not change them)."""
+    forward (scoring does not change them).  Bit for bit with the keys in
+    logical order; the probe's own order (affix keys first) changes only the
+    attention's summation order."""
     w, s, layers, sk, sv, oc = case
     x0, _ = s.batch.refresh(None, 0)
     g0 = down_bits(x0)
-    _, x_probe, _ = s.batch.probe()
+    _, x_probe, _ = s.batch.probe(attention_lse=False)
     np.testing.assert_array_equal(g0, down_bits(x_probe))
+    _, x_first, _ = s.batch.probe()
+    if w.layout.affix_begin == 0:
+        np.testing.assert_array_equal(g0, down_bits(x_first))
+    else:
+        assert_close(down(x_first), down(x0), w.dims.dtype, "probe rows, affix keys first")
     x1, _ = s.batch.direct_reuse()
     np.testing.assert_array_equal(g0, down_bits(x1))
 

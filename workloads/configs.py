@@ -144,6 +144,13 @@ TEST_CONFIGS: Dict[str, Workload] = {
                        dtype="bf16", vocab=1000),
         layout=SeqLayout(seq_len=336, affix_begin=0, affix_len=256, mask_begin=304, mask_len=32),
         batch=3, ratio=0.2, stale="donor"),
+    # infix affix of whole 64-key tiles (the probe reads the affix keys first)
+    "mini-infix64": Workload(
+        name="mini-infix64", seed_id=16,
+        dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ff=768, n_layers=3,
+                       dtype="bf16", vocab=1000),
+        layout=SeqLayout(seq_len=320, affix_begin=64, affix_len=192, mask_begin=288, mask_len=32),
+        batch=2, ratio=0.25, stale="donor"),
     "mini-gqa-infix": Workload(
         name="mini-gqa-infix", seed_id=12,
         dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ff=768, n_layers=2,
