@@ -151,6 +151,13 @@ TEST_CONFIGS: Dict[str, Workload] = {
                        dtype="bf16", vocab=1000),
         layout=SeqLayout(seq_len=320, affix_begin=64, affix_len=192, mask_begin=288, mask_len=32),
         batch=2, ratio=0.25, stale="donor"),
+    # four requests of 256 probe rows over 4352 keys, LLaDA-shaped: the probe's
+    # attention takes the 256-query kernel with two key splits
+    "probe-wide-split": Workload(
+        name="probe-wide-split", seed_id=17,
+        dims=ModelDims(n_layers=2, dtype="bf16", vocab=1024, **LLADA),
+        layout=SeqLayout(seq_len=4352, affix_begin=0, affix_len=4096, mask_begin=4224, mask_len=128),
+        batch=4, ratio=0.2, stale="donor"),
     "mini-gqa-infix": Workload(
         name="mini-gqa-infix", seed_id=12,
         dims=ModelDims(d_model=512, n_heads=4, n_kv_heads=1, head_dim=128, d_ff=768, n_layers=2,
