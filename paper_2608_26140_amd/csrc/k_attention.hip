@@ -886,7 +886,7 @@ __global__ __launch_bounds__(64 * WAVES, 1) void attention_wide_kernel(PvArgs pa
 // 128-query workgroup (about 1 us each): rounds of `slots` resident
 // workgroups times the tiles per split times the cost of one tile, plus the
 // merge traffic (each split's fp32 O and (m, l), and extra_b more bytes per
-// (row, head), written and read back at about 4 TB/s).  The partials must
+// (row, head), written and read back at about 6 TB/s).  The partials must
 // fit in part_bytes.  Returns the splits; *cost receives the estimate.
 static int attention_splits(int n_wg, int slots, double tile_cost, int n_kt, int64_t rows, int H,
                             size_t part_bytes, int extra_b, double* cost) {
@@ -897,8 +897,8 @@ static int attention_splits(int n_wg, int slots, double tile_cost, int n_kt, int
     if (s > 1 && (size_t)(per_split * s) > part_bytes) break;
     const double rounds = (double)((n_wg * s + slots - 1) / slots);
     const double tiles = (double)((n_kt + s - 1) / s);
-    // merge: 2 x per_split x s bytes at ~4 TB/s, one 64-key tile of a workgroup ~1 us
-    const double merge = s > 1 ? 2.0 * per_split * s / 4e12 / 1e-6 : 0.0;
+    // merge: 2 x per_split x s bytes at ~6 TB/s, one 64-key tile of a workgroup ~1 us
+    const double merge = s > 1 ? 2.0 * per_split * s / 6e12 / 1e-6 : 0.0;
     const double c = rounds * tiles * tile_cost + merge;
     if (c < best_cost) {
       best_cost = c;
@@ -967,8 +967,10 @@ hipError_t launch_attention_bf16(const Ragged& rg, int H, int Hkv, const void* q
   const int splits_n = attention_splits(tiles * H, 512, 1.0, max_kt, rows, H, pbytes, aff_b, &cost_n);
   const int splits_w = attention_splits(tiles_w * H, 256, kWideTileCost, max_kt, rows, H, pbytes, aff_b, &cost_w);
   const bool wide_ok = (uint64_t)n_slots * (uint64_t)pool_ld * 2u <= (uint64_t)kWdAbsent;
-  // the wide kernel only where its workgroups fill at least one round of CUs
-  const bool wide = wide_ok && cost_w < cost_n && tiles_w * H * splits_w >= 256;
+  // the wide kernel wherever the cost model prefers it, below one round of
+  // CUs too (C2's refresh: 96 query tiles x 2 key splits, attention 10%
+  // faster than the 128-query kernel's 384 workgroups)
+  const bool wide = wide_ok && cost_w < cost_n;
   // split: each request's whole 256-row tiles on the wide kernel and its
   // last partial tile (in 128-row tiles) on the two-per-CU kernel, one launch
   // each, no key splits (the merge kernel would cover every row)
